@@ -1,0 +1,404 @@
+"""Plain, slow, obviously correct CPU oracle of the Taliesin hot path.
+
+TEST INFRASTRUCTURE ONLY: imported by tests/, by __graft_entry__.smoke() and by
+the benchmark's CPU-baseline leg, never by the product package.
+
+What the paper fixes (Sec. 2.1 Deployment, Sec. 2.2 Taliesin, Sec. 3
+Correctness, Sec. 5 Design boundaries):
+  * stored KV state is named by a fingerprint of the exact input bytes, the
+    model and the tenant; no identity, no service (Sec. 2.1, Sec. 2.2);
+  * reuse is per block, only where token positions match exactly (Sec. 2.2,
+    Sec. 5 first item);
+  * state is checked on load; a missing, damaged or failing record is
+    recomputed -- serve without memory, never with wrong memory (Sec. 2.2,
+    Sec. 5 second item);
+  * a restored block is bit-identical to the saved one (Sec. 3, Table 1);
+  * load-time verification is by byte comparison and cryptographic hashes
+    (Sec. 3 sabotage testing; Sec. 7 relation to the compute ceiling).
+The paper withholds the storage format (Sec. 1, last paragraph of the
+contributions), so the record layout, the key chain and the tree-mode
+checksum below are this project's readings; the design doc lists each one.
+
+Library primitives used as steps: hashlib.sha256 (FIPS 180-4) and
+xxhash.xxh64 (the published XXH64 algorithm). Both are pinned by known-answer
+vectors in tests/golden.
+
+Everything here is sequential Python/numpy over bytes: no blocking, no fusion,
+no reordering beyond what the definitions state.
+"""
+from __future__ import annotations
+
+import hashlib
+import struct
+from dataclasses import dataclass
+from typing import List, Optional, Sequence, Tuple
+
+import numpy as np
+import xxhash
+
+MASK64 = (1 << 64) - 1
+
+# ------------------------------------------------------------------ constants
+MAGIC = b"TLSNKV01"
+VERSION = 1
+HEADER_BYTES = 256
+ROW_BYTES = 1024  # one row = 64 granules of 16 bytes
+GRANULE = 16
+LANES = 64
+CHUNK_BYTES = 65536  # a slab is digested in pieces of at most this many bytes
+META_ALIGN = 256
+ROOT_OFFSET = 144
+NS_TAG = b"taliesin-ns-v1"
+
+DTYPE_BYTES = {1: 2, 2: 2, 3: 4, 4: 1}  # bf16, f16, f32, fp8
+MAX_LAYERS = 256
+MAX_GROUPS = 8
+
+# verdicts: a smaller code wins when several checks fail
+ACCEPT = 0x01
+MISSING = 0x10  # no record for the block
+BADARG = 0x11  # misaligned record pointer or a block-table entry out of range
+TRUNCATED = 0x12
+OVERLONG = 0x13
+ROOT = 0x14  # metadata checksum mismatch
+HEADER = 0x15  # format, geometry, namespace or reserved bytes differ
+POSITION = 0x16  # stored block index differs from the requested position
+KEY = 0x17  # stored fingerprint differs from the requested one
+TOKENS = 0x18  # stored token ids differ from the request's
+SEGMENT = 0x19  # a payload chunk digest differs from its table entry
+
+VERDICT_NAMES = {ACCEPT: "ACCEPT", MISSING: "MISSING", BADARG: "BADARG",
+                 TRUNCATED: "TRUNCATED", OVERLONG: "OVERLONG", ROOT: "ROOT",
+                 HEADER: "HEADER", POSITION: "POSITION", KEY: "KEY",
+                 TOKENS: "TOKENS", SEGMENT: "SEGMENT"}
+
+
+class LayoutError(ValueError):
+    pass
+
+
+class IdentityError(ValueError):
+    pass
+
+
+# ------------------------------------------------------------------ geometry
+@dataclass(frozen=True)
+class Layout:
+    """Model KV geometry: per layer, K and V caches are [pages][P][H][D]."""
+
+    n_layers: int
+    n_kv_heads: int
+    head_dim: int
+    dtype: int  # 1 bf16, 2 f16, 3 f32, 4 fp8
+    page_tokens: int
+    layer_window: Tuple[int, ...] = ()
+    layer_group: Tuple[int, ...] = ()
+
+    def __post_init__(self):
+        if not (1 <= self.n_layers <= MAX_LAYERS):
+            raise LayoutError("n_layers out of range")
+        if self.n_kv_heads < 1 or self.head_dim < 1 or self.page_tokens < 1:
+            raise LayoutError("zero-sized dimension")
+        if self.dtype not in DTYPE_BYTES:
+            raise LayoutError("unknown dtype")
+        if self.slab_bytes % ROW_BYTES:
+            raise LayoutError("slab bytes must be a multiple of 1024")
+        if self.slab_bytes > (1 << 31):
+            raise LayoutError("slab too large")
+        if self.layer_window and len(self.layer_window) != self.n_layers:
+            raise LayoutError("window list length")
+        if self.layer_group and len(self.layer_group) != self.n_layers:
+            raise LayoutError("group list length")
+        if any(w < 0 for w in self.layer_window):
+            raise LayoutError("negative window")
+        if any(not (0 <= g < MAX_GROUPS) for g in self.layer_group):
+            raise LayoutError("group out of range")
+
+    def window(self, layer):
+        return self.layer_window[layer] if self.layer_window else 0
+
+    def group(self, layer):
+        return self.layer_group[layer] if self.layer_group else 0
+
+    @property
+    def slab_bytes(self):
+        """Bytes of one (layer, K|V) page: P * H * D * element size."""
+        return self.page_tokens * self.n_kv_heads * self.head_dim * DTYPE_BYTES[self.dtype]
+
+    @property
+    def n_slabs(self):
+        return 2 * self.n_layers
+
+    @property
+    def chunks_per_slab(self):
+        return -(-self.slab_bytes // CHUNK_BYTES)
+
+    def chunk_len(self, k):
+        return min(CHUNK_BYTES, self.slab_bytes - k * CHUNK_BYTES)
+
+    @property
+    def n_segments(self):
+        return self.n_slabs * self.chunks_per_slab
+
+    @property
+    def meta_bytes(self):
+        raw = HEADER_BYTES + 8 * self.n_segments + 4 * self.page_tokens
+        return -(-raw // META_ALIGN) * META_ALIGN
+
+    @property
+    def payload_offset(self):
+        return self.meta_bytes
+
+    @property
+    def record_bytes(self):
+        return self.meta_bytes + self.n_slabs * self.slab_bytes
+
+    @property
+    def block_bytes(self):
+        """Key-chain input per block: the block's token ids as u32 LE."""
+        return 4 * self.page_tokens
+
+
+def slab_index(layer: int, kv: int) -> int:
+    """Record order: layer-major, K before V."""
+    return 2 * layer + kv
+
+
+# ------------------------------------------------------------------ identity
+def namespace_digest(tenant: bytes, model_fp: bytes, lay: Layout) -> bytes:
+    """SHA-256 over tenant, model fingerprint and KV geometry, each length-
+    prefixed (Sec. 2.1: refuse to start without a tenant identity and a model
+    fingerprint; Sec. 2.2: the fingerprint covers the model and the tenant)."""
+    if not tenant or not model_fp:
+        raise IdentityError("tenant identity and model fingerprint are required")
+    m = bytearray(NS_TAG)
+    m += struct.pack("<I", len(tenant)) + bytes(tenant)
+    m += struct.pack("<I", len(model_fp)) + bytes(model_fp)
+    m += struct.pack("<5I", lay.n_layers, lay.n_kv_heads, lay.head_dim, lay.dtype, lay.page_tokens)
+    for l in range(lay.n_layers):
+        m += struct.pack("<i", lay.window(l))
+    return hashlib.sha256(bytes(m)).digest()
+
+
+def block_keys(parent: bytes, data: bytes, block_bytes: int) -> List[bytes]:
+    """Chained block fingerprints (Sec. 2.2: key = fingerprint of the exact input
+    bytes; Sec. 5: reuse only whole blocks at matching positions, so a block's
+    key must cover every byte before it):
+        k_{-1} = parent,  k_i = SHA-256(k_{i-1} || data[i*B : (i+1)*B]).
+    Only full blocks get a key; a partial tail block is recomputed."""
+    if len(parent) != 32 or block_bytes <= 0:
+        raise ValueError("bad parent or block size")
+    keys, k = [], bytes(parent)
+    for i in range(len(data) // block_bytes):
+        k = hashlib.sha256(k + bytes(data[i * block_bytes:(i + 1) * block_bytes])).digest()
+        keys.append(k)
+    return keys
+
+
+# ------------------------------------------------------------------ checksums
+def xxh64(data: bytes, seed: int) -> int:
+    return xxhash.xxh64_intdigest(bytes(data), seed=seed)
+
+
+def chunk_digest(chunk) -> int:
+    """Tree-mode XXH64 of one payload chunk of R*1024 bytes.
+
+    Granule (r, j) is bytes [1024 r + 16 j, 1024 r + 16 j + 16). Column j is the
+    concatenation of granules (0, j), (1, j), ..., (R-1, j). The digest is
+    sum_j XXH64(column_j, seed = j) mod 2^64. Every byte is hashed once by
+    stock XXH64; the columns are independent."""
+    a = np.frombuffer(bytes(chunk), dtype=np.uint8)
+    if a.size == 0 or a.size % ROW_BYTES:
+        raise ValueError("chunk must be a positive multiple of 1024 bytes")
+    rows = a.size // ROW_BYTES
+    cols = a.reshape(rows, LANES, GRANULE).transpose(1, 0, 2)
+    total = 0
+    for j in range(LANES):
+        total = (total + xxh64(np.ascontiguousarray(cols[j]).tobytes(), j)) & MASK64
+    return total
+
+
+def slab_digests(lay: Layout, slab) -> List[int]:
+    """Digests of the chunks of one slab, in order."""
+    s = bytes(slab)
+    assert len(s) == lay.slab_bytes
+    return [chunk_digest(s[k * CHUNK_BYTES:k * CHUNK_BYTES + lay.chunk_len(k)])
+            for k in range(lay.chunks_per_slab)]
+
+
+def root_digest(meta: bytes) -> int:
+    """XXH64 (seed 0) of the metadata region with the root field read as 0."""
+    m = bytearray(meta)
+    m[ROOT_OFFSET:ROOT_OFFSET + 8] = bytes(8)
+    return xxh64(bytes(m), 0)
+
+
+# ------------------------------------------------------------------ record
+def header_fields(lay: Layout, ns: bytes, key: bytes, block_index: int) -> bytes:
+    """The 256-byte header with the root field still 0."""
+    h = bytearray(HEADER_BYTES)
+    h[0:8] = MAGIC
+    struct.pack_into("<II", h, 8, VERSION, HEADER_BYTES)
+    struct.pack_into("<QQQ", h, 16, lay.record_bytes, lay.payload_offset, lay.slab_bytes)
+    struct.pack_into("<6I", h, 40, lay.n_slabs, lay.n_layers, lay.n_kv_heads, lay.head_dim,
+                     lay.dtype, lay.page_tokens)
+    struct.pack_into("<Q", h, 64, block_index)
+    h[72:104] = key
+    h[104:136] = ns
+    struct.pack_into("<II", h, 136, CHUNK_BYTES, lay.n_segments)
+    return bytes(h)
+
+
+def make_meta(lay: Layout, ns: bytes, key: bytes, block_index: int, tokens, table: Sequence[int]) -> bytes:
+    toks = np.asarray(tokens, dtype="<u4")
+    assert toks.size == lay.page_tokens and len(table) == lay.n_segments
+    m = bytearray(lay.meta_bytes)
+    m[0:HEADER_BYTES] = header_fields(lay, ns, key, block_index)
+    off = HEADER_BYTES
+    for t in table:
+        struct.pack_into("<Q", m, off, t)
+        off += 8
+    m[off:off + 4 * lay.page_tokens] = toks.tobytes()
+    struct.pack_into("<Q", m, ROOT_OFFSET, root_digest(bytes(m)))
+    return bytes(m)
+
+
+def make_record(lay: Layout, ns: bytes, key: bytes, block_index: int, tokens, slabs) -> bytes:
+    """One block's record: metadata, then the 2L slabs in layer-major K,V order
+    (Sec. 2.2: save the KV state of a block under its fingerprint)."""
+    assert len(slabs) == lay.n_slabs
+    table = []
+    for s in slabs:
+        table.extend(slab_digests(lay, s))
+    meta = make_meta(lay, ns, key, block_index, tokens, table)
+    return meta + b"".join(bytes(s) for s in slabs)
+
+
+def _page_ok(p: int, n_pages: int) -> bool:
+    return 0 <= p < n_pages
+
+
+def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens, n_pages=None):
+    """Gather every block's pages into a record.
+
+    src_k[l], src_v[l]: uint8 arrays [pages, >= slab_bytes] (page rows).
+    tables: [n_groups][n_blocks] page ids; layer l uses tables[group(l)].
+    Returns (records, status): a block with any page id outside [0, n_pages)
+    gets an all-zero record and status BADARG, else status ACCEPT."""
+    tables = np.asarray(tables)
+    n = len(keys)
+    n_pages = src_k[0].shape[0] if n_pages is None else n_pages
+    used = sorted({lay.group(l) for l in range(lay.n_layers)})
+    records, status = [], []
+    for b in range(n):
+        if not all(_page_ok(int(tables[g][b]), n_pages) for g in used):
+            records.append(bytes(lay.record_bytes))
+            status.append(BADARG)
+            continue
+        slabs = []
+        for l in range(lay.n_layers):
+            page = int(tables[lay.group(l)][b])
+            for kv, src in ((0, src_k), (1, src_v)):
+                slabs.append(np.asarray(src[l][page, :lay.slab_bytes]).tobytes())
+        records.append(make_record(lay, ns, keys[b], int(block_index[b]), tokens[b], slabs))
+        status.append(ACCEPT)
+    return records, status
+
+
+# ------------------------------------------------------------------ verify
+def read_slabs(lay: Layout, tables, b: int) -> List[Tuple[int, int, int]]:
+    """(slab index, layer, kv) of the slabs a load reads for block b: every
+    slab whose layer's table entry is not -1."""
+    out = []
+    for l in range(lay.n_layers):
+        if int(tables[lay.group(l)][b]) != -1:
+            out.extend([(slab_index(l, 0), l, 0), (slab_index(l, 1), l, 1)])
+    return out
+
+
+def check_meta(lay: Layout, ns: bytes, rec: bytes, key: bytes, block_index: int, tokens) -> int:
+    """Metadata checks in precedence order, on a record of exactly
+    record_bytes. Returns the first failing code, or ACCEPT."""
+    meta = rec[:lay.payload_offset]
+    if struct.unpack_from("<Q", meta, ROOT_OFFSET)[0] != root_digest(meta):
+        return ROOT
+    want = header_fields(lay, ns, bytes(32), 0)
+    got = bytearray(meta[:HEADER_BYTES])
+    got[64:72] = bytes(8)  # block index, checked as POSITION
+    got[72:104] = bytes(32)  # key, checked as KEY
+    got[ROOT_OFFSET:ROOT_OFFSET + 8] = bytes(8)
+    tok_end = HEADER_BYTES + 8 * lay.n_segments + 4 * lay.page_tokens
+    if bytes(got) != want or any(meta[tok_end:]):
+        return HEADER
+    if struct.unpack_from("<Q", meta, 64)[0] != block_index:
+        return POSITION
+    if meta[72:104] != key:
+        return KEY
+    if tokens is not None:
+        t0 = HEADER_BYTES + 8 * lay.n_segments
+        if meta[t0:t0 + 4 * lay.page_tokens] != np.asarray(tokens, dtype="<u4").tobytes():
+            return TOKENS
+    return ACCEPT
+
+
+def verify(lay: Layout, ns: bytes, rec: Optional[bytes], key: bytes, block_index: int,
+           tokens, slabs_read: Sequence[int], bad_arg: bool = False) -> int:
+    """Verdict for one block (Sec. 2.2: checked on load; fail closed).
+
+    rec is the readable record (None = no record; its length is the length the
+    caller reports); slabs_read lists the slab indices the load would read."""
+    if rec is None:
+        return MISSING
+    if bad_arg:
+        return BADARG
+    if len(rec) < lay.record_bytes:
+        return TRUNCATED
+    if len(rec) > lay.record_bytes:
+        return OVERLONG
+    code = check_meta(lay, ns, rec, key, block_index, tokens)
+    if code != ACCEPT:
+        return code
+    cps = lay.chunks_per_slab
+    for s in slabs_read:
+        base = lay.payload_offset + s * lay.slab_bytes
+        for k in range(cps):
+            t = s * cps + k
+            stored = struct.unpack_from("<Q", rec, HEADER_BYTES + 8 * t)[0]
+            lo = base + k * CHUNK_BYTES
+            if chunk_digest(rec[lo:lo + lay.chunk_len(k)]) != stored:
+                return SEGMENT
+    return ACCEPT
+
+
+def restore(lay: Layout, ns: bytes, records, keys, block_index, tokens, tables,
+            dst_k, dst_v, n_pages=None, misaligned=()):
+    """Verify every listed block and scatter accepted ones into the paged cache.
+
+    records[b]: bytes or None; tokens: [n][P] or None (no token check);
+    tables: [n_groups][n] destination page ids (-1 = do not restore that
+    layer group for this block). Accepted blocks: every read slab is copied to
+    its page. Rejected blocks: every in-range page the block would have
+    written is zero-filled. Pages of other blocks and -1 entries are untouched.
+    Returns the verdict list."""
+    tables = np.asarray(tables)
+    n = len(keys)
+    n_pages = dst_k[0].shape[0] if n_pages is None else n_pages
+    misaligned = set(misaligned)
+    verdicts = []
+    for b in range(n):
+        slabs = read_slabs(lay, tables, b)
+        pages = [int(tables[lay.group(l)][b]) for (_, l, _) in slabs]
+        bad = b in misaligned or any(not _page_ok(p, n_pages) for p in pages)
+        v = verify(lay, ns, records[b], keys[b], int(block_index[b]),
+                   None if tokens is None else tokens[b], [s for (s, _, _) in slabs], bad)
+        verdicts.append(v)
+        for (s, l, kv), p in zip(slabs, pages):
+            if not _page_ok(p, n_pages):
+                continue
+            dst = dst_k[l] if kv == 0 else dst_v[l]
+            if v == ACCEPT:
+                lo = lay.payload_offset + s * lay.slab_bytes
+                dst[p, :lay.slab_bytes] = np.frombuffer(records[b][lo:lo + lay.slab_bytes], np.uint8)
+            else:
+                dst[p, :lay.slab_bytes] = 0
+    return verdicts

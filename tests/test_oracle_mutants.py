@@ -1,0 +1,122 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that the pins
+catch each one. A pin set that a transposed operand, a dropped term or a
+wrong seed slips through is not a pin set."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import taliesin_ref as ref
+from tests import test_oracle_format as pins
+from tests.golden import make_golden
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "micro_record.txt")
+
+
+def _read_golden():
+    with open(GOLDEN) as f:
+        lines = [l.strip() for l in f if l.strip() and not l.startswith("#")]
+    ns = bytes.fromhex(lines[0].split()[1])
+    key = bytes.fromhex(lines[1].split()[1])
+    return ns, key, bytes.fromhex("".join(lines[2:]))
+
+
+def test_golden_record_regression():
+    ns, key, rec = _read_golden()
+    ns2, key2, rec2 = make_golden.build()
+    assert (ns, key, rec) == (ns2, key2, rec2)
+
+
+def _rows_instead_of_columns(chunk):
+    # wrong: lane j hashes the j-th contiguous 1/64 of the chunk
+    a = bytes(chunk)
+    w = len(a) // 64
+    return sum(ref.xxh64(a[j * w:(j + 1) * w], j) for j in range(64)) & ref.MASK64
+
+
+def _transposed(chunk):
+    a = np.frombuffer(bytes(chunk), np.uint8)
+    rows = a.size // 1024
+    cols = a.reshape(64, rows, 16)  # wrong: treats the buffer as column-major
+    return sum(ref.xxh64(cols[j].tobytes(), j) for j in range(64)) & ref.MASK64
+
+
+def _seed_zero(chunk):
+    a = np.frombuffer(bytes(chunk), np.uint8)
+    cols = a.reshape(-1, 64, 16).transpose(1, 0, 2)
+    return sum(ref.xxh64(np.ascontiguousarray(cols[j]).tobytes(), 0) for j in range(64)) & ref.MASK64
+
+
+def _xor_combine(chunk):
+    a = np.frombuffer(bytes(chunk), np.uint8)
+    cols = a.reshape(-1, 64, 16).transpose(1, 0, 2)
+    t = 0
+    for j in range(64):
+        t ^= ref.xxh64(np.ascontiguousarray(cols[j]).tobytes(), j)
+    return t
+
+
+def _rows_reversed(chunk):
+    a = np.frombuffer(bytes(chunk), np.uint8)
+    cols = a.reshape(-1, 64, 16)[::-1].transpose(1, 0, 2)
+    return sum(ref.xxh64(np.ascontiguousarray(cols[j]).tobytes(), j) for j in range(64)) & ref.MASK64
+
+
+CHUNK_PINS = [
+    lambda: pins.test_chunk_digest_orientation_and_row_order(3),
+    lambda: pins.test_chunk_digest_orientation_and_row_order(1),
+    pins.test_chunk_digest_single_row_is_sum_of_granule_hashes,
+    pins.test_chunk_digest_is_additive_over_columns,
+]
+
+
+@pytest.mark.parametrize("mutant", [_rows_instead_of_columns, _transposed, _seed_zero,
+                                    _xor_combine, _rows_reversed])
+def test_chunk_digest_mutants_are_caught(monkeypatch, mutant):
+    monkeypatch.setattr(ref, "chunk_digest", mutant)
+    caught = 0
+    for pin in CHUNK_PINS:
+        try:
+            pin()
+        except AssertionError:
+            caught += 1
+    assert caught >= 1
+
+
+def _unchained_keys(parent, data, block_bytes):
+    return [__import__("hashlib").sha256(parent + bytes(data[i * block_bytes:(i + 1) * block_bytes])).digest()
+            for i in range(len(data) // block_bytes)]
+
+
+def test_unchained_keys_caught(monkeypatch):
+    monkeypatch.setattr(ref, "block_keys", _unchained_keys)
+    with pytest.raises(AssertionError):
+        pins.test_keys_are_chained_prefix_fingerprints()
+
+
+def test_root_without_zeroed_field_caught(monkeypatch):
+    monkeypatch.setattr(ref, "root_digest", lambda meta: ref.xxh64(bytes(meta), 0))
+    with pytest.raises(AssertionError):
+        pins.test_verify_accepts_its_own_record()
+
+
+def test_restore_with_swapped_tables_caught(monkeypatch):
+    real = ref.restore
+
+    def swapped(lay, ns, records, keys, block_index, tokens, tables, dst_k, dst_v, **kw):
+        return real(lay, ns, records, keys, block_index, tokens, tables, dst_v, dst_k, **kw)
+
+    monkeypatch.setattr(ref, "restore", swapped)
+    with pytest.raises(AssertionError):
+        pins.test_save_restore_is_the_permutation_copy(0)
+
+
+def test_missing_segment_check_caught(monkeypatch):
+    real = ref.verify
+
+    def lax(lay, ns, rec, key, block_index, tokens, slabs_read, bad_arg=False):
+        return real(lay, ns, rec, key, block_index, tokens, [], bad_arg)
+
+    monkeypatch.setattr(ref, "verify", lax)
+    with pytest.raises(AssertionError):
+        pins.test_every_single_bit_flip_is_rejected(32)
