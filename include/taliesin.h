@@ -1,0 +1,234 @@
+/*
+ * taliesin.h -- C ABI of libtaliesin.so, the MI355X (gfx950) hot path of the
+ * Taliesin KV memory layer: chained block keys, save of paged KV into
+ * checksummed records, and verified restore into a paged KV cache.
+ *
+ * Paper: Schelpe, "Working Around the Compute Ceiling: Galahad's Byte-Exact
+ * Memory Makes LLM Reading a One-Time Cost" (2026).
+ *   Sec. 2.1  the library refuses to start without a tenant identity and a
+ *             model fingerprint.
+ *   Sec. 2.2  KV state of a block is written under a fingerprint of the exact
+ *             input bytes, the model and the tenant; a later request with the
+ *             same block loads it instead of recomputing; stored state is
+ *             checked on load; missing, damaged or failing records are
+ *             recomputed (serve without memory, never with wrong memory);
+ *             reuse is per block at exactly matching positions.
+ *   Sec. 3    restored state is bit-identical (Table 1); confirmation hash and
+ *             byte comparison on load (sabotage testing).
+ *   Sec. 5    block-level reuse; fail-closed by design.
+ * The paper withholds the storage format; the record layout, key chain and
+ * tree-mode XXH64 checksum implemented here are documented field by field in
+ * the repository's design notes and restated in the comments below.
+ *
+ * Conventions for every call:
+ *   - Pointers named d_* are device (HBM) addresses; all others are host.
+ *   - The caller owns every buffer (caches, records, tables, verdicts,
+ *     workspace). tl_save / tl_load allocate no device memory and perform no
+ *     host<->device copies; they only enqueue kernels on `stream`
+ *     (a hipStream_t; NULL = the null stream) and return. Outputs are valid
+ *     after that stream is synchronised.
+ *   - Return value: TL_OK (0) or a negative TL_E* status. On a negative status
+ *     nothing was enqueued, except TL_EDEVICE, which reports a failed launch.
+ *     A problem with one block is never a status: it is that block's verdict.
+ *   - One call handles fewer than 2^24 blocks, and n_blocks times the number
+ *     of chunk digests per record must be below 2^32 (TL_ERANGE otherwise).
+ *   - No call throws; a context is immutable after creation and may be used
+ *     from several host threads; concurrent tl_load calls need separate
+ *     workspaces.
+ */
+#ifndef TALIESIN_H
+#define TALIESIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define TL_OK 0
+#define TL_EINVAL (-1)    /* NULL or inconsistent argument */
+#define TL_ELAYOUT (-2)   /* KV geometry not supported */
+#define TL_ENOIDENT (-3)  /* empty tenant identity or model fingerprint (Sec. 2.1) */
+#define TL_EDEVICE (-4)   /* a HIP launch failed */
+#define TL_ENOMEM (-5)    /* host allocation failed */
+#define TL_EFULL (-6)     /* index is full */
+#define TL_ERANGE (-7)    /* workspace too small, buffer capacity too small */
+
+/* ---- per-block verdicts (tl_load) and save status (tl_save) ----------
+ * When several checks fail, the smallest code wins. */
+#define TL_ACCEPT 0x01
+#define TL_MISSING 0x10   /* record pointer is 0 */
+#define TL_BADARG 0x11    /* record pointer not 16-byte aligned, or a block-
+                             table entry outside [-1, n_pages) */
+#define TL_TRUNCATED 0x12 /* reported length < record bytes */
+#define TL_OVERLONG 0x13  /* reported length > record bytes */
+#define TL_ROOT 0x14      /* metadata checksum mismatch */
+#define TL_HEADER 0x15    /* format, geometry, namespace, reserved or padding */
+#define TL_POSITION 0x16  /* stored block index != requested position */
+#define TL_KEY 0x17       /* stored key != requested key */
+#define TL_TOKENS 0x18    /* stored token ids != expected token ids */
+#define TL_SEGMENT 0x19   /* a payload chunk read by the load != its digest */
+
+#define TL_KEY_BYTES 32
+#define TL_MAX_LAYERS 256
+#define TL_MAX_GROUPS 8
+#define TL_CHUNK_BYTES 65536 /* payload digest granularity */
+
+/* dtype codes; only the element size matters, bytes are moved verbatim */
+#define TL_DTYPE_BF16 1
+#define TL_DTYPE_F16 2
+#define TL_DTYPE_F32 3
+#define TL_DTYPE_FP8 4
+
+/* KV geometry. Per layer, the K and the V cache are each
+ * [pages][page_tokens][n_kv_heads][head_dim] elements; one page of one layer's
+ * K (or V) is a "slab" of page_tokens*n_kv_heads*head_dim*elem bytes, which
+ * must be a multiple of 1024. */
+typedef struct tl_layout {
+  uint32_t n_layers;   /* 1..TL_MAX_LAYERS */
+  uint32_t n_kv_heads;
+  uint32_t head_dim;
+  uint32_t dtype;       /* TL_DTYPE_* */
+  uint32_t page_tokens; /* tokens per page = tokens per block */
+  const int32_t* layer_window; /* host [n_layers] or NULL; 0 = global
+                                  attention, >0 = sliding window (tokens).
+                                  Part of the model identity. */
+  const uint8_t* layer_group;  /* host [n_layers] or NULL (all 0); which of
+                                  the block tables a layer uses, < TL_MAX_GROUPS */
+} tl_layout;
+
+/* Derived sizes of one record (read-only view of a context). */
+typedef struct tl_geometry {
+  uint64_t record_bytes;   /* exact length of every record */
+  uint64_t payload_offset; /* = metadata bytes, a multiple of 256 */
+  uint64_t slab_bytes;
+  uint32_t n_slabs;        /* 2 * n_layers: slab s = 2*layer + (0 K, 1 V) */
+  uint32_t chunks_per_slab;
+  uint32_t n_segments;     /* digest table entries = n_slabs*chunks_per_slab */
+  uint32_t n_groups;       /* max(layer_group) + 1 */
+  uint32_t block_bytes;    /* key-chain input per block = 4 * page_tokens */
+  uint32_t reserved;
+} tl_geometry;
+
+/* A paged KV cache in HBM. Page p of layer l's K cache starts at device
+ * address d_layer_k[l] + p * page_stride (same for V). The caller guarantees
+ * these addresses are valid and 16-byte aligned for every p in [0, n_pages)
+ * that the block tables name; the library checks table entries against
+ * n_pages but cannot check device pointers from the host. */
+typedef struct tl_cache {
+  const uint64_t* d_layer_k; /* device [n_layers] base addresses */
+  const uint64_t* d_layer_v; /* device [n_layers] base addresses */
+  int64_t page_stride;       /* bytes; multiple of 16 and >= slab_bytes */
+  int64_t n_pages;           /* valid page ids are [0, n_pages) */
+} tl_cache;
+
+/* Per-block request description (all device arrays, n = number of blocks). */
+typedef struct tl_blocks {
+  const uint8_t* d_keys;         /* [n][32] block keys (from tl_block_keys) */
+  const uint64_t* d_block_index; /* [n] block position in its document */
+  const uint32_t* d_tokens;      /* [n][page_tokens] token ids; tl_save:
+                                    required; tl_load: NULL skips the TOKENS
+                                    check */
+  const int32_t* d_tables;       /* [n_groups][n] page ids. tl_save: every
+                                    entry must be in [0, n_pages). tl_load:
+                                    -1 = do not restore that layer group for
+                                    this block (its slabs are not read). */
+} tl_blocks;
+
+typedef struct tl_ctx tl_ctx;
+typedef struct tl_index tl_index;
+
+/* ---- context --------------------------------------------------------- */
+/* Create a context for one tenant and one model (Sec. 2.1, Sec. 2.2). The
+ * namespace digest SHA-256("taliesin-ns-v1" | u32 len | tenant | u32 len |
+ * model_fp | u32 L,H,D,dtype,P | i32 window per layer) roots every key chain
+ * and is stored in every record. Returns NULL and sets *status (if non-NULL)
+ * to TL_ENOIDENT when tenant or model_fp is empty, TL_ELAYOUT when the
+ * geometry is unsupported, TL_EINVAL for NULL layout, TL_ENOMEM. */
+tl_ctx* tl_ctx_create(const void* tenant, size_t tenant_len, const void* model_fp,
+                      size_t model_fp_len, const tl_layout* layout, int* status);
+void tl_ctx_destroy(tl_ctx* ctx); /* NULL is a no-op */
+int tl_ctx_geometry(const tl_ctx* ctx, tl_geometry* out);
+int tl_ns_digest(const tl_ctx* ctx, uint8_t out[TL_KEY_BYTES]);
+
+/* Device workspace tl_load needs for n_blocks blocks (4 bytes per block,
+ * rounded up to 256). */
+size_t tl_workspace_bytes(const tl_ctx* ctx, size_t n_blocks);
+
+/* ---- a1: chained block keys (host) -------------------------------------
+ * k_{-1} = parent (NULL: the context's namespace digest),
+ * k_i = SHA-256(k_{i-1} | bytes[i*B, (i+1)*B)), B = block_bytes (0: the
+ * context's 4*page_tokens, i.e. u32 little-endian token ids). Only full blocks
+ * get a key; a partial tail is left for prefill. Sets *n_keys = n_full and
+ * writes the n_full keys (32 bytes each) to keys_out; TL_ERANGE, with nothing
+ * written, if cap < n_full.
+ * Sec. 2.2 (fingerprint of the exact input bytes, model and tenant), Sec. 5
+ * (whole blocks at exact positions: every key covers all bytes before it). */
+int tl_block_keys(const tl_ctx* ctx, const uint8_t* parent, const void* bytes, size_t n_bytes,
+                  size_t block_bytes, uint8_t* keys_out, size_t cap, size_t* n_keys);
+
+/* Same chain for n_docs independent documents, run on host threads
+ * (one chain per thread at a time). doc_off[d], doc_len[d]: byte range of
+ * document d in `bytes`; key_off[d]: first key slot of document d in keys_out
+ * (caller sizes it for floor(doc_len/B) keys); n_keys_out[d] (optional)
+ * receives the number of keys. parents: NULL or [n_docs][32]. */
+int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* bytes,
+                        const uint64_t* doc_off, const uint64_t* doc_len, size_t n_docs,
+                        size_t block_bytes, uint8_t* keys_out, const uint64_t* key_off,
+                        uint64_t* n_keys_out, int n_threads);
+
+/* ---- a6: save -----------------------------------------------------------
+ * Gathers block b's 2*L slabs (layer l uses page d_tables[group(l)][b] of
+ * src) into the record at d_record_ptrs[b] (record_bytes long, 16-byte
+ * aligned, caller-allocated): metadata (header, chunk digest table, token
+ * ids, zero padding, root) followed by the slabs verbatim. d_status[b]
+ * (optional, device [n]): TL_ACCEPT when written; TL_MISSING for a 0
+ * pointer and TL_BADARG for a misaligned pointer (nothing written); TL_BADARG
+ * for a page id outside [0, n_pages) (the whole record is written as zeros, so
+ * any later load fails). Sec. 2.2 (save after prefill), Fig. 1. */
+int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
+            const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status);
+
+/* ---- a3-a5: verified restore ---------------------------------------------
+ * For every block b: d_record_ptrs[b] (0 = no record) with reported length
+ * d_record_lens[b]; the library never reads past that length and takes every
+ * offset from the context, never from the record. Checks, in order: pointer,
+ * length, root (metadata checksum), header fields and namespace, position
+ * (d_block_index[b]), key (d_keys[b]), token ids (if d_tokens), and the tree
+ * XXH64 of every payload chunk it reads. It copies each read slab to page
+ * d_tables[group(l)][b] of dst in the same pass and writes d_verdicts[b]
+ * (device [n], TL_ACCEPT or the first failing code). Every page a rejected
+ * block would have written is zero-filled; pages of -1 entries are untouched.
+ * Distinct blocks must not name the same destination page.
+ * d_workspace: device, >= tl_workspace_bytes(ctx, n_blocks), 4-byte aligned;
+ * its contents need no initialisation. Sec. 2.2, Sec. 3, Sec. 5. */
+int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_record_ptrs,
+            const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
+            uint8_t* d_verdicts, void* d_workspace, size_t workspace_bytes);
+
+/* ---- a2: key -> record index (host) --------------------------------------
+ * Open addressing over 32-byte keys, 64-bit handles. Readers may run
+ * concurrently; writers need external exclusion. */
+tl_index* tl_index_create(size_t capacity);
+void tl_index_destroy(tl_index* idx);
+/* insert or overwrite; TL_EFULL beyond capacity */
+int tl_index_put(tl_index* idx, const uint8_t key[TL_KEY_BYTES], uint64_t handle);
+/* handles_out[i] = handle of keys[i], or UINT64_MAX when absent */
+int tl_index_get_batch(const tl_index* idx, const uint8_t* keys, size_t n, uint64_t* handles_out);
+size_t tl_index_size(const tl_index* idx);
+
+/* ---- misc ---------------------------------------------------------------- */
+const char* tl_status_string(int status);
+const char* tl_verdict_string(int verdict);
+int tl_abi_version(void); /* 1 */
+/* Self-test hook: SHA-256 of data with the portable compression function
+ * (impl 0) or the x86 SHA-extension one (impl 1; TL_EINVAL when the host CPU
+ * lacks it). Used to check both implementations against FIPS 180-4 vectors. */
+int tl_test_sha256(const void* data, size_t n, int impl, uint8_t out[TL_KEY_BYTES]);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TALIESIN_H */

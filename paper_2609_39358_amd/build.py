@@ -1,0 +1,55 @@
+"""Builds libtaliesin.so in-tree: host runtime (C++17, g++) + HIP kernels
+(hipcc, gfx950 only). Run: python -m paper_2609_39358_amd.build"""
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+INCLUDE = os.path.join(ROOT, "include")
+OUT = os.path.join(PKG, "libtaliesin.so")
+BUILD_DIR = os.path.join(PKG, "_build")
+
+HIP_FLAGS = [
+    "-O3", "-fPIC", "-std=c++17", "--offload-arch=gfx950",
+    # no packed FP32 instructions anywhere (the kernels do no FP32 math)
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+CXX_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-Wall", "-Wextra", "-Wno-unused-parameter"]
+
+
+def _run(cmd, verbose):
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout)
+        raise RuntimeError("build step failed: " + " ".join(cmd[:3]))
+    return r.stdout
+
+
+def build(verbose: bool = False, extra_hip_flags=()) -> str:
+    hipcc = os.environ.get("HIPCC") or shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+    cxx = os.environ.get("CXX") or shutil.which("g++") or "g++"
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    inc = ["-I", INCLUDE, "-I", CSRC]
+    objs = []
+    for src in ("ctx.cpp", "sha256.cpp"):
+        o = os.path.join(BUILD_DIR, src + ".o")
+        _run([cxx, *CXX_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        objs.append(o)
+    o = os.path.join(BUILD_DIR, "kernels.hip.o")
+    _run([hipcc, *HIP_FLAGS, *extra_hip_flags, *inc, "-c", os.path.join(CSRC, "kernels.hip"), "-o", o],
+         verbose)
+    objs.append(o)
+    tmp = OUT + ".tmp"
+    _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs], verbose)
+    os.replace(tmp, OUT)
+    return OUT
+
+
+if __name__ == "__main__":
+    print(build(verbose=True))

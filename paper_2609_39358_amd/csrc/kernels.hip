@@ -1,0 +1,547 @@
+// HIP kernels (gfx950) of libtaliesin: save and verified restore of paged KV.
+//
+// Work decomposition. A record holds one block: metadata, then 2L slabs
+// (slab s = 2*layer + kv is one page of one layer's K or V cache). Each slab
+// is digested in chunks of at most 64 KiB; a chunk is R rows of 1024 bytes and
+// its digest is sum_j XXH64(column_j, seed = j) mod 2^64, where column j is the
+// 16-byte granule at offset 16*j of every row. One wavefront owns one
+// (block, chunk): lane j moves granule j of every row with a 16-byte load and
+// a 16-byte store (each row is one fully coalesced 1 KiB access) and feeds
+// the same 16 bytes into its own XXH64 state, so every byte crosses HBM once
+// in each direction and is hashed from registers. The 64 leaf digests are
+// summed with a ds_swizzle butterfly.
+//
+//   save:  k_save_seg  (page -> record payload, chunk digest -> table)
+//          k_save_meta (header, token ids, padding, root over the metadata)
+//   load:  k_load_meta (pointer/length/root/header/position/key/token checks)
+//          k_load_seg  (record -> page copy + chunk digest + compare)
+//          k_load_final(verdicts; zero-fill pages of blocks failing a chunk)
+//
+// Sec. 2.2 (save under a fingerprint, check on load, recompute on failure),
+// Sec. 3 Table 1 (bit-identical restore), Sec. 5 (block-level reuse, fail
+// closed). XXH64 follows the published algorithm description (xxHash
+// specification); the tree arrangement is this library's record format.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace {
+
+constexpr uint64_t kP1 = 0x9E3779B185EBCA87ull;
+constexpr uint64_t kP2 = 0xC2B2AE3D27D4EB4Full;
+constexpr uint64_t kP3 = 0x165667B19E3779F9ull;
+constexpr uint64_t kP4 = 0x85EBCA77C2B2AE63ull;
+constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
+
+constexpr uint32_t kSegWaves = 4;       // wavefronts per workgroup in the chunk kernels
+constexpr uint32_t kMetaTile = 4096;    // metadata bytes staged in LDS at a time
+constexpr uint32_t kSegFailBit = 0x100; // status bit: some chunk digest mismatched
+
+// 16 bytes per lane: a native vector so that the compiler emits dwordx4
+// accesses and accepts the non-temporal builtins.
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ v4u zero4() { return v4u{0u, 0u, 0u, 0u}; }
+
+// ---- XXH64 pieces --------------------------------------------------------
+__device__ __forceinline__ uint64_t rotl64(uint64_t x, int r) { return (x << r) | (x >> (64 - r)); }
+
+__device__ __forceinline__ uint64_t xx_round(uint64_t acc, uint64_t in) {
+  acc += in * kP2;
+  acc = rotl64(acc, 31);
+  return acc * kP1;
+}
+
+__device__ __forceinline__ uint64_t xx_merge(uint64_t acc, uint64_t v) {
+  acc ^= xx_round(0, v);
+  return acc * kP1 + kP4;
+}
+
+__device__ __forceinline__ uint64_t xx_avalanche(uint64_t h) {
+  h ^= h >> 33;
+  h *= kP2;
+  h ^= h >> 29;
+  h *= kP3;
+  h ^= h >> 32;
+  return h;
+}
+
+__device__ __forceinline__ uint64_t lo64(v4u v) { return (uint64_t)v.y << 32 | v.x; }
+__device__ __forceinline__ uint64_t hi64(v4u v) { return (uint64_t)v.w << 32 | v.z; }
+
+// XXH64 state of one lane's column.
+struct Column {
+  uint64_t v1, v2, v3, v4;
+  __device__ __forceinline__ void init(uint64_t seed) {
+    v1 = seed + kP1 + kP2;
+    v2 = seed + kP2;
+    v3 = seed;
+    v4 = seed - kP1;
+  }
+  // one 32-byte stripe = two consecutive granules of the column
+  __device__ __forceinline__ void stripe(v4u a, v4u b) {
+    v1 = xx_round(v1, lo64(a));
+    v2 = xx_round(v2, hi64(a));
+    v3 = xx_round(v3, lo64(b));
+    v4 = xx_round(v4, hi64(b));
+  }
+  // digest of a column of `rows` granules; `last` is the odd final granule
+  __device__ __forceinline__ uint64_t finish(uint64_t seed, uint32_t rows, v4u last) const {
+    uint64_t h;
+    if (rows >= 2) {
+      h = rotl64(v1, 1) + rotl64(v2, 7) + rotl64(v3, 12) + rotl64(v4, 18);
+      h = xx_merge(h, v1);
+      h = xx_merge(h, v2);
+      h = xx_merge(h, v3);
+      h = xx_merge(h, v4);
+    } else {
+      h = seed + kP5;
+    }
+    h += (uint64_t)rows * 16;
+    if (rows & 1) {
+      h ^= xx_round(0, lo64(last));
+      h = rotl64(h, 27) * kP1 + kP4;
+      h ^= xx_round(0, hi64(last));
+      h = rotl64(h, 27) * kP1 + kP4;
+    }
+    return xx_avalanche(h);
+  }
+};
+
+// ---- wavefront reductions --------------------------------------------------
+// ds_swizzle in bit-mask mode: offset = xor_mask << 10 | or_mask << 5 | and_mask.
+template <int X>
+__device__ __forceinline__ uint64_t swz_xor(uint64_t v) {
+  const int pat = (X << 10) | 0x1f;
+  uint32_t lo = (uint32_t)__builtin_amdgcn_ds_swizzle((int)(uint32_t)v, pat);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_ds_swizzle((int)(uint32_t)(v >> 32), pat);
+  return (uint64_t)hi << 32 | lo;
+}
+
+// Sum of v over the 64 lanes (mod 2^64), returned uniformly.
+__device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
+  v += swz_xor<1>(v);
+  v += swz_xor<2>(v);
+  v += swz_xor<4>(v);
+  v += swz_xor<8>(v);
+  v += swz_xor<16>(v);
+  const uint32_t lo0 = __builtin_amdgcn_readlane((int)(uint32_t)v, 0);
+  const uint32_t hi0 = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 0);
+  const uint32_t lo1 = __builtin_amdgcn_readlane((int)(uint32_t)v, 32);
+  const uint32_t hi1 = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 32);
+  return ((uint64_t)hi0 << 32 | lo0) + ((uint64_t)hi1 << 32 | lo1);
+}
+
+__device__ __forceinline__ uint32_t uniform(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// ---- kernel arguments ---------------------------------------------------------
+struct SegArgs {
+  tl::Geo g;
+  const uint64_t* rec;   // [n] record device addresses
+  const int32_t* tables; // [n_groups][n]
+  const uint64_t* lk;    // [L] K cache bases
+  const uint64_t* lv;    // [L] V cache bases
+  int64_t stride;
+  int64_t n_pages;
+  uint32_t n;            // blocks
+  uint32_t total;        // n * n_seg work items
+  uint32_t* status;      // load: per-block status words
+};
+
+struct MetaArgs {
+  tl::Geo g;
+  const uint64_t* rec;
+  const uint64_t* len;       // load only
+  const uint8_t* keys;       // [n][32]
+  const uint64_t* bidx;      // [n]
+  const uint32_t* tokens;    // [n][P] or null (load)
+  const int32_t* tables;
+  int64_t n_pages;
+  uint32_t n;
+  uint32_t* status;          // load: status words; save: unused
+  uint8_t* out_status;       // save: per-block status bytes (optional)
+  uint32_t tmpl[tl::kHeaderBytes / 4];
+};
+
+// Slab work item -> (block, table entry, page base, record chunk offset).
+struct Item {
+  uint32_t b, t, s, k, rows;
+  int32_t page;
+};
+
+__device__ __forceinline__ Item decode(const SegArgs& a, uint32_t w) {
+  Item it;
+  it.b = w / a.g.n_seg;
+  it.t = w - it.b * a.g.n_seg;
+  it.s = it.t / a.g.cps;
+  it.k = it.t - it.s * a.g.cps;
+  const uint32_t layer = it.s >> 1;
+  it.page = a.tables[(uint64_t)a.g.group[layer] * a.n + it.b];
+  const uint64_t clen = a.g.slab_bytes - (uint64_t)it.k * tl::kChunkBytes;
+  it.rows = (uint32_t)((clen < tl::kChunkBytes ? clen : tl::kChunkBytes) / tl::kRowBytes);
+  return it;
+}
+
+__device__ __forceinline__ char* page_chunk(const SegArgs& a, const Item& it) {
+  const uint32_t layer = it.s >> 1;
+  const uint64_t base = (it.s & 1) ? a.lv[layer] : a.lk[layer];
+  return (char*)(base + (uint64_t)it.page * (uint64_t)a.stride + (uint64_t)it.k * tl::kChunkBytes);
+}
+
+__device__ __forceinline__ char* record_chunk(const SegArgs& a, uint64_t rec, const Item& it) {
+  return (char*)(rec + a.g.payload_offset + (uint64_t)it.s * a.g.slab_bytes +
+                 (uint64_t)it.k * tl::kChunkBytes);
+}
+
+__device__ __forceinline__ void zero_rows(char* dst, uint32_t rows, uint32_t lane) {
+  v4u* d = (v4u*)dst + lane;
+  const v4u z = zero4();
+  for (uint32_t r = 0; r < rows; ++r) d[(uint64_t)r * 64] = z;
+}
+
+// Copy `rows` rows of 1 KiB from src to dst and return this lane's column
+// digest (seed = lane). Eight rows are in flight per lane per batch.
+__device__ __forceinline__ uint64_t copy_hash(const char* src, char* dst, uint32_t rows,
+                                              uint32_t lane) {
+  const v4u* s = (const v4u*)src + lane;
+  v4u* d = (v4u*)dst + lane;
+  Column c;
+  c.init(lane);
+  uint32_t r = 0;
+  for (; r + 8 <= rows; r += 8) {
+    v4u x[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __builtin_nontemporal_load(s + (uint64_t)(r + i) * 64);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) __builtin_nontemporal_store(x[i], d + (uint64_t)(r + i) * 64);
+#pragma unroll
+    for (int i = 0; i < 8; i += 2) c.stripe(x[i], x[i + 1]);
+  }
+  for (; r + 2 <= rows; r += 2) {
+    const v4u x0 = s[(uint64_t)r * 64], x1 = s[(uint64_t)(r + 1) * 64];
+    d[(uint64_t)r * 64] = x0;
+    d[(uint64_t)(r + 1) * 64] = x1;
+    c.stripe(x0, x1);
+  }
+  v4u last = zero4();
+  if (r < rows) {
+    last = s[(uint64_t)r * 64];
+    d[(uint64_t)r * 64] = last;
+  }
+  return c.finish(lane, rows, last);
+}
+
+__device__ __forceinline__ bool page_in_range(int32_t p, int64_t n_pages) {
+  return p >= 0 && (int64_t)p < n_pages;
+}
+
+// ---- save ---------------------------------------------------------------------
+__device__ __forceinline__ bool block_pages_valid(const tl::Geo& g, const int32_t* tables,
+                                                  uint32_t n, uint32_t b, int64_t n_pages) {
+  bool ok = true;
+  for (uint32_t grp = 0; grp < g.n_groups; ++grp)
+    if (g.groups_used >> grp & 1) ok = ok && page_in_range(tables[(uint64_t)grp * n + b], n_pages);
+  return ok;
+}
+
+__global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t step = gridDim.x * kSegWaves;
+  for (uint32_t w = blockIdx.x * kSegWaves + uniform(threadIdx.x >> 6); w < a.total; w += step) {
+    const Item it = decode(a, w);
+    const uint64_t rec = a.rec[it.b];
+    if (rec == 0 || (rec & 15)) continue;
+    char* out = record_chunk(a, rec, it);
+    if (!block_pages_valid(a.g, a.tables, a.n, it.b, a.n_pages)) {
+      zero_rows(out, it.rows, lane);  // k_save_meta zeroes the metadata
+      continue;
+    }
+    const uint64_t leaf = copy_hash(page_chunk(a, it), out, it.rows, lane);
+    const uint64_t digest = wave_sum64(leaf);
+    if (lane == 0) *(uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t) = digest;
+  }
+}
+
+// Assembles (save) or loads (load) one metadata tile into LDS, 4 bytes per
+// lane-step. Lanes 0..3 then run the four XXH64 accumulators over the tile.
+__device__ __forceinline__ void hash_tile(const uint64_t* tile64, uint32_t n_bytes, uint32_t off,
+                                          uint32_t lane, uint64_t& acc) {
+  if (lane < 4) {
+    const uint32_t stripes = n_bytes / 32;
+    for (uint32_t st = 0; st < stripes; ++st) {
+      uint64_t x = tile64[st * 4 + lane];
+      if (off + st * 32 + lane * 8 == tl::kRootOffset) x = 0;  // the root reads as zero
+      acc = xx_round(acc, x);
+    }
+  }
+}
+
+__device__ __forceinline__ uint64_t finish_root(uint64_t acc, uint64_t len) {
+  const uint64_t v1 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 0) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 0);
+  const uint64_t v2 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 1) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 1);
+  const uint64_t v3 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 2) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 2);
+  const uint64_t v4 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 3) << 32) |
+                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 3);
+  uint64_t h = rotl64(v1, 1) + rotl64(v2, 7) + rotl64(v3, 12) + rotl64(v4, 18);
+  h = xx_merge(h, v1);
+  h = xx_merge(h, v2);
+  h = xx_merge(h, v3);
+  h = xx_merge(h, v4);
+  h += len;  // metadata length is a multiple of 256: no tail bytes
+  return xx_avalanche(h);
+}
+
+__device__ __forceinline__ uint64_t root_init(uint32_t lane) {
+  // seed 0: v1 = P1 + P2, v2 = P2, v3 = 0, v4 = -P1
+  return lane == 0 ? kP1 + kP2 : lane == 1 ? kP2 : lane == 2 ? 0 : (uint64_t)0 - kP1;
+}
+
+__global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
+  __shared__ uint64_t tile64[kMetaTile / 8];
+  uint32_t* tile32 = (uint32_t*)tile64;
+  const uint32_t lane = threadIdx.x;
+  const uint32_t b = blockIdx.x;
+  const uint64_t rec = a.rec[b];
+  if (rec == 0 || (rec & 15)) {
+    if (lane == 0 && a.out_status) a.out_status[b] = rec == 0 ? TL_MISSING : TL_BADARG;
+    return;
+  }
+  const uint32_t meta = (uint32_t)a.g.payload_offset;
+  if (!block_pages_valid(a.g, a.tables, a.n, b, a.n_pages)) {
+    v4u* d = (v4u*)rec;
+    for (uint32_t i = lane; i < meta / 16; i += 64) d[i] = zero4();
+    if (lane == 0 && a.out_status) a.out_status[b] = TL_BADARG;
+    return;
+  }
+  const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
+  const uint32_t* tok = a.tokens + (uint64_t)a.g.page_tokens * b;
+  const uint64_t bi = a.bidx[b];
+  uint64_t acc = root_init(lane);
+  for (uint32_t off = 0; off < meta; off += kMetaTile) {
+    const uint32_t nb = meta - off < kMetaTile ? meta - off : kMetaTile;
+    for (uint32_t wd = lane; wd < nb / 4; wd += 64) {
+      const uint32_t o = off + 4 * wd;
+      uint32_t x;
+      if (o < tl::kHeaderBytes) {
+        if (o == tl::kIndexOffset) x = (uint32_t)bi;
+        else if (o == tl::kIndexOffset + 4) x = (uint32_t)(bi >> 32);
+        else if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) x = key32[(o - tl::kKeyOffset) / 4];
+        else x = a.tmpl[o / 4];  // root field is zero in the template
+      } else if (o < a.g.tok_off) {
+        x = *(const uint32_t*)(rec + o);  // chunk digest written by k_save_seg
+      } else if (o < a.g.tok_end) {
+        x = tok[(o - a.g.tok_off) / 4];
+      } else {
+        x = 0;
+      }
+      tile32[wd] = x;
+    }
+    __syncthreads();
+    hash_tile(tile64, nb, off, lane, acc);
+    // write the tile back; the 16 bytes holding the root are written last
+    const v4u* t4 = (const v4u*)tile64;
+    v4u* d = (v4u*)(rec + off);
+    for (uint32_t i = lane; i < nb / 16; i += 64)
+      if (off + 16 * i != tl::kRootOffset) d[i] = t4[i];
+    __syncthreads();
+  }
+  const uint64_t root = finish_root(acc, meta);
+  if (lane == 0) {
+    *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32), 0u, 0u};
+    if (a.out_status) a.out_status[b] = TL_ACCEPT;
+  }
+}
+
+// ---- load ---------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
+  __shared__ uint64_t tile64[kMetaTile / 8];
+  const uint32_t* tile32 = (const uint32_t*)tile64;
+  const uint32_t lane = threadIdx.x;
+  const uint32_t b = blockIdx.x;
+  const uint64_t rec = a.rec[b];
+  const uint64_t len = a.len[b];
+  uint32_t code = 0;
+  if (rec == 0) {
+    code = TL_MISSING;
+  } else if ((rec & 15) || ![&] {
+               bool ok = true;
+               for (uint32_t grp = 0; grp < a.g.n_groups; ++grp)
+                 if (a.g.groups_used >> grp & 1) {
+                   const int32_t p = a.tables[(uint64_t)grp * a.n + b];
+                   ok = ok && p >= -1 && (int64_t)p < a.n_pages;
+                 }
+               return ok;
+             }()) {
+    code = TL_BADARG;
+  } else if (len < a.g.record_bytes) {
+    code = TL_TRUNCATED;
+  } else if (len > a.g.record_bytes) {
+    code = TL_OVERLONG;
+  }
+  if (code) {
+    if (lane == 0) a.status[b] = code;
+    return;
+  }
+  const uint32_t meta = (uint32_t)a.g.payload_offset;
+  const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
+  const uint32_t* tok = a.tokens ? a.tokens + (uint64_t)a.g.page_tokens * b : nullptr;
+  const uint64_t bi = a.bidx[b];
+  bool hdr_bad = false, pos_bad = false, key_bad = false, tok_bad = false;
+  uint64_t stored_root = 0;
+  uint64_t acc = root_init(lane);
+  for (uint32_t off = 0; off < meta; off += kMetaTile) {
+    const uint32_t nb = meta - off < kMetaTile ? meta - off : kMetaTile;
+    const v4u* s = (const v4u*)(rec + off);
+    v4u* t4 = (v4u*)tile64;
+    for (uint32_t i = lane; i < nb / 16; i += 64) t4[i] = s[i];
+    __syncthreads();
+    if (off == 0) stored_root = tile64[tl::kRootOffset / 8];
+    for (uint32_t wd = lane; wd < nb / 4; wd += 64) {
+      const uint32_t o = off + 4 * wd;
+      const uint32_t x = tile32[wd];
+      if (o < tl::kHeaderBytes) {
+        if (o == tl::kIndexOffset) pos_bad |= x != (uint32_t)bi;
+        else if (o == tl::kIndexOffset + 4) pos_bad |= x != (uint32_t)(bi >> 32);
+        else if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) key_bad |= x != key32[(o - tl::kKeyOffset) / 4];
+        else if (o == tl::kRootOffset || o == tl::kRootOffset + 4) {}
+        else hdr_bad |= x != a.tmpl[o / 4];
+      } else if (o < a.g.tok_off) {
+        // chunk digests: checked by k_load_seg, covered by the root
+      } else if (o < a.g.tok_end) {
+        if (tok) tok_bad |= x != tok[(o - a.g.tok_off) / 4];
+      } else {
+        hdr_bad |= x != 0;
+      }
+    }
+    hash_tile(tile64, nb, off, lane, acc);
+    __syncthreads();
+  }
+  const bool root_bad = finish_root(acc, meta) != stored_root;
+  if (__any(hdr_bad)) hdr_bad = true;
+  if (__any(pos_bad)) pos_bad = true;
+  if (__any(key_bad)) key_bad = true;
+  if (__any(tok_bad)) tok_bad = true;
+  code = root_bad ? TL_ROOT : hdr_bad ? TL_HEADER : pos_bad ? TL_POSITION : key_bad ? TL_KEY
+                                                                          : tok_bad ? TL_TOKENS : 0;
+  if (lane == 0) a.status[b] = code;
+}
+
+__global__ __launch_bounds__(64 * kSegWaves) void k_load_seg(SegArgs a) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t step = gridDim.x * kSegWaves;
+  for (uint32_t w = blockIdx.x * kSegWaves + uniform(threadIdx.x >> 6); w < a.total; w += step) {
+    const Item it = decode(a, w);
+    if (!page_in_range(it.page, a.n_pages)) continue;  // -1: not restored; else BADARG
+    char* dst = page_chunk(a, it);
+    const uint32_t st = a.status[it.b];
+    if (st & 0xff) {  // rejected by its metadata: never read the record, clear the page
+      zero_rows(dst, it.rows, lane);
+      continue;
+    }
+    const uint64_t rec = a.rec[it.b];
+    const uint64_t leaf = copy_hash(record_chunk(a, rec, it), dst, it.rows, lane);
+    const uint64_t digest = wave_sum64(leaf);
+    if (lane == 0) {
+      const uint64_t want = *(const uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t);
+      if (want != digest) atomicOr(&a.status[it.b], kSegFailBit);
+    }
+  }
+}
+
+struct FinalArgs {
+  SegArgs s;
+  uint8_t* verdicts;
+};
+
+// One workgroup per block: the verdict, and the zero-fill of every page of a
+// block whose chunk check failed (its bytes were already copied).
+__global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
+  const SegArgs& a = f.s;
+  const uint32_t b = blockIdx.x;
+  const uint32_t st = a.status[b];
+  const uint32_t code = (st & 0xff) ? (st & 0xff) : (st & kSegFailBit) ? TL_SEGMENT : TL_ACCEPT;
+  if (threadIdx.x == 0) f.verdicts[b] = (uint8_t)code;
+  if (code != TL_SEGMENT) return;
+  for (uint32_t t = 0; t < a.g.n_seg; ++t) {
+    const Item it = decode(a, b * a.g.n_seg + t);
+    if (!page_in_range(it.page, a.n_pages)) continue;
+    v4u* d = (v4u*)page_chunk(a, it);
+    for (uint32_t i = threadIdx.x; i < it.rows * 64; i += blockDim.x) d[i] = zero4();
+  }
+}
+
+void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, const int32_t* tables,
+              const tl_cache* c, uint32_t* status) {
+  a.g = ctx->geo;
+  a.rec = rec;
+  a.tables = tables;
+  a.lk = c->d_layer_k;
+  a.lv = c->d_layer_v;
+  a.stride = c->page_stride;
+  a.n_pages = c->n_pages;
+  a.n = (uint32_t)n;
+  a.total = (uint32_t)(n * ctx->geo.n_seg);
+  a.status = status;
+}
+
+void fill_meta(MetaArgs& m, const tl_ctx* ctx, size_t n, const uint64_t* rec, const uint64_t* len,
+               const tl_blocks* blk, int64_t n_pages, uint32_t* status, uint8_t* out_status) {
+  m.g = ctx->geo;
+  m.rec = rec;
+  m.len = len;
+  m.keys = blk->d_keys;
+  m.bidx = blk->d_block_index;
+  m.tokens = blk->d_tokens;
+  m.tables = blk->d_tables;
+  m.n_pages = n_pages;
+  m.n = (uint32_t)n;
+  m.status = status;
+  m.out_status = out_status;
+  __builtin_memcpy(m.tmpl, ctx->header_template, sizeof m.tmpl);
+}
+
+int launched() { return hipGetLastError() == hipSuccess ? TL_OK : TL_EDEVICE; }
+
+// Workgroups for a chunk kernel: one wavefront per work item, capped so the
+// grid (in work-items, a 32-bit quantity) stays small; the kernels stride.
+uint32_t seg_grid(uint32_t total) {
+  const uint32_t want = (total + kSegWaves - 1) / kSegWaves;
+  return want < (1u << 20) ? want : (1u << 20);
+}
+
+}  // namespace
+
+namespace tl {
+
+int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
+                const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
+  hipStream_t s = (hipStream_t)stream;
+  SegArgs a;
+  fill_seg(a, ctx, n, d_rec, blk->d_tables, src, nullptr);
+  MetaArgs m;
+  fill_meta(m, ctx, n, d_rec, nullptr, blk, src->n_pages, nullptr, d_status);
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
+  hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  return launched();
+}
+
+int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,
+                const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
+                uint8_t* d_verdicts, uint32_t* d_ws) {
+  hipStream_t s = (hipStream_t)stream;
+  MetaArgs m;
+  fill_meta(m, ctx, n, d_rec, d_len, blk, dst->n_pages, d_ws, nullptr);
+  FinalArgs f;
+  fill_seg(f.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
+  f.verdicts = d_verdicts;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(k_load_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  hipLaunchKernelGGL(k_load_seg, dim3(seg_grid(f.s.total)), dim3(64 * kSegWaves), 0, s, f.s);
+  hipLaunchKernelGGL(k_load_final, dim3((uint32_t)n), dim3(256), 0, s, f);
+  return launched();
+}
+
+}  // namespace tl

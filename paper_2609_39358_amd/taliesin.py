@@ -1,0 +1,305 @@
+"""ctypes binding of libtaliesin.so (include/taliesin.h). Argument marshalling
+only: every step runs in the library (host C++ for keys and the index, HIP
+kernels for save and load). Device arguments are torch tensors (their
+data_ptr()) or raw integer addresses; streams are torch streams, integer
+hipStream_t handles or None (null stream).
+
+The library is required: importing this module without a built
+libtaliesin.so raises ImportError (build it with
+`python -m paper_2609_39358_amd.build`)."""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtaliesin.so")
+
+TL_OK, TL_EINVAL, TL_ELAYOUT, TL_ENOIDENT, TL_EDEVICE, TL_ENOMEM, TL_EFULL, TL_ERANGE = 0, -1, -2, -3, -4, -5, -6, -7
+ACCEPT, MISSING, BADARG, TRUNCATED, OVERLONG = 0x01, 0x10, 0x11, 0x12, 0x13
+ROOT, HEADER, POSITION, KEY, TOKENS, SEGMENT = 0x14, 0x15, 0x16, 0x17, 0x18, 0x19
+DTYPE = {"bf16": 1, "f16": 2, "f32": 3, "fp8": 4}
+KEY_BYTES = 32
+
+
+class TaliesinError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s (%d)" % (what, _lib.tl_status_string(status).decode(), status))
+
+
+class tl_layout(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_uint32), ("n_kv_heads", ctypes.c_uint32),
+                ("head_dim", ctypes.c_uint32), ("dtype", ctypes.c_uint32),
+                ("page_tokens", ctypes.c_uint32),
+                ("layer_window", ctypes.POINTER(ctypes.c_int32)),
+                ("layer_group", ctypes.POINTER(ctypes.c_uint8))]
+
+
+class tl_geometry(ctypes.Structure):
+    _fields_ = [("record_bytes", ctypes.c_uint64), ("payload_offset", ctypes.c_uint64),
+                ("slab_bytes", ctypes.c_uint64), ("n_slabs", ctypes.c_uint32),
+                ("chunks_per_slab", ctypes.c_uint32), ("n_segments", ctypes.c_uint32),
+                ("n_groups", ctypes.c_uint32), ("block_bytes", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32)]
+
+
+class tl_cache(ctypes.Structure):
+    _fields_ = [("d_layer_k", ctypes.c_void_p), ("d_layer_v", ctypes.c_void_p),
+                ("page_stride", ctypes.c_int64), ("n_pages", ctypes.c_int64)]
+
+
+class tl_blocks(ctypes.Structure):
+    _fields_ = [("d_keys", ctypes.c_void_p), ("d_block_index", ctypes.c_void_p),
+                ("d_tokens", ctypes.c_void_p), ("d_tables", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libtaliesin.so is not built (python -m paper_2609_39358_amd.build)")
+    try:  # bind the library's HIP calls to the runtime torch has already loaded
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    lib = ctypes.CDLL(LIB_PATH)
+    c = ctypes
+    P = c.c_void_p
+    sig = {
+        "tl_ctx_create": (P, [P, c.c_size_t, P, c.c_size_t, c.POINTER(tl_layout), c.POINTER(c.c_int)]),
+        "tl_ctx_destroy": (None, [P]),
+        "tl_ctx_geometry": (c.c_int, [P, c.POINTER(tl_geometry)]),
+        "tl_ns_digest": (c.c_int, [P, P]),
+        "tl_workspace_bytes": (c.c_size_t, [P, c.c_size_t]),
+        "tl_block_keys": (c.c_int, [P, P, P, c.c_size_t, c.c_size_t, P, c.c_size_t,
+                                    c.POINTER(c.c_size_t)]),
+        "tl_block_keys_batch": (c.c_int, [P, P, P, P, P, c.c_size_t, c.c_size_t, P, P, P, c.c_int]),
+        "tl_save": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P, P]),
+        "tl_load": (c.c_int, [P, P, c.c_size_t, P, P, c.POINTER(tl_blocks), c.POINTER(tl_cache),
+                              P, P, c.c_size_t]),
+        "tl_index_create": (P, [c.c_size_t]),
+        "tl_index_destroy": (None, [P]),
+        "tl_index_put": (c.c_int, [P, P, c.c_uint64]),
+        "tl_index_get_batch": (c.c_int, [P, P, c.c_size_t, P]),
+        "tl_index_size": (c.c_size_t, [P]),
+        "tl_status_string": (c.c_char_p, [c.c_int]),
+        "tl_verdict_string": (c.c_char_p, [c.c_int]),
+        "tl_abi_version": (c.c_int, []),
+        "tl_test_sha256": (c.c_int, [P, c.c_size_t, c.c_int, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    return lib
+
+
+_lib = _load()
+EXPORTED = (
+    "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
+    "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_load", "tl_index_create",
+    "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
+    "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256")
+
+
+def lib():
+    return _lib
+
+
+def _addr(x) -> Optional[int]:
+    """Device or host address of a torch tensor / numpy array / int / None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if isinstance(x, np.ndarray):
+        return x.ctypes.data
+    raise TypeError("expected a tensor, an array or an address, got %r" % type(x))
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        return None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _host_buf(data) -> bytes:
+    if isinstance(data, (bytes, bytearray, memoryview)):
+        return bytes(data)
+    return np.ascontiguousarray(data).tobytes()
+
+
+def _check(st: int, what: str):
+    if st != TL_OK:
+        raise TaliesinError(st, what)
+
+
+# ------------------------------------------------------------------ context
+class Ctx:
+    """Owns a tl_ctx*. Geometry fields mirror tl_geometry."""
+
+    def __init__(self, handle: int):
+        self._h = handle
+        g = tl_geometry()
+        _check(_lib.tl_ctx_geometry(handle, ctypes.byref(g)), "tl_ctx_geometry")
+        for name, _ in tl_geometry._fields_:
+            setattr(self, name, int(getattr(g, name)))
+
+    @property
+    def handle(self) -> int:
+        return self._h
+
+    def close(self):
+        if self._h:
+            _lib.tl_ctx_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def tl_ctx_create(tenant: bytes, model_fp: bytes, n_layers: int, n_kv_heads: int, head_dim: int,
+                  dtype="bf16", page_tokens: int = 16, layer_window: Optional[Sequence[int]] = None,
+                  layer_group: Optional[Sequence[int]] = None) -> Ctx:
+    lay = tl_layout(n_layers, n_kv_heads, head_dim, DTYPE.get(dtype, dtype), page_tokens)
+    keep = []
+    if layer_window is not None:
+        w = (ctypes.c_int32 * len(layer_window))(*layer_window)
+        keep.append(w)
+        lay.layer_window = ctypes.cast(w, ctypes.POINTER(ctypes.c_int32))
+    if layer_group is not None:
+        g = (ctypes.c_uint8 * len(layer_group))(*layer_group)
+        keep.append(g)
+        lay.layer_group = ctypes.cast(g, ctypes.POINTER(ctypes.c_uint8))
+    st = ctypes.c_int(0)
+    t, f = bytes(tenant), bytes(model_fp)
+    h = _lib.tl_ctx_create(t, len(t), f, len(f), ctypes.byref(lay), ctypes.byref(st))
+    if not h:
+        raise TaliesinError(st.value, "tl_ctx_create")
+    return Ctx(h)
+
+
+def tl_ns_digest(ctx: Ctx) -> bytes:
+    out = ctypes.create_string_buffer(32)
+    _check(_lib.tl_ns_digest(ctx.handle, out), "tl_ns_digest")
+    return out.raw
+
+
+def tl_workspace_bytes(ctx: Ctx, n_blocks: int) -> int:
+    return int(_lib.tl_workspace_bytes(ctx.handle, n_blocks))
+
+
+def tl_block_keys(ctx: Ctx, data, parent: Optional[bytes] = None, block_bytes: int = 0) -> np.ndarray:
+    """Chained keys of every full block of `data`, as uint8 [n, 32]."""
+    buf = _host_buf(data)
+    B = block_bytes or ctx.block_bytes
+    n_full = len(buf) // B
+    out = np.empty((n_full, KEY_BYTES), dtype=np.uint8)
+    nk = ctypes.c_size_t(0)
+    par = None if parent is None else bytes(parent)
+    _check(_lib.tl_block_keys(ctx.handle, par, buf, len(buf), block_bytes, out.ctypes.data, n_full,
+                              ctypes.byref(nk)), "tl_block_keys")
+    return out
+
+
+def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int = 0,
+                        n_threads: int = 0):
+    """Keys for several documents in parallel; returns a list of [n_i, 32] arrays."""
+    bufs = [_host_buf(d) for d in docs]
+    B = block_bytes or ctx.block_bytes
+    lens = np.array([len(b) for b in bufs], dtype=np.uint64)
+    offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.uint64) if bufs else np.zeros(0, np.uint64)
+    nk = lens // np.uint64(B)
+    koff = np.concatenate([[0], np.cumsum(nk)[:-1]]).astype(np.uint64) if bufs else np.zeros(0, np.uint64)
+    allb = b"".join(bufs)
+    keys = np.empty((int(nk.sum()), KEY_BYTES), dtype=np.uint8)
+    nout = np.zeros(len(bufs), dtype=np.uint64)
+    par = None
+    if parents is not None:
+        par = np.ascontiguousarray(np.asarray(parents, dtype=np.uint8).reshape(len(bufs), 32))
+    _check(_lib.tl_block_keys_batch(ctx.handle, None if par is None else par.ctypes.data, allb or None,
+                                    offs.ctypes.data, lens.ctypes.data, len(bufs), block_bytes,
+                                    keys.ctypes.data, koff.ctypes.data, nout.ctypes.data, n_threads),
+           "tl_block_keys_batch")
+    return [keys[int(o):int(o) + int(k)] for o, k in zip(koff, nk)]
+
+
+# ------------------------------------------------------------------ save / load
+def make_cache(d_layer_k, d_layer_v, page_stride: int, n_pages: int) -> tl_cache:
+    return tl_cache(_addr(d_layer_k), _addr(d_layer_v), page_stride, n_pages)
+
+
+def make_blocks(d_keys, d_block_index, d_tokens, d_tables) -> tl_blocks:
+    return tl_blocks(_addr(d_keys), _addr(d_block_index), _addr(d_tokens), _addr(d_tables))
+
+
+def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
+            d_status=None):
+    _check(_lib.tl_save(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src), ctypes.byref(blocks),
+                        _addr(d_record_ptrs), _addr(d_status)), "tl_save")
+
+
+def tl_load(ctx: Ctx, stream, n_blocks: int, d_record_ptrs, d_record_lens, blocks: tl_blocks,
+            dst: tl_cache, d_verdicts, d_workspace, workspace_bytes: int):
+    _check(_lib.tl_load(ctx.handle, _stream(stream), n_blocks, _addr(d_record_ptrs),
+                        _addr(d_record_lens), ctypes.byref(blocks), ctypes.byref(dst),
+                        _addr(d_verdicts), _addr(d_workspace), workspace_bytes), "tl_load")
+
+
+# ------------------------------------------------------------------ index
+class Index:
+    def __init__(self, capacity: int):
+        self._h = _lib.tl_index_create(capacity)
+        if not self._h:
+            raise TaliesinError(TL_ENOMEM, "tl_index_create")
+
+    def put(self, key: bytes, handle: int):
+        _check(_lib.tl_index_put(self._h, bytes(key), handle), "tl_index_put")
+
+    def put_many(self, keys: np.ndarray, handles: Sequence[int]):
+        for k, h in zip(np.asarray(keys, np.uint8).reshape(-1, 32), handles):
+            self.put(k.tobytes(), int(h))
+
+    def get_batch(self, keys: np.ndarray) -> np.ndarray:
+        k = np.ascontiguousarray(np.asarray(keys, dtype=np.uint8).reshape(-1, 32))
+        out = np.empty(k.shape[0], dtype=np.uint64)
+        _check(_lib.tl_index_get_batch(self._h, k.ctypes.data, k.shape[0], out.ctypes.data),
+               "tl_index_get_batch")
+        return out
+
+    def __len__(self):
+        return int(_lib.tl_index_size(self._h))
+
+    def close(self):
+        if self._h:
+            _lib.tl_index_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def tl_index_create(capacity: int) -> Index:
+    return Index(capacity)
+
+
+def sha256_selftest(data: bytes, impl: int) -> Optional[bytes]:
+    out = ctypes.create_string_buffer(32)
+    st = _lib.tl_test_sha256(bytes(data), len(data), impl, out)
+    return out.raw if st == TL_OK else None
+
+
+def verdict_name(v: int) -> str:
+    return _lib.tl_verdict_string(int(v)).decode()

@@ -1,0 +1,196 @@
+"""Host side of libtaliesin, on the CPU: exported symbols, identity gate,
+geometry, namespace digest and key chain against the oracle, the index, and
+argument validation (errors are returned before anything is enqueued, so no
+GPU is touched)."""
+import ctypes
+import hashlib
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import taliesin_ref as ref
+import workloads as wl
+
+T = pytest.importorskip("paper_2609_39358_amd.taliesin")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+TEN, FP = b"tenant-a", b"model-fp-0001"
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "taliesin.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(tl_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert len(names) >= 18
+    lib = ctypes.CDLL(T.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(T.EXPORTED)
+    assert T.lib().tl_abi_version() == 1
+
+
+@pytest.mark.parametrize("impl", [0, 1])
+def test_sha256_both_implementations(impl):
+    from tests.test_oracle_primitives import _kat, _spec_bytes
+    if T.sha256_selftest(b"", impl) is None:
+        pytest.skip("host CPU lacks SHA extensions")
+    for data, want in _kat("sha256_kat.txt"):
+        assert T.sha256_selftest(_spec_bytes(data), impl).hex() == want
+    rng = np.random.default_rng(1)
+    for n in list(range(0, 200)) + [4095, 4096, 4097]:
+        d = rng.integers(0, 256, n, dtype=np.uint8).tobytes()
+        assert T.sha256_selftest(d, impl) == hashlib.sha256(d).digest()
+
+
+def _layout(cfg):
+    g = cfg.geom
+    return ref.Layout(g.n_layers, g.n_kv_heads, g.head_dim, 1, g.page_tokens, g.layer_window, g.layer_group)
+
+
+def _ctx(cfg, tenant=TEN, fp=FP):
+    g = cfg.geom
+    return T.tl_ctx_create(tenant, fp, g.n_layers, g.n_kv_heads, g.head_dim, "bf16", g.page_tokens,
+                           list(g.layer_window) or None, list(g.layer_group) or None)
+
+
+@pytest.mark.parametrize("i", [0, 1, 2, 3, 4])
+def test_geometry_and_namespace_match_oracle(i):
+    cfg = wl.CONFIGS[i]
+    lay = _layout(cfg)
+    c = _ctx(cfg)
+    assert (c.record_bytes, c.payload_offset, c.slab_bytes) == (lay.record_bytes, lay.payload_offset,
+                                                                lay.slab_bytes)
+    assert (c.n_slabs, c.chunks_per_slab, c.n_segments, c.block_bytes) == (
+        lay.n_slabs, lay.chunks_per_slab, lay.n_segments, lay.block_bytes)
+    assert c.n_groups == cfg.geom.n_groups
+    assert T.tl_ns_digest(c) == ref.namespace_digest(TEN, FP, lay)
+
+
+def test_identity_gate_and_layout_errors():
+    for t, f in ((b"", FP), (TEN, b"")):
+        with pytest.raises(T.TaliesinError) as e:
+            T.tl_ctx_create(t, f, 4, 4, 64)
+        assert e.value.status == T.TL_ENOIDENT
+    bad = [dict(n_layers=0), dict(n_layers=257), dict(head_dim=4), dict(dtype=9),
+           dict(page_tokens=0), dict(layer_group=[0, 8, 0, 0]), dict(layer_window=[0, -1, 0, 0])]
+    for kw in bad:
+        args = dict(n_layers=4, n_kv_heads=4, head_dim=64, dtype="bf16", page_tokens=16)
+        args.update(kw)
+        with pytest.raises(T.TaliesinError) as e:
+            T.tl_ctx_create(TEN, FP, **args)
+        assert e.value.status == T.TL_ELAYOUT, kw
+    # the oracle refuses the same layouts
+    with pytest.raises(ref.LayoutError):
+        ref.Layout(4, 4, 4, 1, 16)
+
+
+def test_keys_match_oracle():
+    cfg = wl.CONFIGS[2]
+    c = _ctx(cfg)
+    lay = _layout(cfg)
+    toks = wl.tokens(cfg.n_tokens, cfg.seed)
+    keys = T.tl_block_keys(c, toks)
+    assert keys.shape == (6062, 32)
+    want = ref.block_keys(ref.namespace_digest(TEN, FP, lay), toks.tobytes(), lay.block_bytes)
+    assert [k.tobytes() for k in keys] == want
+    # explicit parent and block size; tail ignored; empty input
+    par = bytes(range(32))
+    k2 = T.tl_block_keys(c, toks[:100], parent=par, block_bytes=40)
+    assert [k.tobytes() for k in k2] == ref.block_keys(par, toks[:100].tobytes(), 40)
+    assert T.tl_block_keys(c, b"").shape == (0, 32)
+
+
+def test_block_keys_capacity_error():
+    c = _ctx(wl.CONFIGS[0])
+    n = ctypes.c_size_t(0)
+    buf = bytes(64 * 3)
+    out = (ctypes.c_uint8 * 64)()
+    st = T.lib().tl_block_keys(c.handle, None, buf, len(buf), 0, out, 2, ctypes.byref(n))
+    assert st == T.TL_ERANGE and n.value == 3
+
+
+def test_batch_keys_match_single_chains():
+    cfg = wl.CONFIGS[3]
+    c = _ctx(cfg)
+    docs = [wl.tokens(n, 5, i) for i, n in enumerate([0, 15, 16, 17, 1000, 4096, 33])]
+    got = T.tl_block_keys_batch(c, docs, n_threads=4)
+    for d, k in zip(docs, got):
+        assert np.array_equal(k, T.tl_block_keys(c, d))
+    pars = np.random.default_rng(0).integers(0, 256, (len(docs), 32), dtype=np.uint8)
+    got = T.tl_block_keys_batch(c, docs, parents=pars, n_threads=3)
+    for d, k, p in zip(docs, got, pars):
+        assert np.array_equal(k, T.tl_block_keys(c, d, parent=p.tobytes()))
+
+
+def test_index_put_get():
+    idx = T.tl_index_create(1000)
+    rng = np.random.default_rng(0)
+    keys = rng.integers(0, 256, (1000, 32), dtype=np.uint8)
+    idx.put_many(keys, range(1000))
+    assert len(idx) == 1000
+    assert np.array_equal(idx.get_batch(keys), np.arange(1000, dtype=np.uint64))
+    miss = rng.integers(0, 256, (50, 32), dtype=np.uint8)
+    assert (idx.get_batch(miss) == np.uint64(2**64 - 1)).all()
+    idx.put(keys[5].tobytes(), 77)  # overwrite keeps the size
+    assert len(idx) == 1000 and idx.get_batch(keys[5:6])[0] == 77
+    with pytest.raises(T.TaliesinError) as e:
+        idx.put(miss[0].tobytes(), 1)
+    assert e.value.status == T.TL_EFULL
+    # keys sharing their first 8 bytes still resolve (probe sequence)
+    k2 = np.zeros((20, 32), np.uint8)
+    k2[:, 31] = np.arange(20)
+    j = T.tl_index_create(20)
+    j.put_many(k2, range(100, 120))
+    assert np.array_equal(j.get_batch(k2), np.arange(100, 120, dtype=np.uint64))
+
+
+def test_save_load_argument_validation_enqueues_nothing():
+    c = _ctx(wl.CONFIGS[0])
+    L = T.lib()
+    good_cache = T.make_cache(0x10000, 0x20000, c.slab_bytes, 128)
+    good_blk = T.make_blocks(0x30000, 0x40000, 0x50000, 0x60000)
+    ws = T.tl_workspace_bytes(c, 64)
+    assert ws == 256
+    P = ctypes.byref
+
+    def load(n=64, rec=0x70000, lens=0x80000, blk=good_blk, cache=good_cache, verd=0x90000,
+             wsp=0xA0000, wsb=ws):
+        return L.tl_load(c.handle, None, n, rec, lens, P(blk), P(cache), verd, wsp, wsb)
+
+    def save(n=64, cache=good_cache, blk=good_blk, rec=0x70000):
+        return L.tl_save(c.handle, None, n, P(cache), P(blk), rec, None)
+
+    assert load(n=0) == T.TL_OK and save(n=0) == T.TL_OK  # nothing to do
+    assert load(rec=None) == T.TL_EINVAL
+    assert load(lens=None) == T.TL_EINVAL
+    assert load(verd=None) == T.TL_EINVAL
+    assert load(wsp=None) == T.TL_EINVAL
+    assert load(wsb=ws - 1) == T.TL_ERANGE
+    assert load(wsp=0xA0002) == T.TL_EINVAL
+    assert load(rec=0x70004) == T.TL_EINVAL
+    assert load(cache=T.make_cache(0x10000, 0x20000, c.slab_bytes - 16, 128)) == T.TL_EINVAL
+    assert load(cache=T.make_cache(0x10000, 0x20000, c.slab_bytes + 8, 128)) == T.TL_EINVAL
+    assert load(cache=T.make_cache(0x10000, 0x20000, c.slab_bytes, -1)) == T.TL_EINVAL
+    assert load(cache=T.make_cache(None, 0x20000, c.slab_bytes, 128)) == T.TL_EINVAL
+    assert load(blk=T.make_blocks(None, 0x40000, 0x50000, 0x60000)) == T.TL_EINVAL
+    assert load(blk=T.make_blocks(0x30001, 0x40000, 0x50000, 0x60000)) == T.TL_EINVAL
+    assert load(blk=T.make_blocks(0x30000, 0x40004, 0x50000, 0x60000)) == T.TL_EINVAL
+    assert save(blk=T.make_blocks(0x30000, 0x40000, None, 0x60000)) == T.TL_EINVAL
+    assert save(rec=None) == T.TL_EINVAL
+    assert L.tl_load(None, None, 1, 1, 1, None, None, 1, 1, 1) == T.TL_EINVAL
+    # grid index must fit in 32 bits
+    assert load(n=(1 << 32) // c.n_segments + 1, wsb=1 << 40) == T.TL_ERANGE
+
+
+def test_status_and_verdict_strings():
+    assert T.verdict_name(T.ACCEPT) == "ACCEPT"
+    assert T.verdict_name(T.SEGMENT) == "SEGMENT"
+    assert T.verdict_name(0x77) == "UNKNOWN"
+    for code, name in ref.VERDICT_NAMES.items():
+        assert T.verdict_name(code) == name
