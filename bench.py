@@ -1,0 +1,264 @@
+#!/usr/bin/env python
+"""Benchmark of the Taliesin hot path on one MI355X.
+
+One step = one verified restore of the whole paper-scale corpus (97,000
+tokens, 60 layers, 16 KV heads, head_dim 128, bf16, 16-token pages: 6,062
+full blocks, 47.7 GB of KV): chained block keys (host C++), index lookup
+(host C++), upload of the per-block pointer/length/key arrays, and tl_load
+(metadata checks, fused copy + tree-XXH64 verify + scatter, verdicts). Records
+are resident in HBM before the timed region (saved by tl_save; save
+throughput is reported separately). Inputs are seeded synthetic tensors.
+
+Prints one JSON line. `value` is algorithmic GB/s of the step: record bytes
+read + payload bytes written per block, over the measured step time.
+"""
+import argparse
+import hashlib
+import json
+import os
+import resource
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "KV restore+verify GB/s (and prefill tokens avoided/s), % of HBM peak"
+HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "load_seg_paper_corpus_traffic.json")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_39358_amd", "csrc", "kernels.hip")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def stored_traffic():
+    """Measured HBM bytes of k_load_seg from committed rocprofv3 counters, if
+    they were taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return t.get("traffic_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--save-steps", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-blocks", type=int, default=256)
+    ap.add_argument("--no-copy-ceiling", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one MI355X: this build has no multi-GPU path "
+              "(--gpus %d is not supported; run with --gpus 1)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py is single-process; WORLD_SIZE > 1 is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2609_39358_amd import taliesin as T
+    from paper_2609_39358_amd.device import PagedCache, RecordStore
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = "cuda"
+    cfg = wl.CONFIGS[2]
+    g = cfg.geom
+    P = g.page_tokens
+    tokens = wl.tokens(cfg.n_tokens, cfg.seed)
+    ctx = T.tl_ctx_create(b"bench-tenant", b"gemma-31b-class-fp", g.n_layers, g.n_kv_heads, g.head_dim,
+                          g.dtype, P)
+    n = cfg.n_tokens // P
+    rb = ctx.record_bytes
+    payload = ctx.n_slabs * ctx.slab_bytes
+    step_bytes = n * (rb + payload)  # records read + pages written
+    log("workload paper_corpus: %d tokens, %d blocks, record %d B, step %.2f GB"
+        % (cfg.n_tokens, n, rb, step_bytes / 1e9))
+
+    # ---- inputs resident in HBM: source cache, records (saved), block arrays
+    stream = torch.cuda.current_stream()
+    src = PagedCache(g.n_layers, cfg.src_pages, ctx.slab_bytes, dev)
+    for l in range(g.n_layers):
+        for kv, t in ((0, src.k[l]), (1, src.v[l])):
+            t.copy_(wl.kv_layer_torch(cfg.src_pages, g, cfg.seed, l, kv, dev).view(torch.uint8)
+                    .reshape(cfg.src_pages, -1))
+    keys0 = T.tl_block_keys(ctx, tokens)
+    d_keys0 = torch.from_numpy(keys0).to(dev)
+    d_bidx = torch.arange(n, dtype=torch.int64, device=dev)
+    d_tokens = torch.from_numpy(tokens[:n * P].view(np.int32).reshape(n, P).copy()).to(dev)
+    d_tsrc = torch.from_numpy(wl.page_table(n, cfg.src_pages, cfg.seed, 0)[None, :]).to(dev)
+    d_tdst = torch.from_numpy(wl.page_table(n, cfg.dst_pages, cfg.seed, 1)[None, :]).to(dev)
+    store = RecordStore(n, rb, dev)
+    save_blocks = T.make_blocks(d_keys0, d_bidx, d_tokens, d_tsrc)
+    d_status = torch.zeros(n, dtype=torch.uint8, device=dev)
+
+    # ---- save (reported separately)
+    T.tl_timing(True)
+    T.tl_save(ctx, stream, n, src.tl(), save_blocks, store.ptrs, d_status)
+    torch.cuda.synchronize()
+    assert (d_status == T.ACCEPT).all().item(), "save failed"
+    T.tl_timing_read("save_seg"), T.tl_timing_read("save_meta")
+    t0 = time.perf_counter()
+    for _ in range(args.save_steps):
+        T.tl_save(ctx, stream, n, src.tl(), save_blocks, store.ptrs, d_status)
+    torch.cuda.synchronize()
+    save_ms = (time.perf_counter() - t0) * 1e3 / max(args.save_steps, 1)
+    ss_ms, ss_n = T.tl_timing_read("save_seg")
+    sm_ms, sm_n = T.tl_timing_read("save_meta")
+    save = {"GBps": step_bytes / (save_ms * 1e-3) / 1e9, "ms": save_ms,
+            "save_seg_ms": ss_ms / max(ss_n, 1), "save_meta_ms": sm_ms / max(sm_n, 1),
+            "hbm_frac": step_bytes / (save_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+    log("save: %.3f ms/step, %.0f GB/s" % (save_ms, save["GBps"]))
+
+    # ---- the store's index: key -> record slot
+    idx = T.tl_index_create(n)
+    idx.put_many(keys0, range(n))
+    rec_base = store.buf.data_ptr()
+    del src, save_blocks  # the load does not need the source cache
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    dst = PagedCache(g.n_layers, cfg.dst_pages, ctx.slab_bytes, dev)
+    ws_bytes = T.tl_workspace_bytes(ctx, n)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    verd = torch.zeros(n, dtype=torch.uint8, device=dev)
+    # double-buffered pinned staging for the per-step host->device arrays
+    stage = []
+    for _ in range(2):
+        h = {"ptrs": torch.empty(n, dtype=torch.int64, pin_memory=True),
+             "lens": torch.empty(n, dtype=torch.int64, pin_memory=True),
+             "keys": torch.empty((n, 32), dtype=torch.uint8, pin_memory=True)}
+        d = {k: torch.empty_like(v, device=dev) for k, v in h.items()}
+        stage.append((h, d, torch.cuda.Event()))
+    miss = np.uint64(2**64 - 1)
+
+    def step(i):
+        h, d, ev = stage[i & 1]
+        ev.synchronize()  # the copy that last read this staging set is done
+        keys = T.tl_block_keys(ctx, tokens)  # a1
+        handles = idx.get_batch(keys)  # a2
+        hit = handles != miss
+        ptrs = np.where(hit, np.uint64(rec_base) + handles * np.uint64(rb), np.uint64(0))
+        h["ptrs"].numpy()[:] = ptrs.view(np.int64)
+        h["lens"].numpy()[:] = np.where(hit, rb, 0)
+        h["keys"].numpy()[:] = keys
+        for k in d:
+            d[k].copy_(h[k], non_blocking=True)
+        ev.record(stream)
+        blocks = T.make_blocks(d["keys"], d_bidx, d_tokens, d_tdst)
+        T.tl_load(ctx, stream, n, d["ptrs"], d["lens"], blocks, dst.tl(), verd, ws, ws_bytes)  # a3-a5
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    assert (verd == T.ACCEPT).all().item(), "verification rejected blocks of an undamaged corpus"
+    for k in T.KERNELS:
+        T.tl_timing_read(k)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = dt * 1e3 / args.steps
+    kern = {}
+    for k in ("load_meta", "load_seg", "load_final"):
+        ms, cnt = T.tl_timing_read(k)
+        kern[k] = ms / max(cnt, 1)
+    T.tl_timing(False)
+    assert (verd == T.ACCEPT).all().item()
+    gbps = step_bytes / (ms_step * 1e-3) / 1e9
+    tokens_avoided = n * P
+    log("load step: %.3f ms, %.0f GB/s, kernels %s" % (ms_step, gbps, kern))
+
+    # dominant kernel: algorithmic bytes of k_load_seg per launch
+    seg_bytes = n * ctx.n_segments * (2 * 65536 + 8)
+    seg_gbps = seg_bytes / (kern["load_seg"] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": seg_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": seg_gbps / HBM_PEAK_GBPS, "traffic": stored_traffic(),
+                "kernel": "k_load_seg", "algorithmic_bytes_per_launch": seg_bytes,
+                "avg_launch_ms": kern["load_seg"]}
+
+    # ---- practical ceiling: a device-to-device copy of the same byte count
+    copy = None
+    if not args.no_copy_ceiling:
+        half = payload * n // 2
+        a = torch.empty(half, dtype=torch.uint8, device=dev)
+        b = store.buf.view(-1)[:half]
+        a.copy_(b)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(5):
+            a.copy_(b)
+        torch.cuda.synchronize()
+        cms = (time.perf_counter() - t0) * 1e3 / 5
+        copy = {"bytes_read_plus_written": 2 * half, "ms": cms, "GBps": 2 * half / (cms * 1e-3) / 1e9}
+        del a
+        log("copy ceiling: %.0f GB/s" % copy["GBps"])
+
+    # ---- CPU baseline: the oracle on a bounded sample of the same workload
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import taliesin_ref as ref
+
+        m = min(args.cpu_sample_blocks, n)
+        lay = ref.Layout(g.n_layers, g.n_kv_heads, g.head_dim, 1, P)
+        ns = T.tl_ns_digest(ctx)
+        recs = [bytes(store.buf[b].cpu().numpy()) for b in range(m)]
+        hk = [np.zeros((m, ctx.slab_bytes), np.uint8) for _ in range(g.n_layers)]
+        hv = [np.zeros((m, ctx.slab_bytes), np.uint8) for _ in range(g.n_layers)]
+        table = np.arange(m, dtype=np.int32)[None, :]
+        toks = tokens[:m * P].reshape(m, P)
+        ru0 = resource.getrusage(resource.RUSAGE_SELF)
+        t0 = time.perf_counter()
+        vs = ref.restore(lay, ns, recs, [k.tobytes() for k in keys0[:m]], np.arange(m), toks, table, hk, hv)
+        cdt = time.perf_counter() - t0
+        ru1 = resource.getrusage(resource.RUSAGE_SELF)
+        assert vs == [ref.ACCEPT] * m
+        cpu_s = (ru1.ru_utime - ru0.ru_utime) + (ru1.ru_stime - ru0.ru_stime)
+        cpu = {"value": m * (rb + payload) / cdt / 1e9, "unit": "GB/s",
+               "cores": max(1, round(cpu_s / cdt)), "kind": "oracle",
+               "sample": "verify+restore of %d of %d blocks (%.2f GB of records) on the host, "
+                         "single process" % (m, n, m * rb / 1e9),
+               "seconds": cdt, "tokens_avoided_per_s": m * P / cdt}
+        log("cpu oracle: %.2f GB/s over %.1f s" % (cpu["value"], cdt))
+
+    out = {
+        "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic",
+        "config": {"workload": "paper_corpus_97k_tokens", "n_tokens": cfg.n_tokens, "blocks": n,
+                   "tail_tokens_recomputed": cfg.n_tokens - n * P, "n_layers": g.n_layers,
+                   "n_kv_heads": g.n_kv_heads, "head_dim": g.head_dim, "page_tokens": P,
+                   "kv_dtype": "bf16", "record_bytes": rb, "step_bytes": step_bytes,
+                   "parallelism": "single GPU"},
+        "hbm_frac": gbps / HBM_PEAK_GBPS,
+        "tokens_avoided_per_s": tokens_avoided / (ms_step * 1e-3),
+        "kernel_ms": kern,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "save": save,
+        "copy_ceiling": copy,
+        "kernel_source_sha256_16": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -219,6 +219,22 @@ int tl_index_put(tl_index* idx, const uint8_t key[TL_KEY_BYTES], uint64_t handle
 int tl_index_get_batch(const tl_index* idx, const uint8_t* keys, size_t n, uint64_t* handles_out);
 size_t tl_index_size(const tl_index* idx);
 
+/* ---- profiling ------------------------------------------------------------
+ * Opt-in kernel timing for benchmarks: while enabled (process-wide), every
+ * kernel launch is bracketed by two HIP events recorded on the launch stream.
+ * tl_timing returns the previous setting. tl_timing_read waits for the
+ * recorded events of one kernel, returns the summed milliseconds and the
+ * number of launches, and forgets them. Disabled by default; costs two event
+ * records per launch when enabled. */
+#define TL_KERNEL_SAVE_SEG 0
+#define TL_KERNEL_SAVE_META 1
+#define TL_KERNEL_LOAD_META 2
+#define TL_KERNEL_LOAD_SEG 3
+#define TL_KERNEL_LOAD_FINAL 4
+#define TL_KERNEL_COUNT 5
+int tl_timing(int enable);
+int tl_timing_read(int kernel, double* total_ms, uint64_t* count);
+
 /* ---- misc ---------------------------------------------------------------- */
 const char* tl_status_string(int status);
 const char* tl_verdict_string(int verdict);

@@ -23,6 +23,9 @@
 // specification); the tree arrangement is this library's record format.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+#include <vector>
+
 #include "internal.h"
 
 namespace {
@@ -504,6 +507,34 @@ void fill_meta(MetaArgs& m, const tl_ctx* ctx, size_t n, const uint64_t* rec, co
 
 int launched() { return hipGetLastError() == hipSuccess ? TL_OK : TL_EDEVICE; }
 
+// Opt-in per-kernel timing: when on, every launch is bracketed by a pair of
+// HIP events recorded on the launch stream; tl_timing_read sums them.
+struct EventPair {
+  hipEvent_t a, b;
+};
+std::mutex g_timing_mu;
+bool g_timing_on = false;
+std::vector<EventPair> g_events[TL_KERNEL_COUNT];
+
+template <typename F>
+void timed(int kernel, hipStream_t s, F&& launch) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    on = g_timing_on;
+  }
+  EventPair p{nullptr, nullptr};
+  if (on && hipEventCreate(&p.a) == hipSuccess && hipEventCreate(&p.b) == hipSuccess) {
+    (void)hipEventRecord(p.a, s);
+    launch();
+    (void)hipEventRecord(p.b, s);
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    g_events[kernel].push_back(p);
+  } else {
+    launch();
+  }
+}
+
 // Workgroups for a chunk kernel: one wavefront per work item, capped so the
 // grid (in work-items, a 32-bit quantity) stays small; the kernels stride.
 uint32_t seg_grid(uint32_t total) {
@@ -523,8 +554,12 @@ int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
   MetaArgs m;
   fill_meta(m, ctx, n, d_rec, nullptr, blk, src->n_pages, nullptr, d_status);
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
-  hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  timed(TL_KERNEL_SAVE_SEG, s, [&] {
+    hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
+  });
+  timed(TL_KERNEL_SAVE_META, s, [&] {
+    hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  });
   return launched();
 }
 
@@ -538,10 +573,45 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
   fill_seg(f.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
   f.verdicts = d_verdicts;
   (void)hipGetLastError();
-  hipLaunchKernelGGL(k_load_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
-  hipLaunchKernelGGL(k_load_seg, dim3(seg_grid(f.s.total)), dim3(64 * kSegWaves), 0, s, f.s);
-  hipLaunchKernelGGL(k_load_final, dim3((uint32_t)n), dim3(256), 0, s, f);
+  timed(TL_KERNEL_LOAD_META, s, [&] {
+    hipLaunchKernelGGL(k_load_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  });
+  timed(TL_KERNEL_LOAD_SEG, s, [&] {
+    hipLaunchKernelGGL(k_load_seg, dim3(seg_grid(f.s.total)), dim3(64 * kSegWaves), 0, s, f.s);
+  });
+  timed(TL_KERNEL_LOAD_FINAL, s, [&] {
+    hipLaunchKernelGGL(k_load_final, dim3((uint32_t)n), dim3(256), 0, s, f);
+  });
   return launched();
 }
 
 }  // namespace tl
+
+extern "C" int tl_timing(int enable) {
+  std::lock_guard<std::mutex> g(g_timing_mu);
+  const int prev = g_timing_on;
+  g_timing_on = enable != 0;
+  return prev;
+}
+
+extern "C" int tl_timing_read(int kernel, double* total_ms, uint64_t* count) {
+  if (kernel < 0 || kernel >= TL_KERNEL_COUNT || !total_ms || !count) return TL_EINVAL;
+  std::vector<EventPair> ev;
+  {
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    ev.swap(g_events[kernel]);
+  }
+  double sum = 0;
+  int st = TL_OK;
+  for (const EventPair& p : ev) {
+    float ms = 0;
+    if (hipEventSynchronize(p.b) != hipSuccess || hipEventElapsedTime(&ms, p.a, p.b) != hipSuccess)
+      st = TL_EDEVICE;
+    sum += ms;
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  *total_ms = sum;
+  *count = ev.size();
+  return st;
+}

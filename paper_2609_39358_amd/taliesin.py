@@ -88,6 +88,8 @@ def _load():
         "tl_verdict_string": (c.c_char_p, [c.c_int]),
         "tl_abi_version": (c.c_int, []),
         "tl_test_sha256": (c.c_int, [P, c.c_size_t, c.c_int, P]),
+        "tl_timing": (c.c_int, [c.c_int]),
+        "tl_timing_read": (c.c_int, [c.c_int, c.POINTER(c.c_double), c.POINTER(c.c_uint64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -101,7 +103,9 @@ EXPORTED = (
     "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
     "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_load", "tl_index_create",
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
-    "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256")
+    "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
+    "tl_timing_read")
+KERNELS = {"save_seg": 0, "save_meta": 1, "load_meta": 2, "load_seg": 3, "load_final": 4}
 
 
 def lib():
@@ -235,11 +239,15 @@ def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int
 
 # ------------------------------------------------------------------ save / load
 def make_cache(d_layer_k, d_layer_v, page_stride: int, n_pages: int) -> tl_cache:
-    return tl_cache(_addr(d_layer_k), _addr(d_layer_v), page_stride, n_pages)
+    c = tl_cache(_addr(d_layer_k), _addr(d_layer_v), page_stride, n_pages)
+    c._keep = (d_layer_k, d_layer_v)  # the buffers must outlive the enqueued kernels
+    return c
 
 
 def make_blocks(d_keys, d_block_index, d_tokens, d_tables) -> tl_blocks:
-    return tl_blocks(_addr(d_keys), _addr(d_block_index), _addr(d_tokens), _addr(d_tables))
+    b = tl_blocks(_addr(d_keys), _addr(d_block_index), _addr(d_tokens), _addr(d_tables))
+    b._keep = (d_keys, d_block_index, d_tokens, d_tables)
+    return b
 
 
 def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
@@ -303,3 +311,14 @@ def sha256_selftest(data: bytes, impl: int) -> Optional[bytes]:
 
 def verdict_name(v: int) -> str:
     return _lib.tl_verdict_string(int(v)).decode()
+
+
+def tl_timing(enable: bool) -> bool:
+    return bool(_lib.tl_timing(1 if enable else 0))
+
+
+def tl_timing_read(kernel: str):
+    """(summed milliseconds, launches) of one kernel since the last read."""
+    ms, n = ctypes.c_double(0), ctypes.c_uint64(0)
+    _check(_lib.tl_timing_read(KERNELS[kernel], ctypes.byref(ms), ctypes.byref(n)), "tl_timing_read")
+    return ms.value, int(n.value)
