@@ -58,7 +58,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--save-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-blocks", type=int, default=256)
+    ap.add_argument("--cpu-sample-blocks", type=int, default=1536)
     ap.add_argument("--no-copy-ceiling", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
