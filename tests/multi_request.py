@@ -1,0 +1,138 @@
+"""The multi-request restore pipeline on the GPU: base documents are saved
+once; every request computes its chained keys, looks them up in the index and
+restores the hits into a shared page pool, batch by batch; damaged records
+must be rejected. Used by the multi-request GPU tests."""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Dict, List
+
+import numpy as np
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import taliesin as T
+from paper_2609_39358_amd.device import PagedCache, RecordStore
+from tests.gpu_case import DEV, FP, TEN, ctx_of, fill_cache, i32, i64, layout_of, log
+
+
+@dataclass
+class Batch:
+    requests: List[int]
+    blocks: List[tuple] = field(default_factory=list)  # (request, position, record id, pool page)
+    verdicts: np.ndarray = None
+
+
+class MultiRun:
+    def __init__(self, w: wl.MultiWorkload, pool_pages: int, seed: int = 3):
+        self.w, self.g = w, w.geom
+        g = self.g
+        self.lay = layout_of(g)
+        self.ctx = ctx_of(g)
+        self.ns = ref.namespace_digest(TEN, FP, self.lay)
+        P = g.page_tokens
+        self.bpd = len(w.base_docs[0]) // P  # full blocks per base document
+        self.n_stored = len(w.base_docs) * self.bpd
+        self.rb = self.lay.record_bytes
+        self.pool_pages = pool_pages
+        # base documents: source pages (random placement), keys, records
+        self.src_table = wl.page_table(self.n_stored, self.n_stored, seed, 7)
+        log("multi-request: %d stored records of %d B, pool %d pages" % (self.n_stored, self.rb, pool_pages))
+        self.src = fill_cache(PagedCache(g.n_layers, self.n_stored, self.lay.slab_bytes, DEV), g, seed)
+        base_keys = T.tl_block_keys_batch(self.ctx, w.base_docs)
+        self.keys = np.concatenate(base_keys)
+        self.bidx = np.tile(np.arange(self.bpd, dtype=np.uint64), len(w.base_docs))
+        self.tokens = np.concatenate([d[:self.bpd * P].reshape(self.bpd, P) for d in w.base_docs])
+        self.store = RecordStore(self.n_stored, self.rb, DEV)
+        st = torch.zeros(self.n_stored, dtype=torch.uint8, device=DEV)
+        self._save_in = (torch.from_numpy(self.keys).to(DEV), i64(self.bidx),
+                         i32(self.tokens.view(np.int32)), i32(self.src_table[None, :]))
+        T.tl_save(self.ctx, torch.cuda.current_stream(), self.n_stored, self.src.tl(),
+                  T.make_blocks(*self._save_in), self.store.ptrs, st)
+        torch.cuda.synchronize()
+        assert (st == ref.ACCEPT).all().item()
+        # damage: bit flips in place, truncations as shorter reported lengths
+        self.lens = np.full(self.n_stored, self.rb, np.uint64)
+        self.flip_bits: Dict[int, int] = {}
+        for rid, frac in w.corrupt_flip:
+            bit = wl.scale_bit(frac, self.rb)
+            self.flip_bits[rid] = bit
+            self.store.buf[rid, bit >> 3] ^= 1 << (bit & 7)
+        for rid, frac in w.corrupt_trunc:
+            self.lens[rid] = wl.scale_len(frac, self.rb)
+        self.index = T.tl_index_create(self.n_stored)
+        self.index.put_many(self.keys, range(self.n_stored))
+        self.dst = PagedCache(g.n_layers, pool_pages, self.lay.slab_bytes, DEV)
+
+    def run(self, check=None):
+        """Restore every request's hits, admission batch by admission batch.
+        `check(batch)` is called after each batch (pages still in the pool)."""
+        w, P = self.w, self.g.page_tokens
+        req_keys = T.tl_block_keys_batch(self.ctx, [q.tokens for q in w.requests])
+        batches = wl.admission_batches(w.requests, self.pool_pages)
+        base = self.store.buf.data_ptr()
+        ws = torch.empty(max(T.tl_workspace_bytes(self.ctx, self.pool_pages), 4), dtype=torch.uint8,
+                         device=DEV)
+        out = []
+        for bi, reqs in enumerate(batches):
+            b = Batch(reqs)
+            keys, bidx, toks, rids = [], [], [], []
+            for r in reqs:
+                q = w.requests[r]
+                h = self.index.get_batch(req_keys[r])
+                hit = h != np.uint64(2**64 - 1)
+                n_hit = int(np.argmin(hit)) if not hit.all() else len(hit)
+                assert hit[:n_hit].all() and not hit[n_hit:].any()  # hits are exactly a prefix
+                assert n_hit == q.shared_blocks, (r, n_hit, q.shared_blocks)
+                for i in range(n_hit):
+                    b.blocks.append((r, i, int(h[i]), len(b.blocks)))
+                keys.append(req_keys[r][:n_hit])
+                bidx.append(np.arange(n_hit, dtype=np.uint64))
+                toks.append(q.tokens[:n_hit * P].reshape(n_hit, P))
+                rids.append(h[:n_hit].astype(np.int64))
+            n = len(b.blocks)
+            if n == 0:
+                b.verdicts = np.zeros(0, np.uint8)
+                out.append(b)
+                continue
+            rid = np.concatenate(rids)
+            ptrs = i64(np.uint64(base) + rid.astype(np.uint64) * np.uint64(self.rb))
+            lens = i64(self.lens[rid])
+            table = np.arange(n, dtype=np.int32)[None, :]
+            d_keys = torch.from_numpy(np.ascontiguousarray(np.concatenate(keys))).to(DEV)
+            d_bidx, d_tok = i64(np.concatenate(bidx)), i32(np.concatenate(toks).view(np.int32))
+            d_tab = i32(table)
+            verd = torch.zeros(n, dtype=torch.uint8, device=DEV)
+            log("batch %d: %d requests, %d blocks" % (bi, len(reqs), n))
+            T.tl_load(self.ctx, torch.cuda.current_stream(), n, ptrs, lens,
+                      T.make_blocks(d_keys, d_bidx, d_tok, d_tab), self.dst.tl(), verd, ws, ws.numel())
+            torch.cuda.synchronize()
+            b.verdicts = verd.cpu().numpy()
+            if check:
+                check(b)
+            out.append(b)
+        return out
+
+    def oracle_verdict(self, rid: int) -> int:
+        """The oracle's verdict for stored record rid loaded at its own position."""
+        rec = self.store.buf[rid].cpu().numpy().tobytes()[:int(self.lens[rid])]
+        return ref.verify(self.lay, self.ns, rec, self.keys[rid].tobytes(), int(self.bidx[rid]),
+                          self.tokens[rid], range(self.lay.n_slabs))
+
+    def check_pages(self, b: Batch, rejected: set):
+        """Accepted blocks' pool pages equal their source pages; rejected ones are zero."""
+        slab = self.lay.slab_bytes
+        acc = [(blk[2], blk[3]) for blk, v in zip(b.blocks, b.verdicts) if v == ref.ACCEPT]
+        rej = [blk[3] for blk, v in zip(b.blocks, b.verdicts) if v != ref.ACCEPT]
+        assert {blk[2] for blk, v in zip(b.blocks, b.verdicts) if v != ref.ACCEPT} <= rejected
+        if acc:
+            src_p = torch.from_numpy(self.src_table[[a for a, _ in acc]].astype(np.int64)).to(DEV)
+            dst_p = torch.from_numpy(np.array([p for _, p in acc], np.int64)).to(DEV)
+            for l in range(self.g.n_layers):
+                assert torch.equal(self.dst.k[l][dst_p, :slab], self.src.k[l][src_p, :slab]), l
+                assert torch.equal(self.dst.v[l][dst_p, :slab], self.src.v[l][src_p, :slab]), l
+        if rej:
+            rp = torch.from_numpy(np.array(rej, np.int64)).to(DEV)
+            for l in range(self.g.n_layers):
+                assert not self.dst.k[l][rp].any().item() and not self.dst.v[l][rp].any().item()

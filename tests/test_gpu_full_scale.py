@@ -1,0 +1,158 @@
+"""Full-size GPU parity on the paper-corpus and hybrid workloads, in the same
+library calls the benchmark times. At these sizes the oracle checks sampled
+blocks one by one (records byte for byte, verdicts, restored pages); every
+block is checked by properties that hold at any size (all verdicts, and
+destination pages equal the source pages under the two block tables)."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import taliesin as T
+from paper_2609_39358_amd.device import PagedCache, RecordStore
+from tests.gpu_case import DEV, Case, i32, i64, log
+
+pytestmark = pytest.mark.gpu
+
+
+def sample_blocks(n, k, seed):
+    r = np.random.default_rng(seed)
+    return sorted({0, n - 1, *r.choice(n, size=k, replace=False).tolist()})
+
+
+def oracle_record(c: Case, b: int):
+    """The oracle's record for block b, from host copies of just its pages."""
+    G = c.geom.n_groups
+    hk, hv = [], []
+    for l in range(c.geom.n_layers):
+        p = int(c.t_src[c.geom.group(l)][b])
+        hk.append(c.src.k[l][p:p + 1].cpu().numpy())
+        hv.append(c.src.v[l][p:p + 1].cpu().numpy())
+    recs, st = ref.save(c.lay, c.ns, hk, hv, np.zeros((G, 1), np.int32), [c.keys[b].tobytes()],
+                        [int(c.bidx[b])], c.tokens[b:b + 1], n_pages=1)
+    assert st == [ref.ACCEPT]
+    return recs[0]
+
+
+def check_pages_equal(c: Case, dst: PagedCache, tables, blocks=None):
+    """dst page tables[g(l)][b] == src page t_src[g(l)][b] for every read slab."""
+    slab = c.lay.slab_bytes
+    for l in range(c.geom.n_layers):
+        grp = c.geom.group(l)
+        td = np.asarray(tables[grp])
+        sel = np.nonzero(td >= 0)[0] if blocks is None else np.array([b for b in blocks if td[b] >= 0])
+        if sel.size == 0:
+            continue
+        ts = torch.from_numpy(c.t_src[grp][sel].astype(np.int64)).to(DEV)
+        tdd = torch.from_numpy(td[sel].astype(np.int64)).to(DEV)
+        for s_t, d_t in ((c.src.k[l], dst.k[l]), (c.src.v[l], dst.v[l])):
+            assert torch.equal(d_t[tdd, :slab], s_t[ts, :slab]), ("layer", l)
+
+
+def test_paper_corpus_full_scale():
+    cfg = wl.CONFIGS[2]
+    n = cfg.n_tokens // cfg.geom.page_tokens
+    c = Case(cfg.geom, n, cfg.src_pages, cfg.dst_pages, cfg.seed)
+    log("paper corpus: %d blocks, %.1f GB of records" % (n, n * c.lay.record_bytes / 1e9))
+    # keys of the whole corpus (tail tokens unkeyed) against the oracle's chain
+    toks = wl.tokens(cfg.n_tokens, cfg.seed)
+    keys = T.tl_block_keys(c.ctx, toks)
+    assert [k.tobytes() for k in keys] == ref.block_keys(c.ns, toks.tobytes(), c.lay.block_bytes)
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    samp = sample_blocks(n, 10, 1)
+    rb = c.lay.record_bytes
+    for b in samp:
+        assert store.buf[b].cpu().numpy().tobytes() == oracle_record(c, b), b
+    # damage three sampled records (metadata bit, payload bit, truncation)
+    dmg = {samp[1]: ("bit", 77 * 8 + 3), samp[2]: ("bit", (rb - 5) * 8 + 6), samp[3]: ("trunc", rb - 1)}
+    lens = np.full(n, rb, np.uint64)
+    host_rec = {}
+    for b in samp:
+        host_rec[b] = bytearray(store.buf[b].cpu().numpy().tobytes())
+    for b, (kind, x) in dmg.items():
+        if kind == "bit":
+            store.buf[b, x >> 3] ^= 1 << (x & 7)
+            host_rec[b][x >> 3] ^= 1 << (x & 7)
+        else:
+            lens[b] = x
+    dst = PagedCache(c.geom.n_layers, cfg.dst_pages, c.stride, DEV)
+    for t in dst.k + dst.v:
+        t.fill_(0x5A)
+    v = c.load(store.ptrs, i64(lens), c.t_dst, dst)
+    want = {b: ref.verify(c.lay, c.ns, bytes(host_rec[b][:int(lens[b])]), c.keys[b].tobytes(), b,
+                          c.tokens[b], range(c.lay.n_slabs)) for b in samp}
+    for b in samp:
+        assert int(v[b]) == want[b], (b, want[b])
+    assert [want[b] for b in dmg] == [ref.ROOT, ref.SEGMENT, ref.TRUNCATED]
+    ok = np.ones(n, bool)
+    ok[list(dmg)] = False
+    assert (v[ok] == ref.ACCEPT).all()
+    # every accepted block restored exactly; rejected blocks' pages are zero
+    good = np.nonzero(ok)[0]
+    check_pages_equal(c, dst, c.t_dst, blocks=good)
+    for b in dmg:
+        p = int(c.t_dst[0][b])
+        for l in range(c.geom.n_layers):
+            assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
+    # sampled accepted blocks: restored pages are the oracle record's slabs
+    for b in samp:
+        if b in dmg:
+            continue
+        p = int(c.t_dst[0][b])
+        rec = host_rec[b]
+        po, S = c.lay.payload_offset, c.lay.slab_bytes
+        for l in (0, c.geom.n_layers // 2, c.geom.n_layers - 1):
+            assert dst.k[l][p].cpu().numpy().tobytes() == bytes(rec[po + 2 * l * S: po + (2 * l + 1) * S])
+            assert dst.v[l][p].cpu().numpy().tobytes() == bytes(rec[po + (2 * l + 1) * S: po + (2 * l + 2) * S])
+
+
+def test_hybrid_full_scale():
+    cfg = wl.CONFIGS[4]
+    g = cfg.geom
+    n = cfg.n_tokens // g.page_tokens
+    c = Case(g, n, cfg.src_pages, cfg.dst_pages, cfg.seed)
+    log("hybrid: %d blocks of %d tokens, record %.1f MB" % (n, g.page_tokens, c.lay.record_bytes / 1e6))
+    assert c.lay.chunks_per_slab == 16
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    samp = [0, 100, 252, 255]
+    for b in samp:
+        assert store.buf[b].cpu().numpy().tobytes() == oracle_record(c, b), b
+    tables = wl.hybrid_tables(cfg, c.t_dst[0])
+    assert (tables[1] >= 0).sum() == 4 and (tables[0] >= 0).sum() == n
+    rb, po, S = c.lay.record_bytes, c.lay.payload_offset, c.lay.slab_bytes
+    # block 10: flip inside layer 0 K (a sliding-window layer; not read for block 10)
+    store.buf[10, po + 12345] ^= 1
+    # block 253: flip inside layer 0 K (read: block 253 is window-resident)
+    store.buf[253, po + 12345] ^= 1
+    # block 20: flip inside layer 5 V (a global layer; always read)
+    store.buf[20, po + 11 * S + 999] ^= 8
+    dst = PagedCache(g.n_layers, cfg.dst_pages, c.stride, DEV)
+    for t in dst.k + dst.v:
+        t.fill_(0x3C)
+    v = c.load(store.ptrs, store.lens, tables, dst)
+    exp = np.full(n, ref.ACCEPT)
+    exp[253] = ref.SEGMENT
+    exp[20] = ref.SEGMENT
+    assert np.array_equal(v, exp), np.nonzero(v != exp)
+    for b in (10, 20, 253, 254):
+        rec = store.buf[b].cpu().numpy().tobytes()
+        read = [s for s, _, _ in ref.read_slabs(c.lay, tables, b)]
+        assert int(v[b]) == ref.verify(c.lay, c.ns, rec, c.keys[b].tobytes(), b, c.tokens[b], read), b
+    good = [b for b in range(n) if b not in (20, 253)]
+    check_pages_equal(c, dst, tables, blocks=good)
+    # pages a load never touches keep their bytes: local layers, non-window blocks
+    for l in range(g.n_layers):
+        if g.group(l) == 1:
+            p = int(c.t_dst[0][5])
+            assert (dst.k[l][p] == 0x3C).all().item() and (dst.v[l][p] == 0x3C).all().item()
+    # rejected blocks: every page they would have written is zero
+    for b in (20, 253):
+        for l in range(g.n_layers):
+            p = int(tables[g.group(l)][b])
+            if p >= 0:
+                assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()

@@ -1,0 +1,80 @@
+"""Multi-request reuse on the GPU: chained keys, index lookup and verified
+restore of every request's shared prefix, with 5 % of the stored records
+damaged. A reduced instance is checked against the oracle in full (every
+verdict and every pool byte); the full-size workload (256 requests, 16,384
+stored records of 2 MiB, a 64 GiB page pool) is checked by the oracle on every
+damaged record and a sample of undamaged ones, and by properties on all."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from tests.gpu_case import log
+from tests.multi_request import MultiRun
+
+pytestmark = pytest.mark.gpu
+
+
+def test_multi_request_reduced_full_oracle():
+    geom = wl.Geometry(2, 2, 64, 16)
+    w = wl.multi_request(n_requests=16, n_base=3, base_tokens=512, median=200, lo=40, hi=512,
+                         corrupt_frac=0.10, geom=geom, seed=21)
+    run = MultiRun(w, pool_pages=128, seed=21)
+    damaged = {r for r, _ in w.corrupt_flip} | {r for r, _ in w.corrupt_trunc}
+    assert len(damaged) == int(0.10 * run.n_stored)
+    lay = run.lay
+    slab = lay.slab_bytes
+
+    def check(b):
+        # the oracle restores the same batch into host copies of the pool
+        hk = [t.cpu().numpy().copy() for t in run.dst.k]
+        hv = [t.cpu().numpy().copy() for t in run.dst.v]
+        n = len(b.blocks)
+        recs, keys, bidx, toks = [], [], [], []
+        for r, i, rid, page in b.blocks:
+            recs.append(run.store.buf[rid].cpu().numpy().tobytes()[:int(run.lens[rid])])
+            q = w.requests[r]
+            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * 16].tobytes(), 64)[i])
+            bidx.append(i)
+            toks.append(q.tokens[i * 16:(i + 1) * 16])
+        # every pool page of this batch is written by the batch (accepted:
+        # the record's slabs, rejected: zeros), so the prior contents do not matter
+        vo = ref.restore(lay, run.ns, recs, keys, bidx, toks, np.arange(n)[None, :], hk, hv)
+        assert [int(x) for x in b.verdicts] == vo
+        for l in range(geom.n_layers):
+            assert np.array_equal(run.dst.k[l][:n].cpu().numpy()[:, :slab], hk[l][:n, :slab])
+            assert np.array_equal(run.dst.v[l][:n].cpu().numpy()[:, :slab], hv[l][:n, :slab])
+
+    batches = run.run(check)
+    assert len(batches) >= 2
+    n_rej = sum(int((b.verdicts != ref.ACCEPT).sum()) for b in batches)
+    n_dmg_loaded = sum(1 for b in batches for blk in b.blocks if blk[2] in damaged)
+    assert n_rej == n_dmg_loaded > 0
+
+
+def test_multi_request_full_size():
+    w = wl.multi_request(seed=3)
+    run = MultiRun(w, pool_pages=32768, seed=3)  # 32,768 x 2 MiB = 64 GiB
+    damaged = {r for r, _ in w.corrupt_flip} | {r for r, _ in w.corrupt_trunc}
+    assert len(damaged) == 819
+    want = {rid: run.oracle_verdict(rid) for rid in sorted(damaged)}
+    assert all(v != ref.ACCEPT for v in want.values())
+    r = np.random.default_rng(0)
+    clean = [int(x) for x in r.choice([i for i in range(run.n_stored) if i not in damaged], 12, replace=False)]
+    for rid in clean:
+        assert run.oracle_verdict(rid) == ref.ACCEPT
+    log("oracle verdicts ready: %d damaged records" % len(want))
+    seen = {"blocks": 0, "rejected": 0}
+
+    def check(b):
+        for (req, pos, rid, page), v in zip(b.blocks, b.verdicts):
+            assert int(v) == want.get(rid, ref.ACCEPT), (req, pos, rid)
+        run.check_pages(b, damaged)
+        seen["blocks"] += len(b.blocks)
+        seen["rejected"] += int((b.verdicts != ref.ACCEPT).sum())
+
+    batches = run.run(check)
+    total_shared = sum(q.shared_blocks for q in w.requests)
+    assert seen["blocks"] == total_shared
+    log("restored %d blocks in %d batches, %d rejected" % (seen["blocks"], len(batches), seen["rejected"]))
+    assert seen["rejected"] > 0
