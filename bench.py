@@ -195,22 +195,46 @@ def main():
                 "kernel": "k_load_seg", "algorithmic_bytes_per_launch": seg_bytes,
                 "avg_launch_ms": kern["load_seg"]}
 
-    # ---- practical ceiling: a device-to-device copy of the same byte count
+    # ---- host steps a1 (keys) and a2 (lookup) on their own
+    t_keys, t_look = [], []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        keys = T.tl_block_keys(ctx, tokens)
+        t1 = time.perf_counter()
+        idx.get_batch(keys)
+        t2 = time.perf_counter()
+        t_keys.append((t1 - t0) * 1e3)
+        t_look.append((t2 - t1) * 1e3)
+    host = {"keys_ms": sorted(t_keys)[2], "lookup_ms": sorted(t_look)[2],
+            "sha256_extensions": T.sha256_selftest(b"", 1) is not None}
+
+    # ---- practical ceilings with torch's own kernels over the same byte count:
+    # a device-to-device copy, a read-only reduction and a write-only fill
     copy = None
     if not args.no_copy_ceiling:
         half = payload * n // 2
         a = torch.empty(half, dtype=torch.uint8, device=dev)
         b = store.buf.view(-1)[:half]
-        a.copy_(b)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(5):
-            a.copy_(b)
-        torch.cuda.synchronize()
-        cms = (time.perf_counter() - t0) * 1e3 / 5
-        copy = {"bytes_read_plus_written": 2 * half, "ms": cms, "GBps": 2 * half / (cms * 1e-3) / 1e9}
-        del a
-        log("copy ceiling: %.0f GB/s" % copy["GBps"])
+
+        def timed_ms(f, reps=5):
+            f()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                f()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t0) * 1e3 / reps
+
+        cms = timed_ms(lambda: a.copy_(b))
+        b64 = b.view(torch.int64)
+        rms = timed_ms(lambda: b64.sum())
+        wms = timed_ms(lambda: a.fill_(0))
+        copy = {"bytes_read_plus_written": 2 * half, "ms": cms, "GBps": 2 * half / (cms * 1e-3) / 1e9,
+                "read_only_GBps": half / (rms * 1e-3) / 1e9, "write_only_GBps": half / (wms * 1e-3) / 1e9,
+                "how": "torch copy_, int64 sum and fill_ over %d bytes" % half}
+        del a, b64
+        log("torch ceilings: copy %.0f, read %.0f, write %.0f GB/s"
+            % (copy["GBps"], copy["read_only_GBps"], copy["write_only_GBps"]))
 
     # ---- CPU baseline: the oracle on a bounded sample of the same workload
     cpu = None
@@ -254,6 +278,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "save": save,
+        "host_ms": host,
         "copy_ceiling": copy,
         "kernel_source_sha256_16": kernel_source_hash(),
     }

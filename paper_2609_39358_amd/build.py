@@ -31,24 +31,26 @@ def _run(cmd, verbose):
     return r.stdout
 
 
-def build(verbose: bool = False, extra_hip_flags=()) -> str:
+def build(verbose: bool = False, extra_hip_flags=(), out: str = OUT, build_dir: str = BUILD_DIR) -> str:
+    """Compile and link libtaliesin.so; extra_hip_flags (e.g. -DTL_BATCH_ROWS=16)
+    and out/build_dir allow building a variant next to the default library."""
     hipcc = os.environ.get("HIPCC") or shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
     cxx = os.environ.get("CXX") or shutil.which("g++") or "g++"
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    os.makedirs(build_dir, exist_ok=True)
     inc = ["-I", INCLUDE, "-I", CSRC]
     objs = []
     for src in ("ctx.cpp", "sha256.cpp"):
-        o = os.path.join(BUILD_DIR, src + ".o")
+        o = os.path.join(build_dir, src + ".o")
         _run([cxx, *CXX_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)
-    o = os.path.join(BUILD_DIR, "kernels.hip.o")
+    o = os.path.join(build_dir, "kernels.hip.o")
     _run([hipcc, *HIP_FLAGS, *extra_hip_flags, *inc, "-c", os.path.join(CSRC, "kernels.hip"), "-o", o],
          verbose)
     objs.append(o)
-    tmp = OUT + ".tmp"
+    tmp = out + ".tmp"
     _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs], verbose)
-    os.replace(tmp, OUT)
-    return OUT
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -36,14 +36,52 @@ constexpr uint64_t kP3 = 0x165667B19E3779F9ull;
 constexpr uint64_t kP4 = 0x85EBCA77C2B2AE63ull;
 constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 
-constexpr uint32_t kSegWaves = 4;       // wavefronts per workgroup in the chunk kernels
+// Tuning knobs (compile-time; the defaults are the measured best on MI355X).
+#ifndef TL_SEG_WAVES
+#define TL_SEG_WAVES 4      // wavefronts per workgroup in the chunk kernels
+#endif
+#ifndef TL_BATCH_ROWS
+#define TL_BATCH_ROWS 8     // rows each lane has in flight per batch
+#endif
+#ifndef TL_PREFETCH
+#define TL_PREFETCH 1       // load the next batch before hashing this one
+#endif
+#ifndef TL_NT_LOAD
+#define TL_NT_LOAD 1        // non-temporal (streaming) loads of the source
+#endif
+#ifndef TL_NT_STORE
+#define TL_NT_STORE 1       // non-temporal (streaming) stores of the copy
+#endif
+#ifndef TL_GRID_WGS_PER_CU
+#define TL_GRID_WGS_PER_CU 0  // >0: cap the chunk grid at this many workgroups per CU
+#endif
+
+constexpr uint32_t kSegWaves = TL_SEG_WAVES;
 constexpr uint32_t kMetaTile = 4096;    // metadata bytes staged in LDS at a time
 constexpr uint32_t kSegFailBit = 0x100; // status bit: some chunk digest mismatched
 
 // 16 bytes per lane: a native vector so that the compiler emits dwordx4
-// accesses and accepts the non-temporal builtins.
+// accesses and accepts the non-temporal builtins; gv4u lives in the global
+// address space so that the accesses are global_* rather than flat_*.
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) v4u gv4u;
 __device__ __forceinline__ v4u zero4() { return v4u{0u, 0u, 0u, 0u}; }
+
+__device__ __forceinline__ v4u ld16(const gv4u* p) {
+#if TL_NT_LOAD
+  return __builtin_nontemporal_load(p);
+#else
+  return *p;
+#endif
+}
+
+__device__ __forceinline__ void st16(gv4u* p, v4u v) {
+#if TL_NT_STORE
+  __builtin_nontemporal_store(v, p);
+#else
+  *p = v;
+#endif
+}
 
 // ---- XXH64 pieces --------------------------------------------------------
 __device__ __forceinline__ uint64_t rotl64(uint64_t x, int r) { return (x << r) | (x >> (64 - r)); }
@@ -196,39 +234,71 @@ __device__ __forceinline__ char* record_chunk(const SegArgs& a, uint64_t rec, co
 }
 
 __device__ __forceinline__ void zero_rows(char* dst, uint32_t rows, uint32_t lane) {
-  v4u* d = (v4u*)dst + lane;
-  const v4u z = zero4();
-  for (uint32_t r = 0; r < rows; ++r) d[(uint64_t)r * 64] = z;
+  gv4u* d = (gv4u*)dst + lane;
+  for (uint32_t r = 0; r < rows; ++r) st16(d + (uint64_t)r * 64, zero4());
+}
+
+template <int B>
+__device__ __forceinline__ void load_batch(v4u (&x)[B], const gv4u* s, uint32_t r) {
+#pragma unroll
+  for (int i = 0; i < B; ++i) x[i] = ld16(s + (uint64_t)(r + i) * 64);
+}
+
+// Stores a batch of rows and feeds it, two rows (one 32-byte stripe) at a
+// time, to the lane's column state.
+template <int B>
+__device__ __forceinline__ void store_hash_batch(const v4u (&x)[B], gv4u* d, uint32_t r, Column& c) {
+#pragma unroll
+  for (int i = 0; i < B; ++i) st16(d + (uint64_t)(r + i) * 64, x[i]);
+#pragma unroll
+  for (int i = 0; i < B; i += 2) c.stripe(x[i], x[i + 1]);
 }
 
 // Copy `rows` rows of 1 KiB from src to dst and return this lane's column
-// digest (seed = lane). Eight rows are in flight per lane per batch.
+// digest (seed = lane). Lane j moves granule j of every row. Rows go in
+// batches of B; with prefetching, the next batch's loads are in flight while
+// the current batch is stored and hashed.
 __device__ __forceinline__ uint64_t copy_hash(const char* src, char* dst, uint32_t rows,
                                               uint32_t lane) {
-  const v4u* s = (const v4u*)src + lane;
-  v4u* d = (v4u*)dst + lane;
+  constexpr int B = TL_BATCH_ROWS;
+  static_assert(B % 2 == 0, "batches hold whole stripes");
+  const gv4u* s = (const gv4u*)src + lane;
+  gv4u* d = (gv4u*)dst + lane;
   Column c;
   c.init(lane);
+  const uint32_t full = rows / B * B;
   uint32_t r = 0;
-  for (; r + 8 <= rows; r += 8) {
-    v4u x[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = __builtin_nontemporal_load(s + (uint64_t)(r + i) * 64);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) __builtin_nontemporal_store(x[i], d + (uint64_t)(r + i) * 64);
-#pragma unroll
-    for (int i = 0; i < 8; i += 2) c.stripe(x[i], x[i + 1]);
+#if TL_PREFETCH
+  if (full) {
+    v4u x[B], y[B];
+    load_batch<B>(x, s, 0);
+    for (r = 0; r < full; r += 2 * B) {
+      const bool has_y = r + B < full;
+      if (has_y) load_batch<B>(y, s, r + B);
+      store_hash_batch<B>(x, d, r, c);
+      if (!has_y) { r += B; break; }
+      if (r + 2 * B < full) load_batch<B>(x, s, r + 2 * B);
+      store_hash_batch<B>(y, d, r + B, c);
+    }
+    r = full;
   }
+#else
+  for (; r < full; r += B) {
+    v4u x[B];
+    load_batch<B>(x, s, r);
+    store_hash_batch<B>(x, d, r, c);
+  }
+#endif
   for (; r + 2 <= rows; r += 2) {
-    const v4u x0 = s[(uint64_t)r * 64], x1 = s[(uint64_t)(r + 1) * 64];
-    d[(uint64_t)r * 64] = x0;
-    d[(uint64_t)(r + 1) * 64] = x1;
+    const v4u x0 = ld16(s + (uint64_t)r * 64), x1 = ld16(s + (uint64_t)(r + 1) * 64);
+    st16(d + (uint64_t)r * 64, x0);
+    st16(d + (uint64_t)(r + 1) * 64, x1);
     c.stripe(x0, x1);
   }
   v4u last = zero4();
   if (r < rows) {
-    last = s[(uint64_t)r * 64];
-    d[(uint64_t)r * 64] = last;
+    last = ld16(s + (uint64_t)r * 64);
+    st16(d + (uint64_t)r * 64, last);
   }
   return c.finish(lane, rows, last);
 }
@@ -538,8 +608,15 @@ void timed(int kernel, hipStream_t s, F&& launch) {
 // Workgroups for a chunk kernel: one wavefront per work item, capped so the
 // grid (in work-items, a 32-bit quantity) stays small; the kernels stride.
 uint32_t seg_grid(uint32_t total) {
+  uint32_t cap = 1u << 20;
+#if TL_GRID_WGS_PER_CU > 0
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+    cap = (uint32_t)cus * TL_GRID_WGS_PER_CU;
+#endif
   const uint32_t want = (total + kSegWaves - 1) / kSegWaves;
-  return want < (1u << 20) ? want : (1u << 20);
+  return want < cap ? want : cap;
 }
 
 }  // namespace

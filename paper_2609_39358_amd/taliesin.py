@@ -16,7 +16,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libtaliesin.so")
+# TALIESIN_LIB may point at another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("TALIESIN_LIB") or os.path.join(_HERE, "libtaliesin.so")
 
 TL_OK, TL_EINVAL, TL_ELAYOUT, TL_ENOIDENT, TL_EDEVICE, TL_ENOMEM, TL_EFULL, TL_ERANGE = 0, -1, -2, -3, -4, -5, -6, -7
 ACCEPT, MISSING, BADARG, TRUNCATED, OVERLONG = 0x01, 0x10, 0x11, 0x12, 0x13
