@@ -191,10 +191,33 @@ int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* b
 int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
             const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status);
 
+/* Save in parts, as prefill finishes each layer (Sec. 2.2: state is saved
+ * after the runtime computes it; saving layer by layer lets the copy overlap
+ * the prefill of later layers). tl_save_layers writes the slabs of layers
+ * [layer_begin, layer_end) and their chunk digests for every block (same
+ * arguments and rules as tl_save; a block with an invalid page id gets zero
+ * chunks). tl_save_seal then writes every block's header, token ids, padding
+ * and root, and d_status as tl_save does; n_pages is the source cache's page
+ * count, used to report TL_BADARG. A record is valid only after its seal, and
+ * only if every layer range was saved before the seal (stream order). tl_save
+ * is exactly tl_save_layers(0, n_layers) followed by tl_save_seal. TL_EINVAL
+ * if layer_begin >= layer_end or layer_end > n_layers. */
+int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
+                   const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
+                   uint32_t layer_end);
+int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pages,
+                 const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status);
+
 /* ---- a3-a5: verified restore ---------------------------------------------
  * For every block b: d_record_ptrs[b] (0 = no record) with reported length
  * d_record_lens[b]; the library never reads past that length and takes every
- * offset from the context, never from the record. Checks, in order: pointer,
+ * offset from the context, never from the record. Records may live in device
+ * memory or in pinned host memory that the device can address (hipHostMalloc,
+ * e.g. torch's pin_memory): the kernels then read them over the host link
+ * with no staging copy, so a host-resident store restores into HBM at link
+ * speed while using no device memory beyond the destination pages (the
+ * paper's blocks streamed in and discarded after use, Sec. 4.3 "Long windows
+ * at flat GPU memory"). Checks, in order: pointer,
  * length, root (metadata checksum), header fields and namespace, position
  * (d_block_index[b]), key (d_keys[b]), token ids (if d_tokens), and the tree
  * XXH64 of every payload chunk it reads. It copies each read slab to page

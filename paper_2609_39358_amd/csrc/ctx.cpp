@@ -303,6 +303,31 @@ int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* sr
   return tl::launch_save(ctx, stream, n_blocks, src, blocks, d_record_ptrs, d_status);
 }
 
+int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
+                   const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
+                   uint32_t layer_end) {
+  if (!ctx) return TL_EINVAL;
+  if (layer_begin >= layer_end || layer_end > ctx->L) return TL_EINVAL;
+  if (n_blocks == 0) return TL_OK;
+  int r = check_cache(ctx, src);
+  if (r) return r;
+  if ((r = check_blocks(ctx, n_blocks, blocks, false))) return r;
+  if (!d_record_ptrs || ((uintptr_t)d_record_ptrs & 7)) return TL_EINVAL;
+  return tl::launch_save_layers(ctx, stream, n_blocks, src, blocks, d_record_ptrs, layer_begin,
+                                layer_end);
+}
+
+int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pages,
+                 const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status) {
+  if (!ctx) return TL_EINVAL;
+  if (n_blocks == 0) return TL_OK;
+  if (n_pages < 0 || n_pages > 0x7fffffff) return TL_EINVAL;
+  int r = check_blocks(ctx, n_blocks, blocks, true);
+  if (r) return r;
+  if (!d_record_ptrs || ((uintptr_t)d_record_ptrs & 7)) return TL_EINVAL;
+  return tl::launch_save_seal(ctx, stream, n_blocks, n_pages, blocks, d_record_ptrs, d_status);
+}
+
 int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_record_ptrs,
             const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
             uint8_t* d_verdicts, void* d_workspace, size_t workspace_bytes) {

@@ -55,6 +55,11 @@ bool sha256_has_shani();
 // Kernel launchers; kernels.hip.
 int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                 const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status);
+int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
+                       const tl_blocks* blk, const uint64_t* d_rec, uint32_t layer_begin,
+                       uint32_t layer_end);
+int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
+                     const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status);
 int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,
                 const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
                 uint8_t* d_verdicts, uint32_t* d_ws);

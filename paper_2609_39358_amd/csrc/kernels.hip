@@ -184,7 +184,9 @@ struct SegArgs {
   int64_t stride;
   int64_t n_pages;
   uint32_t n;            // blocks
-  uint32_t total;        // n * n_seg work items
+  uint32_t t_begin;      // first chunk index of the range handled (save by layers)
+  uint32_t n_sub;        // chunks per block in that range
+  uint32_t total;        // n * n_sub work items
   uint32_t* status;      // load: per-block status words
 };
 
@@ -211,8 +213,8 @@ struct Item {
 
 __device__ __forceinline__ Item decode(const SegArgs& a, uint32_t w) {
   Item it;
-  it.b = w / a.g.n_seg;
-  it.t = w - it.b * a.g.n_seg;
+  it.b = w / a.n_sub;
+  it.t = a.t_begin + (w - it.b * a.n_sub);
   it.s = it.t / a.g.cps;
   it.k = it.t - it.s * a.g.cps;
   const uint32_t layer = it.s >> 1;
@@ -546,7 +548,8 @@ __global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
 }
 
 void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, const int32_t* tables,
-              const tl_cache* c, uint32_t* status) {
+              const tl_cache* c, uint32_t* status, uint32_t layer_begin = 0, uint32_t layer_end = 0) {
+  if (layer_end == 0) layer_end = ctx->geo.n_layers;
   a.g = ctx->geo;
   a.rec = rec;
   a.tables = tables;
@@ -555,7 +558,9 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.stride = c->page_stride;
   a.n_pages = c->n_pages;
   a.n = (uint32_t)n;
-  a.total = (uint32_t)(n * ctx->geo.n_seg);
+  a.t_begin = 2 * layer_begin * ctx->geo.cps;
+  a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.cps;
+  a.total = (uint32_t)(n * a.n_sub);
   a.status = status;
 }
 
@@ -623,21 +628,36 @@ uint32_t seg_grid(uint32_t total) {
 
 namespace tl {
 
-int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
-                const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
+int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
+                       const tl_blocks* blk, const uint64_t* d_rec, uint32_t layer_begin,
+                       uint32_t layer_end) {
   hipStream_t s = (hipStream_t)stream;
   SegArgs a;
-  fill_seg(a, ctx, n, d_rec, blk->d_tables, src, nullptr);
-  MetaArgs m;
-  fill_meta(m, ctx, n, d_rec, nullptr, blk, src->n_pages, nullptr, d_status);
+  fill_seg(a, ctx, n, d_rec, blk->d_tables, src, nullptr, layer_begin, layer_end);
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
     hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
   });
+  return launched();
+}
+
+int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
+                     const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
+  hipStream_t s = (hipStream_t)stream;
+  MetaArgs m;
+  fill_meta(m, ctx, n, d_rec, nullptr, blk, n_pages, nullptr, d_status);
+  (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_META, s, [&] {
     hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
   });
   return launched();
+}
+
+int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
+                const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
+  int r = launch_save_layers(ctx, stream, n, src, blk, d_rec, 0, ctx->geo.n_layers);
+  if (r) return r;
+  return launch_save_seal(ctx, stream, n, src->n_pages, blk, d_rec, d_status);
 }
 
 int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,

@@ -78,6 +78,9 @@ def _load():
                                     c.POINTER(c.c_size_t)]),
         "tl_block_keys_batch": (c.c_int, [P, P, P, P, P, c.c_size_t, c.c_size_t, P, P, P, c.c_int]),
         "tl_save": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P, P]),
+        "tl_save_layers": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P,
+                                     c.c_uint32, c.c_uint32]),
+        "tl_save_seal": (c.c_int, [P, P, c.c_size_t, c.c_int64, c.POINTER(tl_blocks), P, P]),
         "tl_load": (c.c_int, [P, P, c.c_size_t, P, P, c.POINTER(tl_blocks), c.POINTER(tl_cache),
                               P, P, c.c_size_t]),
         "tl_index_create": (P, [c.c_size_t]),
@@ -102,7 +105,7 @@ def _load():
 _lib = _load()
 EXPORTED = (
     "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
-    "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_load", "tl_index_create",
+    "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_save_layers", "tl_save_seal", "tl_load", "tl_index_create",
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
     "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
     "tl_timing_read")
@@ -255,6 +258,19 @@ def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d
             d_status=None):
     _check(_lib.tl_save(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src), ctypes.byref(blocks),
                         _addr(d_record_ptrs), _addr(d_status)), "tl_save")
+
+
+def tl_save_layers(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
+                   layer_begin: int, layer_end: int):
+    _check(_lib.tl_save_layers(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src),
+                               ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end),
+           "tl_save_layers")
+
+
+def tl_save_seal(ctx: Ctx, stream, n_blocks: int, n_pages: int, blocks: tl_blocks, d_record_ptrs,
+                 d_status=None):
+    _check(_lib.tl_save_seal(ctx.handle, _stream(stream), n_blocks, n_pages, ctypes.byref(blocks),
+                             _addr(d_record_ptrs), _addr(d_status)), "tl_save_seal")
 
 
 def tl_load(ctx: Ctx, stream, n_blocks: int, d_record_ptrs, d_record_lens, blocks: tl_blocks,

@@ -1,0 +1,127 @@
+"""GPU tests of the two paths around the HBM restore: saving layer by layer
+while prefill proceeds (tl_save_layers + tl_save_seal), and restoring from
+records that live in pinned host memory (read by the kernels over the host
+link). Both are checked byte for byte against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import taliesin as T
+from paper_2609_39358_amd.device import PagedCache, RecordStore
+from tests.gpu_case import DEV, Case, host_layers, i32, i64, log, random_fill
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("geom", [wl.CONFIGS[0].geom,
+                                  wl.hybrid_geometry(n_layers=6, n_kv_heads=2, head_dim=64,
+                                                     page_tokens=16, window=32),
+                                  wl.Geometry(3, 16, 128, 32)])
+def test_save_by_layer_ranges_equals_whole_save(geom):
+    n = 20
+    c = Case(geom, n, 32, 32, seed=12)
+    c.make_src()
+    whole, st = c.save()
+    parts = RecordStore(n, c.lay.record_bytes, DEV)
+    parts.buf.fill_(0xEE)
+    L = geom.n_layers
+    cuts = sorted({0, L, *np.random.default_rng(1).integers(1, L, size=min(3, L - 1)).tolist()})
+    ranges = list(zip(cuts[:-1], cuts[1:]))[::-1]  # any order before the seal
+    blk = c.blocks(i32(c.t_src))
+    s = torch.cuda.current_stream()
+    for a, b in ranges:
+        T.tl_save_layers(c.ctx, s, n, c.src.tl(), blk, parts.ptrs, a, b)
+    st2 = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    T.tl_save_seal(c.ctx, s, n, c.src_pages, blk, parts.ptrs, st2)
+    torch.cuda.synchronize()
+    assert torch.equal(parts.buf, whole.buf)
+    assert (st2.cpu().numpy() == st).all()
+    recs_o, _ = c.oracle_save()
+    got = parts.buf.cpu().numpy()
+    for b in range(n):
+        assert got[b].tobytes() == recs_o[b], b
+
+
+def test_save_layers_overlapped_with_prefill():
+    """Layer l is "prefilled" (its pages rewritten) on one stream while the
+    save of layer l-1 runs on another; the sealed records equal the oracle's
+    records of the final cache."""
+    geom = wl.Geometry(8, 4, 64, 16)
+    n = 48
+    c = Case(geom, n, 64, 64, seed=13)
+    c.make_src()
+    store = RecordStore(n, c.lay.record_bytes, DEV)
+    blk = c.blocks(i32(c.t_src))
+    prefill = torch.cuda.Stream()
+    saver = torch.cuda.Stream()
+    prefill.wait_stream(torch.cuda.current_stream())  # the initial fill and the
+    saver.wait_stream(torch.cuda.current_stream())  # argument uploads are done first
+    done = [torch.cuda.Event() for _ in range(geom.n_layers)]
+    g = torch.Generator(device=DEV)
+    g.manual_seed(5)
+    for l in range(geom.n_layers):
+        with torch.cuda.stream(prefill):
+            for t in (c.src.k[l], c.src.v[l]):
+                t.copy_(torch.randint(0, 256, t.shape, generator=g, device=DEV, dtype=torch.uint8))
+            done[l].record(prefill)
+        saver.wait_event(done[l])
+        T.tl_save_layers(c.ctx, saver, n, c.src.tl(), blk, store.ptrs, l, l + 1)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    T.tl_save_seal(c.ctx, saver, n, c.src_pages, blk, store.ptrs, st)
+    torch.cuda.synchronize()
+    assert (st == ref.ACCEPT).all().item()
+    recs_o, _ = c.oracle_save()
+    got = store.buf.cpu().numpy()
+    for b in range(n):
+        assert got[b].tobytes() == recs_o[b], b
+
+
+def test_save_layers_argument_errors():
+    geom = wl.Geometry(4, 2, 64, 16)
+    c = Case(geom, 4, 8, 8, seed=14)
+    c.make_src()
+    store = RecordStore(4, c.lay.record_bytes, DEV)
+    blk = c.blocks(i32(c.t_src))
+    for a, b in ((2, 2), (3, 1), (0, 5)):
+        with pytest.raises(T.TaliesinError) as e:
+            T.tl_save_layers(c.ctx, None, 4, c.src.tl(), blk, store.ptrs, a, b)
+        assert e.value.status == T.TL_EINVAL
+
+
+@pytest.mark.parametrize("name", ["tiny", "two_chunks"])
+def test_restore_from_pinned_host_records(name):
+    geom = wl.CONFIGS[0].geom if name == "tiny" else wl.Geometry(2, 16, 128, 32)
+    n = 40
+    c = Case(geom, n, 64, 64, seed=15)
+    c.make_src()
+    store, st = c.save()
+    recs_o, _ = c.oracle_save()
+    rb = c.lay.record_bytes
+    host = torch.empty((n, rb), dtype=torch.uint8, pin_memory=True)
+    host.copy_(store.buf)
+    torch.cuda.synchronize()
+    recs = [bytearray(r) for r in recs_o]
+    po = c.lay.payload_offset
+    for b, off in ((3, 200), (7, po + 77), (11, rb - 1)):
+        host[b, off] ^= 0x04
+        recs[b][off] ^= 0x04
+    lens = np.full(n, rb, np.uint64)
+    lens[5] = rb // 2
+    ptrs = torch.tensor([host.data_ptr() + i * rb for i in range(n)], dtype=torch.int64, device=DEV)
+    ptrs[9] = 0
+    host_recs = [bytes(r[:int(lens[b])]) for b, r in enumerate(recs)]
+    host_recs[9] = None
+    dst = random_fill(PagedCache(geom.n_layers, 64, c.stride, DEV), 16)
+    hk0, hv0 = host_layers(dst)
+    log("restore from pinned host records:", n, "blocks")
+    v = c.load(ptrs, i64(lens), c.t_dst, dst)
+    vo = ref.restore(c.lay, c.ns, host_recs, [k.tobytes() for k in c.keys], c.bidx, c.tokens, c.t_dst,
+                     hk0, hv0, n_pages=64)
+    assert [int(x) for x in v] == vo
+    assert [vo[b] for b in (3, 5, 7, 9, 11)] == [ref.ROOT, ref.TRUNCATED, ref.SEGMENT, ref.MISSING,
+                                                 ref.SEGMENT]
+    hk, hv = host_layers(dst)
+    for l in range(geom.n_layers):
+        assert np.array_equal(hk[l], hk0[l]) and np.array_equal(hv[l], hv0[l])

@@ -184,6 +184,13 @@ def test_save_load_argument_validation_enqueues_nothing():
     assert save(blk=T.make_blocks(0x30000, 0x40000, None, 0x60000)) == T.TL_EINVAL
     assert save(rec=None) == T.TL_EINVAL
     assert L.tl_load(None, None, 1, 1, 1, None, None, 1, 1, 1) == T.TL_EINVAL
+    # layer-wise save: a non-empty range inside [0, n_layers); the seal needs tokens
+    sl = lambda a, b, n=64: L.tl_save_layers(c.handle, None, n, P(good_cache), P(good_blk), 0x70000, a, b)
+    assert sl(0, 0) == T.TL_EINVAL and sl(3, 2) == T.TL_EINVAL and sl(0, 5) == T.TL_EINVAL
+    assert sl(0, 4, n=0) == T.TL_OK
+    seal = lambda blk, n_pages=128: L.tl_save_seal(c.handle, None, 64, n_pages, P(blk), 0x70000, None)
+    assert seal(T.make_blocks(0x30000, 0x40000, None, 0x60000)) == T.TL_EINVAL
+    assert seal(good_blk, n_pages=-1) == T.TL_EINVAL
     # grid index must fit in 32 bits
     assert load(n=(1 << 32) // c.n_segments + 1, wsb=1 << 40) == T.TL_ERANGE
 
