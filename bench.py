@@ -60,6 +60,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=1536)
     ap.add_argument("--no-copy-ceiling", action="store_true")
+    ap.add_argument("--no-host-tier", action="store_true")
+    ap.add_argument("--host-tier-blocks", type=int, default=1024)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one MI355X: this build has no multi-GPU path "
@@ -236,6 +238,41 @@ def main():
         log("torch ceilings: copy %.0f, read %.0f, write %.0f GB/s"
             % (copy["GBps"], copy["read_only_GBps"], copy["write_only_GBps"]))
 
+    # ---- host tier: restore records that live in pinned host memory (read by
+    # the kernels over the host link, no staging), beside a plain H2D copy
+    host_tier = None
+    if not args.no_host_tier:
+        m = min(args.host_tier_blocks, n)
+        hrec = torch.empty((m, rb), dtype=torch.uint8, pin_memory=True)
+        hrec.copy_(store.buf[:m])
+        torch.cuda.synchronize()
+        hptrs = torch.tensor([hrec.data_ptr() + i * rb for i in range(m)], dtype=torch.int64, device=dev)
+        hlens = torch.full((m,), rb, dtype=torch.int64, device=dev)
+        hblk = T.make_blocks(d_keys0[:m], d_bidx[:m], d_tokens[:m], d_tdst[:, :m].contiguous())
+        hws = torch.empty(T.tl_workspace_bytes(ctx, m), dtype=torch.uint8, device=dev)
+        hverd = torch.zeros(m, dtype=torch.uint8, device=dev)
+        hload = lambda: T.tl_load(ctx, stream, m, hptrs, hlens, hblk, dst.tl(), hverd, hws, hws.numel())
+        hload()
+        torch.cuda.synchronize()
+        assert (hverd == T.ACCEPT).all().item()
+        t0 = time.perf_counter()
+        for _ in range(3):
+            hload()
+        torch.cuda.synchronize()
+        hms = (time.perf_counter() - t0) * 1e3 / 3
+        dbuf = store.buf[:m]
+        t0 = time.perf_counter()
+        for _ in range(3):
+            dbuf.copy_(hrec, non_blocking=True)
+        torch.cuda.synchronize()
+        cms = (time.perf_counter() - t0) * 1e3 / 3
+        host_tier = {"blocks": m, "record_GB": m * rb / 1e9, "ms": hms, "GBps": m * rb / (hms * 1e-3) / 1e9,
+                     "h2d_copy_GBps": m * rb / (cms * 1e-3) / 1e9,
+                     "tokens_avoided_per_s": m * P / (hms * 1e-3)}
+        host_tier["frac_of_h2d_copy"] = host_tier["GBps"] / host_tier["h2d_copy_GBps"]
+        del hrec
+        log("host tier: %.1f GB/s of records (plain H2D copy %.1f GB/s)" % (host_tier["GBps"], host_tier["h2d_copy_GBps"]))
+
     # ---- CPU baseline: the oracle on a bounded sample of the same workload
     cpu = None
     if not args.no_cpu_baseline:
@@ -279,6 +316,7 @@ def main():
         "cpu_baseline": cpu,
         "save": save,
         "host_ms": host,
+        "host_tier": host_tier,
         "copy_ceiling": copy,
         "kernel_source_sha256_16": kernel_source_hash(),
     }

@@ -17,7 +17,7 @@ Correctness, Sec. 5 Design boundaries):
     (Sec. 3 sabotage testing; Sec. 7 relation to the compute ceiling).
 The paper withholds the storage format (Sec. 1, last paragraph of the
 contributions), so the record layout, the key chain and the tree-mode
-checksum below are this project's readings; the design doc lists each one.
+checksum below are this project's readings of what the paper leaves open.
 
 Library primitives used as steps: hashlib.sha256 (FIPS 180-4) and
 xxhash.xxh64 (the published XXH64 algorithm). Both are pinned by known-answer

@@ -52,6 +52,9 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 #ifndef TL_NT_STORE
 #define TL_NT_STORE 1       // non-temporal (streaming) stores of the copy
 #endif
+#ifndef TL_SAVE_SLAB_MAJOR
+#define TL_SAVE_SLAB_MAJOR 0  // save work order: 0 = block-major, 1 = slab-major
+#endif
 #ifndef TL_GRID_WGS_PER_CU
 #define TL_GRID_WGS_PER_CU 0  // >0: cap the chunk grid at this many workgroups per CU
 #endif
@@ -187,6 +190,7 @@ struct SegArgs {
   uint32_t t_begin;      // first chunk index of the range handled (save by layers)
   uint32_t n_sub;        // chunks per block in that range
   uint32_t total;        // n * n_sub work items
+  uint32_t slab_major;   // 1: consecutive work items are consecutive blocks of one chunk
   uint32_t* status;      // load: per-block status words
 };
 
@@ -213,8 +217,14 @@ struct Item {
 
 __device__ __forceinline__ Item decode(const SegArgs& a, uint32_t w) {
   Item it;
-  it.b = w / a.n_sub;
-  it.t = a.t_begin + (w - it.b * a.n_sub);
+  if (a.slab_major) {
+    const uint32_t q = w / a.n;
+    it.b = w - q * a.n;
+    it.t = a.t_begin + q;
+  } else {
+    it.b = w / a.n_sub;
+    it.t = a.t_begin + (w - it.b * a.n_sub);
+  }
   it.s = it.t / a.g.cps;
   it.k = it.t - it.s * a.g.cps;
   const uint32_t layer = it.s >> 1;
@@ -561,6 +571,7 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.t_begin = 2 * layer_begin * ctx->geo.cps;
   a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.cps;
   a.total = (uint32_t)(n * a.n_sub);
+  a.slab_major = 0;
   a.status = status;
 }
 
@@ -634,6 +645,7 @@ int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache
   hipStream_t s = (hipStream_t)stream;
   SegArgs a;
   fill_seg(a, ctx, n, d_rec, blk->d_tables, src, nullptr, layer_begin, layer_end);
+  a.slab_major = TL_SAVE_SLAB_MAJOR;
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
     hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);

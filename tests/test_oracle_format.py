@@ -33,7 +33,7 @@ def rand_bytes(n, seed):
 
 # ---------------------------------------------------------------- geometry
 def test_geometry_of_the_five_workloads():
-    # slab, record and metadata sizes that the DESIGN tables quote
+    # slab, metadata and record sizes of the five workloads
     cases = {0: (8192, 512, 66048), 1: (32768, 1024, 2098176), 2: (65536, 1280, 7865600),
              4: (1048576, 13568, 100676864)}
     for i, (slab, meta, rec) in cases.items():

@@ -8,7 +8,9 @@ check see the same bytes.
 
 The workloads stand in for the paper's recall corpus (Sec. 4.1: 96,726 tokens,
 Gemma 4 31B) and its seven real-world datasets (Sec. 4.2), which are not
-available here. Shapes follow the five configurations described in the design doc.
+available here. The five workloads below keep their shapes: a tiny case, a
+mid-size document, the paper-scale corpus, a multi-request reuse mix and a
+hybrid sliding-window layout.
 """
 from __future__ import annotations
 
@@ -98,27 +100,36 @@ def page_table(n_blocks: int, n_pages: int, seed: int, stream: int = 0) -> np.nd
 
 
 def kv_layer_cpu(n_pages: int, geom: Geometry, seed: int, layer: int, kv: int) -> np.ndarray:
-    """One layer's K (kv=0) or V (kv=1) cache, N(0,1) in bf16, as raw bytes
-    [n_pages, page_bytes] (uint8). Drawn with torch's CPU generator."""
+    """One layer's K (kv=0) or V (kv=1) cache as raw bytes [n_pages,
+    page_bytes] (uint8): N(0,1) rounded to the geometry's element type (fp8:
+    uniform random bytes). Drawn with torch's CPU generator."""
     import torch
 
     g = torch.Generator(device="cpu")
     g.manual_seed(int(seed) * 1_000_003 + layer * 2 + kv + 17)
-    x = torch.randn(n_pages * geom.page_tokens * geom.n_kv_heads * geom.head_dim,
-                    generator=g, dtype=torch.float32).to(torch.bfloat16)
+    n = n_pages * geom.page_tokens * geom.n_kv_heads * geom.head_dim
+    if geom.dtype == "fp8":
+        x = torch.randint(0, 256, (n,), generator=g, dtype=torch.uint8)
+    else:
+        x = torch.randn(n, generator=g, dtype=torch.float32)
+        x = x.to({"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[geom.dtype])
     return x.view(torch.uint8).numpy().reshape(n_pages, geom.page_bytes)
 
 
 def kv_layer_torch(n_pages: int, geom: Geometry, seed: int, layer: int, kv: int, device):
-    """Same recipe drawn on `device` (bf16 tensor [n_pages, P, H, D]); the
-    device generator's bytes differ from the CPU one's, so parity checks copy
-    these bytes to the host instead of redrawing them."""
+    """Same recipe drawn on `device` (tensor [n_pages, P, H, D] of the
+    geometry's element type: N(0,1) rounded to bf16/f16/f32; fp8 pages are
+    uniform random bytes). The device generator's bytes differ from the CPU
+    one's, so parity checks copy these bytes to the host instead of redrawing."""
     import torch
 
     g = torch.Generator(device=device)
     g.manual_seed(int(seed) * 1_000_003 + layer * 2 + kv + 17)
-    return torch.randn((n_pages, geom.page_tokens, geom.n_kv_heads, geom.head_dim),
-                       generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
+    shape = (n_pages, geom.page_tokens, geom.n_kv_heads, geom.head_dim)
+    if geom.dtype == "fp8":
+        return torch.randint(0, 256, shape, generator=g, device=device, dtype=torch.uint8)
+    x = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    return x.to({"bf16": torch.bfloat16, "f16": torch.float16, "f32": torch.float32}[geom.dtype])
 
 
 def bit_flips(n_records: int, record_len: int, count: int, seed: int, stream: int = 0):
