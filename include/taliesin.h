@@ -91,7 +91,10 @@ typedef struct tl_layout {
   uint32_t n_kv_heads;
   uint32_t head_dim;
   uint32_t dtype;       /* TL_DTYPE_* */
-  uint32_t page_tokens; /* tokens per page = tokens per block */
+  uint32_t page_tokens; /* tokens per page */
+  uint32_t pages_per_block; /* pages per block (a block is keyed and stored as
+                               one record); 0 is read as 1. Part of the
+                               record layout and of the namespace. */
   const int32_t* layer_window; /* host [n_layers] or NULL; 0 = global
                                   attention, >0 = sliding window (tokens).
                                   Part of the model identity. */
@@ -104,12 +107,13 @@ typedef struct tl_geometry {
   uint64_t record_bytes;   /* exact length of every record */
   uint64_t payload_offset; /* = metadata bytes, a multiple of 256 */
   uint64_t slab_bytes;
-  uint32_t n_slabs;        /* 2 * n_layers: slab s = 2*layer + (0 K, 1 V) */
+  uint32_t n_slabs;        /* 2 * n_layers * pages_per_block: slab
+                              s = (2*layer + (0 K, 1 V)) * pages_per_block + page */
   uint32_t chunks_per_slab;
   uint32_t n_segments;     /* digest table entries = n_slabs*chunks_per_slab */
   uint32_t n_groups;       /* max(layer_group) + 1 */
-  uint32_t block_bytes;    /* key-chain input per block = 4 * page_tokens */
-  uint32_t reserved;
+  uint32_t block_bytes;    /* key-chain input per block = 4 * tokens per block */
+  uint32_t pages_per_block;
 } tl_geometry;
 
 /* A paged KV cache in HBM. Page p of layer l's K cache starts at device
@@ -128,10 +132,12 @@ typedef struct tl_cache {
 typedef struct tl_blocks {
   const uint8_t* d_keys;         /* [n][32] block keys (from tl_block_keys) */
   const uint64_t* d_block_index; /* [n] block position in its document */
-  const uint32_t* d_tokens;      /* [n][page_tokens] token ids; tl_save:
+  const uint32_t* d_tokens;      /* [n][tokens per block] token ids; tl_save:
                                     required; tl_load: NULL skips the TOKENS
                                     check */
-  const int32_t* d_tables;       /* [n_groups][n] page ids. tl_save: every
+  const int32_t* d_tables;       /* [n_groups][n * pages_per_block] page ids,
+                                    page j of block b at b*pages_per_block+j.
+                                    tl_save: every
                                     entry must be in [0, n_pages). tl_load:
                                     -1 = do not restore that layer group for
                                     this block (its slabs are not read). */
@@ -143,7 +149,8 @@ typedef struct tl_index tl_index;
 /* ---- context --------------------------------------------------------- */
 /* Create a context for one tenant and one model (Sec. 2.1, Sec. 2.2). The
  * namespace digest SHA-256("taliesin-ns-v1" | u32 len | tenant | u32 len |
- * model_fp | u32 L,H,D,dtype,P | i32 window per layer) roots every key chain
+ * model_fp | u32 L,H,D,dtype,P,pages_per_block | i32 window per layer) roots
+ * every key chain
  * and is stored in every record. Returns NULL and sets *status (if non-NULL)
  * to TL_ENOIDENT when tenant or model_fp is empty, TL_ELAYOUT when the
  * geometry is unsupported, TL_EINVAL for NULL layout, TL_ENOMEM. */
@@ -160,7 +167,7 @@ size_t tl_workspace_bytes(const tl_ctx* ctx, size_t n_blocks);
 /* ---- a1: chained block keys (host) -------------------------------------
  * k_{-1} = parent (NULL: the context's namespace digest),
  * k_i = SHA-256(k_{i-1} | bytes[i*B, (i+1)*B)), B = block_bytes (0: the
- * context's 4*page_tokens, i.e. u32 little-endian token ids). Only full blocks
+ * context's 4 * tokens per block, i.e. u32 little-endian token ids). Only full blocks
  * get a key; a partial tail is left for prefill. Sets *n_keys = n_full and
  * writes the n_full keys (32 bytes each) to keys_out; TL_ERANGE, with nothing
  * written, if cap < n_full.

@@ -53,6 +53,7 @@ NS_TAG = b"taliesin-ns-v1"
 DTYPE_BYTES = {1: 2, 2: 2, 3: 4, 4: 1}  # bf16, f16, f32, fp8
 MAX_LAYERS = 256
 MAX_GROUPS = 8
+MAX_PAGES_PER_BLOCK = 1 << 16
 
 # verdicts: a smaller code wins when several checks fail
 ACCEPT = 0x01
@@ -84,7 +85,9 @@ class IdentityError(ValueError):
 # ------------------------------------------------------------------ geometry
 @dataclass(frozen=True)
 class Layout:
-    """Model KV geometry: per layer, K and V caches are [pages][P][H][D]."""
+    """Model KV geometry: per layer, K and V caches are [pages][P][H][D]; a
+    block (the unit that is keyed and stored as one record) spans
+    pages_per_block consecutive positions' pages."""
 
     n_layers: int
     n_kv_heads: int
@@ -93,12 +96,15 @@ class Layout:
     page_tokens: int
     layer_window: Tuple[int, ...] = ()
     layer_group: Tuple[int, ...] = ()
+    pages_per_block: int = 1
 
     def __post_init__(self):
         if not (1 <= self.n_layers <= MAX_LAYERS):
             raise LayoutError("n_layers out of range")
         if self.n_kv_heads < 1 or self.head_dim < 1 or self.page_tokens < 1:
             raise LayoutError("zero-sized dimension")
+        if not (1 <= self.pages_per_block <= MAX_PAGES_PER_BLOCK):
+            raise LayoutError("pages per block out of range")
         if self.dtype not in DTYPE_BYTES:
             raise LayoutError("unknown dtype")
         if self.slab_bytes % ROW_BYTES:
@@ -127,7 +133,12 @@ class Layout:
 
     @property
     def n_slabs(self):
-        return 2 * self.n_layers
+        """Slabs per record: every page of the block, for every layer, K and V."""
+        return 2 * self.n_layers * self.pages_per_block
+
+    @property
+    def block_tokens(self):
+        return self.page_tokens * self.pages_per_block
 
     @property
     def chunks_per_slab(self):
@@ -142,7 +153,7 @@ class Layout:
 
     @property
     def meta_bytes(self):
-        raw = HEADER_BYTES + 8 * self.n_segments + 4 * self.page_tokens
+        raw = HEADER_BYTES + 8 * self.n_segments + 4 * self.block_tokens
         return -(-raw // META_ALIGN) * META_ALIGN
 
     @property
@@ -156,12 +167,22 @@ class Layout:
     @property
     def block_bytes(self):
         """Key-chain input per block: the block's token ids as u32 LE."""
-        return 4 * self.page_tokens
+        return 4 * self.block_tokens
+
+    @property
+    def meta_end(self):
+        """End of the token ids inside the metadata (zero padding follows)."""
+        return HEADER_BYTES + 8 * self.n_segments + 4 * self.block_tokens
 
 
-def slab_index(layer: int, kv: int) -> int:
-    """Record order: layer-major, K before V."""
-    return 2 * layer + kv
+def slab_index(lay: Layout, layer: int, kv: int, j: int = 0) -> int:
+    """Record order: layer-major, K before V, then the block's pages in order."""
+    return (2 * layer + kv) * lay.pages_per_block + j
+
+
+def table_entry(lay: Layout, tables, layer: int, b: int, j: int = 0) -> int:
+    """Page id of page j of block b for `layer`: tables[group][b * ppb + j]."""
+    return int(tables[lay.group(layer)][b * lay.pages_per_block + j])
 
 
 # ------------------------------------------------------------------ identity
@@ -174,7 +195,8 @@ def namespace_digest(tenant: bytes, model_fp: bytes, lay: Layout) -> bytes:
     m = bytearray(NS_TAG)
     m += struct.pack("<I", len(tenant)) + bytes(tenant)
     m += struct.pack("<I", len(model_fp)) + bytes(model_fp)
-    m += struct.pack("<5I", lay.n_layers, lay.n_kv_heads, lay.head_dim, lay.dtype, lay.page_tokens)
+    m += struct.pack("<6I", lay.n_layers, lay.n_kv_heads, lay.head_dim, lay.dtype, lay.page_tokens,
+                     lay.pages_per_block)
     for l in range(lay.n_layers):
         m += struct.pack("<i", lay.window(l))
     return hashlib.sha256(bytes(m)).digest()
@@ -246,26 +268,27 @@ def header_fields(lay: Layout, ns: bytes, key: bytes, block_index: int) -> bytes
     h[72:104] = key
     h[104:136] = ns
     struct.pack_into("<II", h, 136, CHUNK_BYTES, lay.n_segments)
+    struct.pack_into("<I", h, 152, lay.pages_per_block)
     return bytes(h)
 
 
 def make_meta(lay: Layout, ns: bytes, key: bytes, block_index: int, tokens, table: Sequence[int]) -> bytes:
     toks = np.asarray(tokens, dtype="<u4")
-    assert toks.size == lay.page_tokens and len(table) == lay.n_segments
+    assert toks.size == lay.block_tokens and len(table) == lay.n_segments
     m = bytearray(lay.meta_bytes)
     m[0:HEADER_BYTES] = header_fields(lay, ns, key, block_index)
     off = HEADER_BYTES
     for t in table:
         struct.pack_into("<Q", m, off, t)
         off += 8
-    m[off:off + 4 * lay.page_tokens] = toks.tobytes()
+    m[off:off + 4 * lay.block_tokens] = toks.tobytes()
     struct.pack_into("<Q", m, ROOT_OFFSET, root_digest(bytes(m)))
     return bytes(m)
 
 
 def make_record(lay: Layout, ns: bytes, key: bytes, block_index: int, tokens, slabs) -> bytes:
-    """One block's record: metadata, then the 2L slabs in layer-major K,V order
-    (Sec. 2.2: save the KV state of a block under its fingerprint)."""
+    """One block's record: metadata, then the slabs in layer-major, K-before-V,
+    page order (Sec. 2.2: save the KV state of a block under its fingerprint)."""
     assert len(slabs) == lay.n_slabs
     table = []
     for s in slabs:
@@ -282,37 +305,42 @@ def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens
     """Gather every block's pages into a record.
 
     src_k[l], src_v[l]: uint8 arrays [pages, >= slab_bytes] (page rows).
-    tables: [n_groups][n_blocks] page ids; layer l uses tables[group(l)].
+    tables: [n_groups][n_blocks * pages_per_block] page ids; layer l uses
+    tables[group(l)], page j of block b at index b * pages_per_block + j.
     Returns (records, status): a block with any page id outside [0, n_pages)
     gets an all-zero record and status BADARG, else status ACCEPT."""
     tables = np.asarray(tables)
     n = len(keys)
+    ppb = lay.pages_per_block
     n_pages = src_k[0].shape[0] if n_pages is None else n_pages
     used = sorted({lay.group(l) for l in range(lay.n_layers)})
     records, status = [], []
     for b in range(n):
-        if not all(_page_ok(int(tables[g][b]), n_pages) for g in used):
+        if not all(_page_ok(int(tables[g][b * ppb + j]), n_pages) for g in used for j in range(ppb)):
             records.append(bytes(lay.record_bytes))
             status.append(BADARG)
             continue
         slabs = []
         for l in range(lay.n_layers):
-            page = int(tables[lay.group(l)][b])
             for kv, src in ((0, src_k), (1, src_v)):
-                slabs.append(np.asarray(src[l][page, :lay.slab_bytes]).tobytes())
+                for j in range(ppb):
+                    page = table_entry(lay, tables, l, b, j)
+                    slabs.append(np.asarray(src[l][page, :lay.slab_bytes]).tobytes())
         records.append(make_record(lay, ns, keys[b], int(block_index[b]), tokens[b], slabs))
         status.append(ACCEPT)
     return records, status
 
 
 # ------------------------------------------------------------------ verify
-def read_slabs(lay: Layout, tables, b: int) -> List[Tuple[int, int, int]]:
-    """(slab index, layer, kv) of the slabs a load reads for block b: every
-    slab whose layer's table entry is not -1."""
+def read_slabs(lay: Layout, tables, b: int) -> List[Tuple[int, int, int, int]]:
+    """(slab index, layer, kv, page j) of the slabs a load reads for block b:
+    every slab whose table entry is not -1."""
     out = []
     for l in range(lay.n_layers):
-        if int(tables[lay.group(l)][b]) != -1:
-            out.extend([(slab_index(l, 0), l, 0), (slab_index(l, 1), l, 1)])
+        for kv in (0, 1):
+            for j in range(lay.pages_per_block):
+                if table_entry(lay, tables, l, b, j) != -1:
+                    out.append((slab_index(lay, l, kv, j), l, kv, j))
     return out
 
 
@@ -327,8 +355,7 @@ def check_meta(lay: Layout, ns: bytes, rec: bytes, key: bytes, block_index: int,
     got[64:72] = bytes(8)  # block index, checked as POSITION
     got[72:104] = bytes(32)  # key, checked as KEY
     got[ROOT_OFFSET:ROOT_OFFSET + 8] = bytes(8)
-    tok_end = HEADER_BYTES + 8 * lay.n_segments + 4 * lay.page_tokens
-    if bytes(got) != want or any(meta[tok_end:]):
+    if bytes(got) != want or any(meta[lay.meta_end:]):
         return HEADER
     if struct.unpack_from("<Q", meta, 64)[0] != block_index:
         return POSITION
@@ -336,7 +363,7 @@ def check_meta(lay: Layout, ns: bytes, rec: bytes, key: bytes, block_index: int,
         return KEY
     if tokens is not None:
         t0 = HEADER_BYTES + 8 * lay.n_segments
-        if meta[t0:t0 + 4 * lay.page_tokens] != np.asarray(tokens, dtype="<u4").tobytes():
+        if meta[t0:t0 + 4 * lay.block_tokens] != np.asarray(tokens, dtype="<u4").tobytes():
             return TOKENS
     return ACCEPT
 
@@ -374,9 +401,9 @@ def restore(lay: Layout, ns: bytes, records, keys, block_index, tokens, tables,
             dst_k, dst_v, n_pages=None, misaligned=()):
     """Verify every listed block and scatter accepted ones into the paged cache.
 
-    records[b]: bytes or None; tokens: [n][P] or None (no token check);
-    tables: [n_groups][n] destination page ids (-1 = do not restore that
-    layer group for this block). Accepted blocks: every read slab is copied to
+    records[b]: bytes or None; tokens: [n][block tokens] or None (no token
+    check); tables: [n_groups][n * pages_per_block] destination page ids
+    (-1 = do not restore that page of that layer group). Accepted blocks: every read slab is copied to
     its page. Rejected blocks: every in-range page the block would have
     written is zero-filled. Pages of other blocks and -1 entries are untouched.
     Returns the verdict list."""
@@ -387,12 +414,12 @@ def restore(lay: Layout, ns: bytes, records, keys, block_index, tokens, tables,
     verdicts = []
     for b in range(n):
         slabs = read_slabs(lay, tables, b)
-        pages = [int(tables[lay.group(l)][b]) for (_, l, _) in slabs]
+        pages = [table_entry(lay, tables, l, b, j) for (_, l, _, j) in slabs]
         bad = b in misaligned or any(not _page_ok(p, n_pages) for p in pages)
         v = verify(lay, ns, records[b], keys[b], int(block_index[b]),
-                   None if tokens is None else tokens[b], [s for (s, _, _) in slabs], bad)
+                   None if tokens is None else tokens[b], [s for (s, *_) in slabs], bad)
         verdicts.append(v)
-        for (s, l, kv), p in zip(slabs, pages):
+        for (s, l, kv, _), p in zip(slabs, pages):
             if not _page_ok(p, n_pages):
                 continue
             dst = dst_k[l] if kv == 0 else dst_v[l]

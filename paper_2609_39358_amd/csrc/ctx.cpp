@@ -30,6 +30,8 @@ void put64(uint8_t* p, uint64_t v) { for (int i = 0; i < 8; ++i) p[i] = (uint8_t
 int make_geometry(const tl_layout* lay, tl::Geo* g) {
   if (lay->n_layers < 1 || lay->n_layers > TL_MAX_LAYERS) return TL_ELAYOUT;
   if (!lay->n_kv_heads || !lay->head_dim || !lay->page_tokens) return TL_ELAYOUT;
+  const uint32_t ppb = lay->pages_per_block ? lay->pages_per_block : 1;
+  if (ppb > tl::kMaxPagesPerBlock) return TL_ELAYOUT;
   const uint32_t e = elem_bytes(lay->dtype);
   if (!e) return TL_ELAYOUT;
   // slab = P*H*D*e, guarded against overflow; at most 2^31 bytes
@@ -44,13 +46,19 @@ int make_geometry(const tl_layout* lay, tl::Geo* g) {
   if (slab > lim || slab % tl::kRowBytes) return TL_ELAYOUT;
   memset(g, 0, sizeof *g);
   g->n_layers = lay->n_layers;
-  g->n_slabs = 2 * lay->n_layers;
+  g->ppb = ppb;
+  if ((uint64_t)2 * lay->n_layers * ppb * ((slab + tl::kChunkBytes - 1) / tl::kChunkBytes) >= (1ull << 28))
+    return TL_ELAYOUT;  // digest table entries per record
+  g->n_slabs = 2 * lay->n_layers * ppb;
   g->slab_bytes = slab;
   g->cps = (uint32_t)((slab + tl::kChunkBytes - 1) / tl::kChunkBytes);
   g->n_seg = g->n_slabs * g->cps;
   g->page_tokens = lay->page_tokens;
+  const uint64_t block_tokens = (uint64_t)lay->page_tokens * ppb;
+  if (block_tokens >= (1ull << 28)) return TL_ELAYOUT;
+  g->block_tokens = (uint32_t)block_tokens;
   const uint64_t tok_off = tl::kHeaderBytes + 8ull * g->n_seg;
-  const uint64_t tok_end = tok_off + 4ull * lay->page_tokens;
+  const uint64_t tok_end = tok_off + 4ull * block_tokens;
   const uint64_t meta = (tok_end + tl::kMetaAlign - 1) / tl::kMetaAlign * tl::kMetaAlign;
   if (meta > lim) return TL_ELAYOUT;
   g->tok_off = (uint32_t)tok_off;
@@ -91,10 +99,10 @@ tl_ctx* tl_ctx_create(const void* tenant, size_t tenant_len, const void* model_f
   int r = make_geometry(layout, &c->geo);
   if (r) { delete c; *st = r; return nullptr; }
   c->L = layout->n_layers; c->H = layout->n_kv_heads; c->D = layout->head_dim;
-  c->dtype = layout->dtype; c->P = layout->page_tokens;
+  c->dtype = layout->dtype; c->P = layout->page_tokens; c->ppb = c->geo.ppb;
   for (uint32_t l = 0; l < c->L; ++l) c->window[l] = layout->layer_window ? layout->layer_window[l] : 0;
 
-  // namespace digest: tag | u32 len | tenant | u32 len | fp | u32 L,H,D,dtype,P | i32 windows
+  // namespace digest: tag | u32 len | tenant | u32 len | fp | u32 L,H,D,dtype,P,ppb | i32 windows
   std::vector<uint8_t> m;
   m.insert(m.end(), tl::kNsTag, tl::kNsTag + strlen(tl::kNsTag));
   uint8_t w[4];
@@ -102,7 +110,7 @@ tl_ctx* tl_ctx_create(const void* tenant, size_t tenant_len, const void* model_f
   m.insert(m.end(), (const uint8_t*)tenant, (const uint8_t*)tenant + tenant_len);
   put32(w, (uint32_t)model_fp_len); m.insert(m.end(), w, w + 4);
   m.insert(m.end(), (const uint8_t*)model_fp, (const uint8_t*)model_fp + model_fp_len);
-  const uint32_t dims[5] = {c->L, c->H, c->D, c->dtype, c->P};
+  const uint32_t dims[6] = {c->L, c->H, c->D, c->dtype, c->P, c->ppb};
   for (uint32_t d : dims) { put32(w, d); m.insert(m.end(), w, w + 4); }
   for (uint32_t l = 0; l < c->L; ++l) { put32(w, (uint32_t)c->window[l]); m.insert(m.end(), w, w + 4); }
   tl::sha256(m.data(), m.size(), nullptr, 0, c->ns);
@@ -120,6 +128,7 @@ tl_ctx* tl_ctx_create(const void* tenant, size_t tenant_len, const void* model_f
   memcpy(h + tl::kNsOffset, c->ns, 32);
   put32(h + 136, tl::kChunkBytes);
   put32(h + 140, c->geo.n_seg);
+  put32(h + tl::kPpbOffset, c->ppb);
   *st = TL_OK;
   return c;
 }
@@ -136,7 +145,8 @@ int tl_ctx_geometry(const tl_ctx* ctx, tl_geometry* out) {
   out->chunks_per_slab = ctx->geo.cps;
   out->n_segments = ctx->geo.n_seg;
   out->n_groups = ctx->geo.n_groups;
-  out->block_bytes = 4 * ctx->P;
+  out->block_bytes = 4 * ctx->geo.block_tokens;
+  out->pages_per_block = ctx->ppb;
   return TL_OK;
 }
 
@@ -164,7 +174,7 @@ static void chain(const uint8_t* parent, const uint8_t* bytes, size_t n_full, si
 int tl_block_keys(const tl_ctx* ctx, const uint8_t* parent, const void* bytes, size_t n_bytes,
                   size_t block_bytes, uint8_t* keys_out, size_t cap, size_t* n_keys) {
   if (!ctx || !n_keys || (n_bytes && !bytes)) return TL_EINVAL;
-  const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->P;
+  const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->geo.block_tokens;
   const size_t n_full = n_bytes / B;
   *n_keys = n_full;
   if (n_full > cap) return TL_ERANGE;
@@ -178,7 +188,7 @@ int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* b
                         size_t block_bytes, uint8_t* keys_out, const uint64_t* key_off,
                         uint64_t* n_keys_out, int n_threads) {
   if (!ctx || (n_docs && (!bytes || !doc_off || !doc_len || !keys_out || !key_off))) return TL_EINVAL;
-  const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->P;
+  const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->geo.block_tokens;
   std::atomic<size_t> next{0};
   auto work = [&]() {
     for (size_t d; (d = next.fetch_add(1)) < n_docs;) {

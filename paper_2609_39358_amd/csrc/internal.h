@@ -18,6 +18,8 @@ constexpr uint32_t kRootOffset = 144;
 constexpr uint32_t kIndexOffset = 64;    // block index (position)
 constexpr uint32_t kKeyOffset = 72;
 constexpr uint32_t kNsOffset = 104;
+constexpr uint32_t kPpbOffset = 152;     // pages per block
+constexpr uint32_t kMaxPagesPerBlock = 1u << 16;
 static const char kMagic[9] = "TLSNKV01";
 static const char kNsTag[] = "taliesin-ns-v1";
 
@@ -26,10 +28,12 @@ struct Geo {
   uint64_t payload_offset;  // = meta bytes
   uint64_t slab_bytes;
   uint32_t n_layers;
-  uint32_t n_slabs;
+  uint32_t ppb;             // pages per block
+  uint32_t n_slabs;         // 2 * n_layers * ppb
   uint32_t cps;             // chunks per slab
   uint32_t n_seg;           // digest table entries
   uint32_t page_tokens;
+  uint32_t block_tokens;    // page_tokens * ppb
   uint32_t tok_off;         // byte offset of the token ids in the metadata
   uint32_t tok_end;         // end of the token ids (padding follows)
   uint32_t n_groups;
@@ -40,7 +44,7 @@ struct Geo {
 }  // namespace tl
 
 struct tl_ctx {
-  uint32_t L, H, D, dtype, P;
+  uint32_t L, H, D, dtype, P, ppb;
   int32_t window[TL_MAX_LAYERS];
   tl::Geo geo;
   uint8_t ns[32];

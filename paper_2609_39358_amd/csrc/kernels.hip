@@ -15,7 +15,8 @@
 //          k_save_meta (header, token ids, padding, root over the metadata)
 //   load:  k_load_meta (pointer/length/root/header/position/key/token checks)
 //          k_load_seg  (record -> page copy + chunk digest + compare)
-//          k_load_final(verdicts; zero-fill pages of blocks failing a chunk)
+//          k_load_final(verdicts; zero-fill pages of blocks failing a chunk,
+//                       one workgroup per group of 64 chunks)
 //
 // Sec. 2.2 (save under a fingerprint, check on load, recompute on failure),
 // Sec. 3 Table 1 (bit-identical restore), Sec. 5 (block-level reuse, fail
@@ -209,9 +210,10 @@ struct MetaArgs {
   uint32_t tmpl[tl::kHeaderBytes / 4];
 };
 
-// Slab work item -> (block, table entry, page base, record chunk offset).
+// Chunk work item: block b, digest-table index t = s * cps + k (slab s, chunk
+// k of the slab); slab s = (2 * layer + kv) * ppb + j holds page j of the block.
 struct Item {
-  uint32_t b, t, s, k, rows;
+  uint32_t b, t, s, k, rows, layer, kv;
   int32_t page;
 };
 
@@ -227,16 +229,19 @@ __device__ __forceinline__ Item decode(const SegArgs& a, uint32_t w) {
   }
   it.s = it.t / a.g.cps;
   it.k = it.t - it.s * a.g.cps;
-  const uint32_t layer = it.s >> 1;
-  it.page = a.tables[(uint64_t)a.g.group[layer] * a.n + it.b];
+  const uint32_t side = it.s / a.g.ppb;
+  const uint32_t j = it.s - side * a.g.ppb;
+  it.layer = side >> 1;
+  it.kv = side & 1;
+  const uint64_t row = (uint64_t)a.n * a.g.ppb;  // table entries per group
+  it.page = a.tables[(uint64_t)a.g.group[it.layer] * row + (uint64_t)it.b * a.g.ppb + j];
   const uint64_t clen = a.g.slab_bytes - (uint64_t)it.k * tl::kChunkBytes;
   it.rows = (uint32_t)((clen < tl::kChunkBytes ? clen : tl::kChunkBytes) / tl::kRowBytes);
   return it;
 }
 
 __device__ __forceinline__ char* page_chunk(const SegArgs& a, const Item& it) {
-  const uint32_t layer = it.s >> 1;
-  const uint64_t base = (it.s & 1) ? a.lv[layer] : a.lk[layer];
+  const uint64_t base = it.kv ? a.lv[it.layer] : a.lk[it.layer];
   return (char*)(base + (uint64_t)it.page * (uint64_t)a.stride + (uint64_t)it.k * tl::kChunkBytes);
 }
 
@@ -320,12 +325,22 @@ __device__ __forceinline__ bool page_in_range(int32_t p, int64_t n_pages) {
 }
 
 // ---- save ---------------------------------------------------------------------
-__device__ __forceinline__ bool block_pages_valid(const tl::Geo& g, const int32_t* tables,
-                                                  uint32_t n, uint32_t b, int64_t n_pages) {
-  bool ok = true;
-  for (uint32_t grp = 0; grp < g.n_groups; ++grp)
-    if (g.groups_used >> grp & 1) ok = ok && page_in_range(tables[(uint64_t)grp * n + b], n_pages);
-  return ok;
+// True when every page id of block b, in every table a layer uses, lies in
+// [lo, n_pages). The wavefront checks the block's entries 64 at a time; all
+// lanes must be active.
+__device__ __forceinline__ bool block_pages_ok(const tl::Geo& g, const int32_t* tables, uint32_t n,
+                                               uint32_t b, int64_t n_pages, int32_t lo, uint32_t lane) {
+  const uint64_t row = (uint64_t)n * g.ppb;
+  bool bad = false;
+  for (uint32_t grp = 0; grp < g.n_groups; ++grp) {
+    if (!(g.groups_used >> grp & 1)) continue;
+    const int32_t* t = tables + grp * row + (uint64_t)b * g.ppb;
+    for (uint32_t j = lane; j < g.ppb; j += 64) {
+      const int32_t p = t[j];
+      bad |= p < lo || (int64_t)p >= n_pages;
+    }
+  }
+  return !__any(bad);
 }
 
 __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
@@ -336,7 +351,7 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
     const uint64_t rec = a.rec[it.b];
     if (rec == 0 || (rec & 15)) continue;
     char* out = record_chunk(a, rec, it);
-    if (!block_pages_valid(a.g, a.tables, a.n, it.b, a.n_pages)) {
+    if (!block_pages_ok(a.g, a.tables, a.n, it.b, a.n_pages, 0, lane)) {
       zero_rows(out, it.rows, lane);  // k_save_meta zeroes the metadata
       continue;
     }
@@ -394,14 +409,14 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
     return;
   }
   const uint32_t meta = (uint32_t)a.g.payload_offset;
-  if (!block_pages_valid(a.g, a.tables, a.n, b, a.n_pages)) {
+  if (!block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, 0, lane)) {
     v4u* d = (v4u*)rec;
     for (uint32_t i = lane; i < meta / 16; i += 64) d[i] = zero4();
     if (lane == 0 && a.out_status) a.out_status[b] = TL_BADARG;
     return;
   }
   const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
-  const uint32_t* tok = a.tokens + (uint64_t)a.g.page_tokens * b;
+  const uint32_t* tok = a.tokens + (uint64_t)a.g.block_tokens * b;
   const uint64_t bi = a.bidx[b];
   uint64_t acc = root_init(lane);
   for (uint32_t off = 0; off < meta; off += kMetaTile) {
@@ -434,7 +449,9 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
   }
   const uint64_t root = finish_root(acc, meta);
   if (lane == 0) {
-    *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32), 0u, 0u};
+    // bytes 152..159 (pages per block, then zero) come from the expected header
+    *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32),
+                                         a.tmpl[tl::kRootOffset / 4 + 2], a.tmpl[tl::kRootOffset / 4 + 3]};
     if (a.out_status) a.out_status[b] = TL_ACCEPT;
   }
 }
@@ -447,18 +464,12 @@ __global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
   const uint32_t b = blockIdx.x;
   const uint64_t rec = a.rec[b];
   const uint64_t len = a.len[b];
+  // every lane takes part in the page-id check, so evaluate it up front
+  const bool pages_ok = block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, -1, lane);
   uint32_t code = 0;
   if (rec == 0) {
     code = TL_MISSING;
-  } else if ((rec & 15) || ![&] {
-               bool ok = true;
-               for (uint32_t grp = 0; grp < a.g.n_groups; ++grp)
-                 if (a.g.groups_used >> grp & 1) {
-                   const int32_t p = a.tables[(uint64_t)grp * a.n + b];
-                   ok = ok && p >= -1 && (int64_t)p < a.n_pages;
-                 }
-               return ok;
-             }()) {
+  } else if ((rec & 15) || !pages_ok) {
     code = TL_BADARG;
   } else if (len < a.g.record_bytes) {
     code = TL_TRUNCATED;
@@ -471,7 +482,7 @@ __global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
   }
   const uint32_t meta = (uint32_t)a.g.payload_offset;
   const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
-  const uint32_t* tok = a.tokens ? a.tokens + (uint64_t)a.g.page_tokens * b : nullptr;
+  const uint32_t* tok = a.tokens ? a.tokens + (uint64_t)a.g.block_tokens * b : nullptr;
   const uint64_t bi = a.bidx[b];
   bool hdr_bad = false, pos_bad = false, key_bad = false, tok_bad = false;
   uint64_t stored_root = 0;
@@ -538,22 +549,30 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_load_seg(SegArgs a) {
 struct FinalArgs {
   SegArgs s;
   uint8_t* verdicts;
+  uint32_t groups;        // chunk groups per block
+  uint32_t total_groups;  // n * groups
 };
 
-// One workgroup per block: the verdict, and the zero-fill of every page of a
-// block whose chunk check failed (its bytes were already copied).
+constexpr uint32_t kFinalGroup = 64;  // chunks per workgroup of k_load_final
+
+// One workgroup per (block, group of 64 chunks): the first group of each block
+// writes the verdict; if the block failed a chunk check (its bytes were
+// already copied), every workgroup of the block zero-fills its chunks' pages.
 __global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
   const SegArgs& a = f.s;
-  const uint32_t b = blockIdx.x;
-  const uint32_t st = a.status[b];
-  const uint32_t code = (st & 0xff) ? (st & 0xff) : (st & kSegFailBit) ? TL_SEGMENT : TL_ACCEPT;
-  if (threadIdx.x == 0) f.verdicts[b] = (uint8_t)code;
-  if (code != TL_SEGMENT) return;
-  for (uint32_t t = 0; t < a.g.n_seg; ++t) {
-    const Item it = decode(a, b * a.g.n_seg + t);
-    if (!page_in_range(it.page, a.n_pages)) continue;
-    v4u* d = (v4u*)page_chunk(a, it);
-    for (uint32_t i = threadIdx.x; i < it.rows * 64; i += blockDim.x) d[i] = zero4();
+  const uint32_t wave = uniform(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  for (uint32_t q = blockIdx.x; q < f.total_groups; q += gridDim.x) {
+    const uint32_t b = q / f.groups, gi = q - b * f.groups;
+    const uint32_t st = a.status[b];
+    const uint32_t code = (st & 0xff) ? (st & 0xff) : (st & kSegFailBit) ? TL_SEGMENT : TL_ACCEPT;
+    if (gi == 0 && threadIdx.x == 0) f.verdicts[b] = (uint8_t)code;
+    if (code != TL_SEGMENT) continue;
+    const uint32_t t_end = min(a.g.n_seg, (gi + 1) * kFinalGroup);
+    for (uint32_t t = gi * kFinalGroup + wave; t < t_end; t += 4) {
+      const Item it = decode(a, b * a.g.n_seg + t);
+      if (!page_in_range(it.page, a.n_pages)) continue;
+      zero_rows(page_chunk(a, it), it.rows, lane);
+    }
   }
 }
 
@@ -568,8 +587,9 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.stride = c->page_stride;
   a.n_pages = c->n_pages;
   a.n = (uint32_t)n;
-  a.t_begin = 2 * layer_begin * ctx->geo.cps;
-  a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.cps;
+  // layers [layer_begin, layer_end) own slabs [2 * begin * ppb, 2 * end * ppb)
+  a.t_begin = 2 * layer_begin * ctx->geo.ppb * ctx->geo.cps;
+  a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.ppb * ctx->geo.cps;
   a.total = (uint32_t)(n * a.n_sub);
   a.slab_major = 0;
   a.status = status;
@@ -681,6 +701,8 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
   FinalArgs f;
   fill_seg(f.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
   f.verdicts = d_verdicts;
+  f.groups = (ctx->geo.n_seg + kFinalGroup - 1) / kFinalGroup;
+  f.total_groups = (uint32_t)(n * f.groups);
   (void)hipGetLastError();
   timed(TL_KERNEL_LOAD_META, s, [&] {
     hipLaunchKernelGGL(k_load_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
@@ -689,7 +711,8 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
     hipLaunchKernelGGL(k_load_seg, dim3(seg_grid(f.s.total)), dim3(64 * kSegWaves), 0, s, f.s);
   });
   timed(TL_KERNEL_LOAD_FINAL, s, [&] {
-    hipLaunchKernelGGL(k_load_final, dim3((uint32_t)n), dim3(256), 0, s, f);
+    hipLaunchKernelGGL(k_load_final, dim3(f.total_groups < (1u << 20) ? f.total_groups : (1u << 20)),
+                       dim3(256), 0, s, f);
   });
   return launched();
 }

@@ -35,7 +35,7 @@ class TaliesinError(RuntimeError):
 class tl_layout(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_uint32), ("n_kv_heads", ctypes.c_uint32),
                 ("head_dim", ctypes.c_uint32), ("dtype", ctypes.c_uint32),
-                ("page_tokens", ctypes.c_uint32),
+                ("page_tokens", ctypes.c_uint32), ("pages_per_block", ctypes.c_uint32),
                 ("layer_window", ctypes.POINTER(ctypes.c_int32)),
                 ("layer_group", ctypes.POINTER(ctypes.c_uint8))]
 
@@ -45,7 +45,7 @@ class tl_geometry(ctypes.Structure):
                 ("slab_bytes", ctypes.c_uint64), ("n_slabs", ctypes.c_uint32),
                 ("chunks_per_slab", ctypes.c_uint32), ("n_segments", ctypes.c_uint32),
                 ("n_groups", ctypes.c_uint32), ("block_bytes", ctypes.c_uint32),
-                ("reserved", ctypes.c_uint32)]
+                ("pages_per_block", ctypes.c_uint32)]
 
 
 class tl_cache(ctypes.Structure):
@@ -177,8 +177,8 @@ class Ctx:
 
 def tl_ctx_create(tenant: bytes, model_fp: bytes, n_layers: int, n_kv_heads: int, head_dim: int,
                   dtype="bf16", page_tokens: int = 16, layer_window: Optional[Sequence[int]] = None,
-                  layer_group: Optional[Sequence[int]] = None) -> Ctx:
-    lay = tl_layout(n_layers, n_kv_heads, head_dim, DTYPE.get(dtype, dtype), page_tokens)
+                  layer_group: Optional[Sequence[int]] = None, pages_per_block: int = 1) -> Ctx:
+    lay = tl_layout(n_layers, n_kv_heads, head_dim, DTYPE.get(dtype, dtype), page_tokens, pages_per_block)
     keep = []
     if layer_window is not None:
         w = (ctypes.c_int32 * len(layer_window))(*layer_window)

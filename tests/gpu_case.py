@@ -23,13 +23,13 @@ def log(*a):
 
 def layout_of(geom: wl.Geometry) -> ref.Layout:
     return ref.Layout(geom.n_layers, geom.n_kv_heads, geom.head_dim, wl.DTYPE_CODES[geom.dtype],
-                      geom.page_tokens, geom.layer_window, geom.layer_group)
+                      geom.page_tokens, geom.layer_window, geom.layer_group, geom.pages_per_block)
 
 
 def ctx_of(geom: wl.Geometry, tenant=TEN, fp=FP) -> T.Ctx:
     return T.tl_ctx_create(tenant, fp, geom.n_layers, geom.n_kv_heads, geom.head_dim, geom.dtype,
                            geom.page_tokens, list(geom.layer_window) or None,
-                           list(geom.layer_group) or None)
+                           list(geom.layer_group) or None, geom.pages_per_block)
 
 
 def fill_cache(cache: PagedCache, geom: wl.Geometry, seed: int, pad_seed: int = 99):
@@ -68,7 +68,9 @@ def i64(a) -> torch.Tensor:
 
 
 class Case:
-    """n blocks of one document: src cache, keys, tokens, tables."""
+    """n blocks of one document: src cache, keys, tokens, tables. Tables hold
+    n * pages_per_block entries per layer group (page j of block b at
+    b * pages_per_block + j)."""
 
     def __init__(self, geom: wl.Geometry, n_blocks: int, src_pages: int, dst_pages: int, seed: int,
                  stride_extra: int = 0, tenant=TEN, block_index=None):
@@ -77,17 +79,17 @@ class Case:
         self.ctx = ctx_of(geom, tenant)
         self.ns = ref.namespace_digest(tenant, FP, self.lay)
         assert T.tl_ns_digest(self.ctx) == self.ns
-        P = geom.page_tokens
+        P = geom.block_tokens
         self.tokens = wl.tokens(n_blocks * P, seed).reshape(n_blocks, P)
         self.keys = T.tl_block_keys(self.ctx, self.tokens)
         assert self.keys.shape == (n_blocks, 32)
         self.bidx = np.arange(n_blocks, dtype=np.uint64) if block_index is None else np.asarray(block_index, np.uint64)
         self.stride = self.lay.slab_bytes + stride_extra
         self.src_pages, self.dst_pages = src_pages, dst_pages
-        G = geom.n_groups
-        t_src = wl.page_table(n_blocks, src_pages, seed, 0) if n_blocks else np.zeros(0, np.int32)
+        G, E = geom.n_groups, n_blocks * geom.pages_per_block
+        t_src = wl.page_table(E, src_pages, seed, 0) if E else np.zeros(0, np.int32)
         self.t_src = np.tile(t_src, (G, 1))
-        t_dst = wl.page_table(n_blocks, dst_pages, seed, 1) if n_blocks else np.zeros(0, np.int32)
+        t_dst = wl.page_table(E, dst_pages, seed, 1) if E else np.zeros(0, np.int32)
         self.t_dst = np.tile(t_dst, (G, 1))
         self.d_keys = torch.from_numpy(np.ascontiguousarray(self.keys)).to(DEV)
         self.d_bidx = i64(self.bidx)

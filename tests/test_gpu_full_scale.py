@@ -141,7 +141,7 @@ def test_hybrid_full_scale():
     assert np.array_equal(v, exp), np.nonzero(v != exp)
     for b in (10, 20, 253, 254):
         rec = store.buf[b].cpu().numpy().tobytes()
-        read = [s for s, _, _ in ref.read_slabs(c.lay, tables, b)]
+        read = [s for s, *_ in ref.read_slabs(c.lay, tables, b)]
         assert int(v[b]) == ref.verify(c.lay, c.ns, rec, c.keys[b].tobytes(), b, c.tokens[b], read), b
     good = [b for b in range(n) if b not in (20, 253)]
     check_pages_equal(c, dst, tables, blocks=good)
@@ -156,3 +156,60 @@ def test_hybrid_full_scale():
             p = int(tables[g.group(l)][b])
             if p >= 0:
                 assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
+
+
+def test_paper_sized_blocks_full_scale():
+    """The corpus as the paper stores it: blocks of ~8,800 tokens (11 blocks
+    for the corpus), here 550 pages of 16 tokens per block, one 4.3 GB record
+    per block. Every block is checked by verdicts and the permutation-copy
+    property; the oracle recomputes the metadata of every record and the
+    digests of 256 sampled chunks from the record bytes."""
+    base = wl.CONFIGS[2].geom
+    geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
+    n = 97000 // geom.block_tokens
+    assert n == 11
+    pages = n * 550
+    c = Case(geom, n, pages, pages, seed=2)
+    lay = c.lay
+    log("paper-sized blocks: %d records of %.2f GB" % (n, lay.record_bytes / 1e9))
+    toks = wl.tokens(97000, 2)
+    assert [k.tobytes() for k in T.tl_block_keys(c.ctx, toks)] == \
+        ref.block_keys(c.ns, toks.tobytes(), lay.block_bytes)
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    po, S, cps = lay.payload_offset, lay.slab_bytes, lay.chunks_per_slab
+    r = np.random.default_rng(3)
+    for b in range(n):
+        meta = store.buf[b, :po].cpu().numpy().tobytes()
+        assert meta[:256] == (lambda h: h[:144] + meta[144:152] + h[152:])(
+            ref.header_fields(lay, c.ns, c.keys[b].tobytes(), b))
+        assert int.from_bytes(meta[144:152], "little") == ref.root_digest(meta)
+        t0 = 256 + 8 * lay.n_segments
+        assert meta[t0:t0 + 4 * lay.block_tokens] == c.tokens[b].tobytes() and not any(meta[lay.meta_end:])
+        for s in r.choice(lay.n_slabs, 24, replace=False):
+            l, kv, j = (s // 550) >> 1, (s // 550) & 1, s % 550
+            page = int(c.t_src[0][b * 550 + j])
+            src = (c.src.k if kv == 0 else c.src.v)[l][page].cpu().numpy().tobytes()
+            body = store.buf[b, po + s * S: po + (s + 1) * S].cpu().numpy().tobytes()
+            assert body == src, (b, s)
+            for k in range(cps):
+                stored = int.from_bytes(meta[256 + 8 * (s * cps + k): 264 + 8 * (s * cps + k)], "little")
+                assert stored == ref.chunk_digest(body[k * 65536:(k + 1) * 65536]), (b, s, k)
+    # damage: one metadata bit in block 3, one payload bit in block 7
+    store.buf[3, 1000] ^= 2
+    store.buf[7, po + 12345678] ^= 64
+    dst = PagedCache(geom.n_layers, pages, c.stride, DEV)
+    for t in dst.k + dst.v:
+        t.fill_(0x11)
+    v = c.load(store.ptrs, store.lens, c.t_dst, dst)
+    exp = np.full(n, ref.ACCEPT)
+    exp[3], exp[7] = ref.ROOT, ref.SEGMENT
+    assert np.array_equal(v, exp), v
+    good = [b for b in range(n) if b not in (3, 7)]
+    ent = np.concatenate([np.arange(b * 550, (b + 1) * 550) for b in good])
+    check_pages_equal(c, dst, c.t_dst, blocks=ent)
+    for b in (3, 7):
+        for l in (0, geom.n_layers - 1):
+            p = torch.from_numpy(c.t_dst[0][b * 550:(b + 1) * 550].astype(np.int64)).to(DEV)
+            assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()

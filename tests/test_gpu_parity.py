@@ -79,6 +79,8 @@ GEOMS = {
     "two_chunks": (wl.Geometry(2, 16, 128, 32), 0),
     "ragged_chunk_padded": (wl.Geometry(1, 12, 128, 32), 1024),
     "hybrid": (wl.hybrid_geometry(n_layers=6, n_kv_heads=2, head_dim=64, page_tokens=16, window=32), 0),
+    "multi_page": (wl.Geometry(2, 2, 64, 16, pages_per_block=3), 0),
+    "multi_page_hybrid": (wl.Geometry(6, 2, 64, 16, "bf16", (32, 32, 32, 32, 32, 0), (1, 1, 1, 1, 1, 0), 2), 0),
 }
 
 
@@ -86,7 +88,9 @@ GEOMS = {
 def test_fault_zoo(name):
     geom, extra = GEOMS[name]
     n = 26
-    c = Case(geom, n, 40, 48, seed=11, stride_extra=extra)
+    ppb = geom.pages_per_block
+    cols = lambda b: slice(b * ppb, (b + 1) * ppb)  # table entries of block b
+    c = Case(geom, n, 40 * ppb, 48 * ppb, seed=11, stride_extra=extra)
     log("fault zoo", name, "slab", c.lay.slab_bytes, "record", c.lay.record_bytes)
     c.make_src()
     store, st = c.save()
@@ -128,12 +132,12 @@ def test_fault_zoo(name):
     keys = c.keys.copy(); keys[13, 0] ^= 1  # KEY
     bidx = c.bidx.copy(); bidx[12] = 999  # POSITION
     tables = c.t_dst.copy()
-    tables[:, 16] = -1  # not restored at all -> ACCEPT, nothing written
-    tables[0, 17] = c.dst_pages  # out of range -> BADARG
+    tables[:, cols(16)] = -1  # not restored at all -> ACCEPT, nothing written
+    tables[0, 17 * ppb + ppb - 1] = c.dst_pages  # one page id out of range -> BADARG
     if geom.n_groups > 1:
         # local layers restore only blocks 20..23 (window residency)
-        tables[1, :20] = -1
-        tables[1, 24:] = -1
+        tables[1, :20 * ppb] = -1
+        tables[1, 24 * ppb:] = -1
     dst = random_fill(PagedCache(geom.n_layers, c.dst_pages, c.stride, DEV), 5)
     hk0, hv0 = host_layers(dst)
     host_recs = [bytes(r) for r in recs]

@@ -18,7 +18,8 @@ pytestmark = pytest.mark.gpu
 @pytest.mark.parametrize("geom", [wl.CONFIGS[0].geom,
                                   wl.hybrid_geometry(n_layers=6, n_kv_heads=2, head_dim=64,
                                                      page_tokens=16, window=32),
-                                  wl.Geometry(3, 16, 128, 32)])
+                                  wl.Geometry(3, 16, 128, 32),
+                                  wl.Geometry(4, 2, 64, 16, pages_per_block=3)])
 def test_save_by_layer_ranges_equals_whole_save(geom):
     n = 20
     c = Case(geom, n, 32, 32, seed=12)

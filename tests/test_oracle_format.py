@@ -361,7 +361,7 @@ def test_hybrid_unread_slabs_not_checked_but_table_is():
     assert lay.group(5) == 0 and lay.group(0) == 1
     ns, key, toks, slabs, rec = make_block(lay, 9)
     tables = np.array([[0], [-1]])  # restore only the global layer's slabs
-    read = [s for s, _, _ in ref.read_slabs(lay, tables, 0)]
+    read = [s for s, *_ in ref.read_slabs(lay, tables, 0)]
     assert read == [10, 11]
     bad = bytearray(rec)
     bad[lay.payload_offset + 0 * lay.slab_bytes + 17] ^= 1  # slab of an unread layer
@@ -379,3 +379,82 @@ def test_window_blocks():
     assert list(wl.window_blocks(1000, 0, 256)) == [0, 1, 2, 3]
     assert list(wl.window_blocks(1000, 5000, 256)) == [0, 1, 2, 3]
     assert list(wl.window_blocks(1000, 100, 256)) == [3]
+
+
+# ---------------------------------------------------------------- multi-page blocks
+def test_multi_page_block_geometry_and_keys():
+    lay = ref.Layout(2, 1, 32, 1, 16, pages_per_block=3)
+    assert lay.n_slabs == 12 and lay.block_tokens == 48 and lay.block_bytes == 192
+    assert lay.meta_bytes == 768 and lay.record_bytes == 768 + 12 * 1024  # 256 + 96 + 192 -> 768
+    with pytest.raises(ref.LayoutError):
+        ref.Layout(2, 1, 32, 1, 16, pages_per_block=0)
+    # the record layout is part of the identity: other pages_per_block, other namespace
+    assert ref.namespace_digest(TEN, FP, lay) != ref.namespace_digest(TEN, FP, ref.Layout(2, 1, 32, 1, 16))
+    ns = ref.namespace_digest(TEN, FP, lay)
+    toks = wl.tokens(48 * 4 + 20, 3).tobytes()
+    k3 = ref.block_keys(ns, toks, lay.block_bytes)
+    assert len(k3) == 4  # whole 48-token blocks only
+    # a 48-token block key is not the key of its 16-token pages
+    assert k3[0] not in ref.block_keys(ns, toks, 64)
+
+
+def test_multi_page_slab_order_is_layer_kv_page():
+    lay = ref.Layout(2, 1, 32, 1, 16, pages_per_block=3)
+    assert [ref.slab_index(lay, l, kv, j) for l in range(2) for kv in (0, 1) for j in range(3)] == list(range(12))
+    ns = ref.namespace_digest(TEN, FP, lay)
+    toks = wl.tokens(48, 4)
+    key = ref.block_keys(ns, toks.tobytes(), lay.block_bytes)[0]
+    sk, sv = _caches(lay, 6, 700)
+    t = np.array([[4, 0, 5]], dtype=np.int32)
+    recs, st = ref.save(lay, ns, sk, sv, t, [key], [0], [toks])
+    po, S = lay.payload_offset, lay.slab_bytes
+    rec = recs[0]
+    # slab (l, kv, j) is page t[0][j] of layer l's K (kv 0) or V (kv 1), verbatim
+    for l in range(2):
+        for kv, src in ((0, sk), (1, sv)):
+            for j in range(3):
+                s = (2 * l + kv) * 3 + j
+                assert rec[po + s * S: po + (s + 1) * S] == src[l][t[0][j]].tobytes()
+    assert struct.unpack_from("<I", rec, 152)[0] == 3
+    assert rec[256 + 8 * 12: 256 + 8 * 12 + 4 * 48] == toks.tobytes()
+
+
+def test_multi_page_restore_is_the_permutation_copy_with_partial_groups():
+    lay = ref.Layout(4, 1, 32, 1, 16, (0, 16, 0, 16), (0, 1, 0, 1), pages_per_block=2)
+    n, pages = 5, 16
+    ns = ref.namespace_digest(TEN, FP, lay)
+    toks = wl.tokens(n * 32, 5)
+    keys = ref.block_keys(ns, toks.tobytes(), lay.block_bytes)
+    sk, sv = _caches(lay, pages, 800)
+    t_src = np.stack([wl.page_table(n * 2, pages, 1, 0), wl.page_table(n * 2, pages, 1, 1)])
+    recs, st = ref.save(lay, ns, sk, sv, t_src, keys, np.arange(n), toks.reshape(n, 32))
+    assert st == [ref.ACCEPT] * n
+    t_dst = np.stack([wl.page_table(n * 2, pages, 2, 0), wl.page_table(n * 2, pages, 2, 1)])
+    t_dst[1, :6] = -1  # group 1 (odd layers) restores only the last pages
+    dk, dv = _caches(lay, pages, 900)
+    dk0, dv0 = [x.copy() for x in dk], [x.copy() for x in dv]
+    vs = ref.restore(lay, ns, recs, keys, np.arange(n), toks.reshape(n, 32), t_dst, dk, dv)
+    assert vs == [ref.ACCEPT] * n
+    for l in range(4):
+        g = lay.group(l)
+        sel = t_dst[g] >= 0
+        for d, d0, s in ((dk[l], dk0[l], sk[l]), (dv[l], dv0[l], sv[l])):
+            want = d0.copy()
+            want[t_dst[g][sel]] = s[t_src[g][sel]]
+            assert np.array_equal(d, want), l
+
+
+def test_multi_page_every_bit_flip_rejected():
+    lay = ref.Layout(1, 1, 32, 1, 16, pages_per_block=2)
+    ns = ref.namespace_digest(TEN, FP, lay)
+    toks = wl.tokens(32, 6)
+    key = ref.block_keys(ns, toks.tobytes(), lay.block_bytes)[0]
+    slabs = [rand_bytes(lay.slab_bytes, 60 + s).tobytes() for s in range(lay.n_slabs)]
+    rec = ref.make_record(lay, ns, key, 0, toks, slabs)
+    assert len(rec) == 4608
+    po = lay.payload_offset
+    for bit in range(len(rec) * 8):
+        bad = bytearray(rec)
+        bad[bit >> 3] ^= 1 << (bit & 7)
+        v = ref.verify(lay, ns, bytes(bad), key, 0, toks, range(lay.n_slabs))
+        assert v == (ref.ROOT if (bit >> 3) < po else ref.SEGMENT), bit

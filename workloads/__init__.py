@@ -36,6 +36,7 @@ class Geometry:
     dtype: str = "bf16"
     layer_window: Tuple[int, ...] = ()  # per layer; 0 = global attention
     layer_group: Tuple[int, ...] = ()  # per layer; which block table it uses
+    pages_per_block: int = 1  # a block (one record) spans this many pages
 
     def window(self, layer: int) -> int:
         return self.layer_window[layer] if self.layer_window else 0
@@ -46,6 +47,10 @@ class Geometry:
     @property
     def n_groups(self) -> int:
         return (max(self.layer_group) + 1) if self.layer_group else 1
+
+    @property
+    def block_tokens(self) -> int:
+        return self.page_tokens * self.pages_per_block
 
     @property
     def page_bytes(self) -> int:
