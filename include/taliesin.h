@@ -258,8 +258,8 @@ size_t tl_index_size(const tl_index* idx);
  * records per launch when enabled. */
 #define TL_KERNEL_SAVE_SEG 0
 #define TL_KERNEL_SAVE_META 1
-#define TL_KERNEL_LOAD_META 2
-#define TL_KERNEL_LOAD_SEG 3
+#define TL_KERNEL_LOAD_INIT 2
+#define TL_KERNEL_LOAD_MAIN 3
 #define TL_KERNEL_LOAD_FINAL 4
 #define TL_KERNEL_COUNT 5
 int tl_timing(int enable);

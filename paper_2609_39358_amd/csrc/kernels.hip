@@ -13,10 +13,12 @@
 //
 //   save:  k_save_seg  (page -> record payload, chunk digest -> table)
 //          k_save_meta (header, token ids, padding, root over the metadata)
-//   load:  k_load_meta (pointer/length/root/header/position/key/token checks)
-//          k_load_seg  (record -> page copy + chunk digest + compare)
-//          k_load_final(verdicts; zero-fill pages of blocks failing a chunk,
-//                       one workgroup per group of 64 chunks)
+//   load:  k_load_init (clear the per-block status words)
+//          k_load_main (one grid: per block, pointer/length/root/header/
+//                       position/key/token checks; per chunk, record -> page
+//                       copy + chunk digest + compare)
+//          k_load_final(verdicts; zero-fill the pages of rejected blocks, one
+//                       workgroup per group of 64 chunks)
 //
 // Sec. 2.2 (save under a fingerprint, check on load, recompute on failure),
 // Sec. 3 Table 1 (bit-identical restore), Sec. 5 (block-level reuse, fail
@@ -39,7 +41,7 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 
 // Tuning knobs (compile-time; the defaults are the measured best on MI355X).
 #ifndef TL_SEG_WAVES
-#define TL_SEG_WAVES 4      // wavefronts per workgroup in the chunk kernels
+#define TL_SEG_WAVES 4      // wavefronts per workgroup in the save chunk kernel
 #endif
 #ifndef TL_BATCH_ROWS
 #define TL_BATCH_ROWS 8     // rows each lane has in flight per batch
@@ -56,8 +58,11 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 #ifndef TL_SAVE_SLAB_MAJOR
 #define TL_SAVE_SLAB_MAJOR 0  // save work order: 0 = block-major, 1 = slab-major
 #endif
+#ifndef TL_LOAD_SLAB_MAJOR
+#define TL_LOAD_SLAB_MAJOR 0  // load work order: 0 = block-major, 1 = slab-major
+#endif
 #ifndef TL_GRID_WGS_PER_CU
-#define TL_GRID_WGS_PER_CU 0  // >0: cap the chunk grid at this many workgroups per CU
+#define TL_GRID_WGS_PER_CU 0  // >0: cap the save chunk grid at this many workgroups per CU
 #endif
 
 constexpr uint32_t kSegWaves = TL_SEG_WAVES;
@@ -182,7 +187,8 @@ __device__ __forceinline__ uint32_t uniform(uint32_t x) { return __builtin_amdgc
 struct SegArgs {
   tl::Geo g;
   const uint64_t* rec;   // [n] record device addresses
-  const int32_t* tables; // [n_groups][n]
+  const uint64_t* len;   // load: [n] reported record lengths
+  const int32_t* tables; // [n_groups][n * ppb]
   const uint64_t* lk;    // [L] K cache bases
   const uint64_t* lv;    // [L] V cache bases
   int64_t stride;
@@ -457,11 +463,24 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
 }
 
 // ---- load ---------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
-  __shared__ uint64_t tile64[kMetaTile / 8];
+// A load is three launches. k_load_init clears the per-block status words.
+// k_load_main runs, in one grid, one metadata item per block (pointer, length,
+// root, header, position, key and token checks) and one chunk item per
+// (block, chunk) read (fused copy + digest + compare). Chunk items do not wait
+// for their block's metadata item: they copy whenever the record's pointer and
+// length allow reading it, and k_load_final, which turns the status words into
+// verdicts, zero-fills every page of a rejected block.
+
+__global__ __launch_bounds__(256) void k_load_init(uint32_t* status, uint32_t n) {
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) status[i] = 0;
+}
+
+// Metadata checks of block b by one wavefront, staging through `tile64`
+// (kMetaTile bytes of LDS). The workgroup must be this one wavefront: the
+// tile barriers are workgroup barriers.
+__device__ __forceinline__ void load_meta_item(const MetaArgs& a, uint32_t b, uint32_t lane,
+                                               uint64_t* tile64) {
   const uint32_t* tile32 = (const uint32_t*)tile64;
-  const uint32_t lane = threadIdx.x;
-  const uint32_t b = blockIdx.x;
   const uint64_t rec = a.rec[b];
   const uint64_t len = a.len[b];
   // every lane takes part in the page-id check, so evaluate it up front
@@ -477,7 +496,7 @@ __global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
     code = TL_OVERLONG;
   }
   if (code) {
-    if (lane == 0) a.status[b] = code;
+    if (lane == 0) atomicOr(&a.status[b], code);
     return;
   }
   const uint32_t meta = (uint32_t)a.g.payload_offset;
@@ -504,7 +523,7 @@ __global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
         else if (o == tl::kRootOffset || o == tl::kRootOffset + 4) {}
         else hdr_bad |= x != a.tmpl[o / 4];
       } else if (o < a.g.tok_off) {
-        // chunk digests: checked by k_load_seg, covered by the root
+        // chunk digests: checked by the chunk items, covered by the root
       } else if (o < a.g.tok_end) {
         if (tok) tok_bad |= x != tok[(o - a.g.tok_off) / 4];
       } else {
@@ -521,28 +540,39 @@ __global__ __launch_bounds__(64) void k_load_meta(MetaArgs a) {
   if (__any(tok_bad)) tok_bad = true;
   code = root_bad ? TL_ROOT : hdr_bad ? TL_HEADER : pos_bad ? TL_POSITION : key_bad ? TL_KEY
                                                                           : tok_bad ? TL_TOKENS : 0;
-  if (lane == 0) a.status[b] = code;
+  if (lane == 0 && code) atomicOr(&a.status[b], code);
 }
 
-__global__ __launch_bounds__(64 * kSegWaves) void k_load_seg(SegArgs a) {
-  const uint32_t lane = threadIdx.x & 63;
-  const uint32_t step = gridDim.x * kSegWaves;
-  for (uint32_t w = blockIdx.x * kSegWaves + uniform(threadIdx.x >> 6); w < a.total; w += step) {
-    const Item it = decode(a, w);
-    if (!page_in_range(it.page, a.n_pages)) continue;  // -1: not restored; else BADARG
-    char* dst = page_chunk(a, it);
-    const uint32_t st = a.status[it.b];
-    if (st & 0xff) {  // rejected by its metadata: never read the record, clear the page
-      zero_rows(dst, it.rows, lane);
-      continue;
-    }
-    const uint64_t rec = a.rec[it.b];
-    const uint64_t leaf = copy_hash(record_chunk(a, rec, it), dst, it.rows, lane);
-    const uint64_t digest = wave_sum64(leaf);
-    if (lane == 0) {
-      const uint64_t want = *(const uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t);
-      if (want != digest) atomicOr(&a.status[it.b], kSegFailBit);
-    }
+// Chunk item w: copy the chunk to its page, digest it on the way, compare
+// with the stored digest. Records with a bad pointer or length are never read.
+__device__ __forceinline__ void load_chunk_item(const SegArgs& a, uint32_t w, uint32_t lane) {
+  const Item it = decode(a, w);
+  if (!page_in_range(it.page, a.n_pages)) return;  // -1: not restored; else BADARG
+  const uint64_t rec = a.rec[it.b];
+  if (rec == 0 || (rec & 15) || a.len[it.b] != a.g.record_bytes) return;
+  const uint64_t leaf = copy_hash(record_chunk(a, rec, it), page_chunk(a, it), it.rows, lane);
+  const uint64_t digest = wave_sum64(leaf);
+  if (lane == 0) {
+    const uint64_t want = *(const uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t);
+    if (want != digest) atomicOr(&a.status[it.b], kSegFailBit);
+  }
+}
+
+struct LoadArgs {
+  MetaArgs m;
+  SegArgs s;
+};
+
+// Items [0, n) are metadata items, [n, n + n * chunks) chunk items; one
+// wavefront per workgroup (see load_meta_item).
+__global__ __launch_bounds__(64) void k_load_main(LoadArgs a) {
+  __shared__ uint64_t tile64[kMetaTile / 8];
+  const uint32_t lane = threadIdx.x;
+  const uint32_t n_meta = a.s.n;
+  const uint32_t total = n_meta + a.s.total;
+  for (uint32_t w = blockIdx.x; w < total; w += gridDim.x) {
+    if (w < n_meta) load_meta_item(a.m, w, lane, tile64);
+    else load_chunk_item(a.s, w - n_meta, lane);
   }
 }
 
@@ -556,8 +586,8 @@ struct FinalArgs {
 constexpr uint32_t kFinalGroup = 64;  // chunks per workgroup of k_load_final
 
 // One workgroup per (block, group of 64 chunks): the first group of each block
-// writes the verdict; if the block failed a chunk check (its bytes were
-// already copied), every workgroup of the block zero-fills its chunks' pages.
+// writes the verdict; if the block is rejected, every workgroup of the block
+// zero-fills its chunks' pages (some of which k_load_main may have written).
 __global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
   const SegArgs& a = f.s;
   const uint32_t wave = uniform(threadIdx.x >> 6), lane = threadIdx.x & 63;
@@ -566,7 +596,7 @@ __global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
     const uint32_t st = a.status[b];
     const uint32_t code = (st & 0xff) ? (st & 0xff) : (st & kSegFailBit) ? TL_SEGMENT : TL_ACCEPT;
     if (gi == 0 && threadIdx.x == 0) f.verdicts[b] = (uint8_t)code;
-    if (code != TL_SEGMENT) continue;
+    if (code == TL_ACCEPT) continue;
     const uint32_t t_end = min(a.g.n_seg, (gi + 1) * kFinalGroup);
     for (uint32_t t = gi * kFinalGroup + wave; t < t_end; t += 4) {
       const Item it = decode(a, b * a.g.n_seg + t);
@@ -581,6 +611,7 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   if (layer_end == 0) layer_end = ctx->geo.n_layers;
   a.g = ctx->geo;
   a.rec = rec;
+  a.len = nullptr;
   a.tables = tables;
   a.lk = c->d_layer_k;
   a.lv = c->d_layer_v;
@@ -696,19 +727,25 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
                 const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
                 uint8_t* d_verdicts, uint32_t* d_ws) {
   hipStream_t s = (hipStream_t)stream;
-  MetaArgs m;
-  fill_meta(m, ctx, n, d_rec, d_len, blk, dst->n_pages, d_ws, nullptr);
+  LoadArgs la;
+  fill_meta(la.m, ctx, n, d_rec, d_len, blk, dst->n_pages, d_ws, nullptr);
+  fill_seg(la.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
+  la.s.len = d_len;
+  la.s.slab_major = TL_LOAD_SLAB_MAJOR;
   FinalArgs f;
-  fill_seg(f.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
+  f.s = la.s;
+  f.s.slab_major = 0;
   f.verdicts = d_verdicts;
   f.groups = (ctx->geo.n_seg + kFinalGroup - 1) / kFinalGroup;
   f.total_groups = (uint32_t)(n * f.groups);
+  const uint32_t n_items = (uint32_t)n + la.s.total;
   (void)hipGetLastError();
-  timed(TL_KERNEL_LOAD_META, s, [&] {
-    hipLaunchKernelGGL(k_load_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+  timed(TL_KERNEL_LOAD_INIT, s, [&] {
+    const uint32_t g = (uint32_t)((n + 255) / 256);
+    hipLaunchKernelGGL(k_load_init, dim3(g < 4096 ? g : 4096), dim3(256), 0, s, d_ws, (uint32_t)n);
   });
-  timed(TL_KERNEL_LOAD_SEG, s, [&] {
-    hipLaunchKernelGGL(k_load_seg, dim3(seg_grid(f.s.total)), dim3(64 * kSegWaves), 0, s, f.s);
+  timed(TL_KERNEL_LOAD_MAIN, s, [&] {
+    hipLaunchKernelGGL(k_load_main, dim3(n_items < (1u << 22) ? n_items : (1u << 22)), dim3(64), 0, s, la);
   });
   timed(TL_KERNEL_LOAD_FINAL, s, [&] {
     hipLaunchKernelGGL(k_load_final, dim3(f.total_groups < (1u << 20) ? f.total_groups : (1u << 20)),

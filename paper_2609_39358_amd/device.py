@@ -13,10 +13,19 @@ from . import taliesin as T
 
 
 class PagedCache:
+    """K and V pages of every layer: one tensor per layer and K/V by default;
+    single=True puts all layers in one device allocation (layer l's K is
+    slice 2l, its V slice 2l+1). Callers may pass their own tensors."""
+
     def __init__(self, n_layers: int, n_pages: int, page_stride: int, device="cuda",
                  layers_k: Optional[List[torch.Tensor]] = None,
-                 layers_v: Optional[List[torch.Tensor]] = None):
+                 layers_v: Optional[List[torch.Tensor]] = None, single: bool = False):
         self.n_layers, self.n_pages, self.page_stride = n_layers, n_pages, page_stride
+        self.buf = None
+        if layers_k is None and single:
+            self.buf = torch.empty((2 * n_layers, n_pages, page_stride), dtype=torch.uint8, device=device)
+            layers_k = [self.buf[2 * l] for l in range(n_layers)]
+            layers_v = [self.buf[2 * l + 1] for l in range(n_layers)]
         mk = lambda: torch.empty((n_pages, page_stride), dtype=torch.uint8, device=device)
         self.k = layers_k if layers_k is not None else [mk() for _ in range(n_layers)]
         self.v = layers_v if layers_v is not None else [mk() for _ in range(n_layers)]

@@ -109,7 +109,7 @@ EXPORTED = (
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
     "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
     "tl_timing_read")
-KERNELS = {"save_seg": 0, "save_meta": 1, "load_meta": 2, "load_seg": 3, "load_final": 4}
+KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4}
 
 
 def lib():

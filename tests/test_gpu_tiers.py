@@ -22,7 +22,7 @@ pytestmark = pytest.mark.gpu
                                   wl.Geometry(4, 2, 64, 16, pages_per_block=3)])
 def test_save_by_layer_ranges_equals_whole_save(geom):
     n = 20
-    c = Case(geom, n, 32, 32, seed=12)
+    c = Case(geom, n, 32 * geom.pages_per_block, 32 * geom.pages_per_block, seed=12)
     c.make_src()
     whole, st = c.save()
     parts = RecordStore(n, c.lay.record_bytes, DEV)
