@@ -10,6 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(PKG, "libtaliesin.so")
+SABOTAGE_OUT = os.path.join(PKG, "libtaliesin_sabotage.so")  # test-only build with switchable checks
 BUILD_DIR = os.path.join(PKG, "_build")
 
 HIP_FLAGS = [
@@ -53,5 +54,13 @@ def build(verbose: bool = False, extra_hip_flags=(), out: str = OUT, build_dir: 
     return out
 
 
+def build_all(verbose: bool = False):
+    """The release library and the sabotage build used by the sabotage tests."""
+    out = build(verbose)
+    build(verbose, extra_hip_flags=("-DTL_SABOTAGE",), out=SABOTAGE_OUT,
+          build_dir=os.path.join(BUILD_DIR, "sabotage"))
+    return out
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build_all(verbose=True))

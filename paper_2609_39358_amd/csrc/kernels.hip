@@ -30,8 +30,22 @@
 #include <vector>
 
 #include "internal.h"
+#ifdef TL_SABOTAGE
+#include "taliesin_debug.h"
+#else
+#define TL_CHECK_ROOT 0u
+#define TL_CHECK_HEADER 0u
+#define TL_CHECK_POSITION 0u
+#define TL_CHECK_KEY 0u
+#define TL_CHECK_TOKENS 0u
+#define TL_CHECK_SEGMENT 0u
+#endif
 
 namespace {
+
+// Load checks switched off. Only the sabotage build (TL_SABOTAGE) can set it;
+// in the release library it is always 0.
+uint32_t g_disabled_checks = 0;
 
 constexpr uint64_t kP1 = 0x9E3779B185EBCA87ull;
 constexpr uint64_t kP2 = 0xC2B2AE3D27D4EB4Full;
@@ -198,6 +212,7 @@ struct SegArgs {
   uint32_t n_sub;        // chunks per block in that range
   uint32_t total;        // n * n_sub work items
   uint32_t slab_major;   // 1: consecutive work items are consecutive blocks of one chunk
+  uint32_t disabled;     // load checks switched off (sabotage build only; else 0)
   uint32_t* status;      // load: per-block status words
 };
 
@@ -213,6 +228,7 @@ struct MetaArgs {
   uint32_t n;
   uint32_t* status;          // load: status words; save: unused
   uint8_t* out_status;       // save: per-block status bytes (optional)
+  uint32_t disabled;         // load checks switched off (sabotage build only; else 0)
   uint32_t tmpl[tl::kHeaderBytes / 4];
 };
 
@@ -533,11 +549,18 @@ __device__ __forceinline__ void load_meta_item(const MetaArgs& a, uint32_t b, ui
     hash_tile(tile64, nb, off, lane, acc);
     __syncthreads();
   }
-  const bool root_bad = finish_root(acc, meta) != stored_root;
-  if (__any(hdr_bad)) hdr_bad = true;
-  if (__any(pos_bad)) pos_bad = true;
-  if (__any(key_bad)) key_bad = true;
-  if (__any(tok_bad)) tok_bad = true;
+  bool root_bad = finish_root(acc, meta) != stored_root;
+  hdr_bad = __any(hdr_bad);
+  pos_bad = __any(pos_bad);
+  key_bad = __any(key_bad);
+  tok_bad = __any(tok_bad);
+  if (a.disabled) {  // sabotage build: a switched-off check never fails
+    root_bad = root_bad && !(a.disabled & TL_CHECK_ROOT);
+    hdr_bad = hdr_bad && !(a.disabled & TL_CHECK_HEADER);
+    pos_bad = pos_bad && !(a.disabled & TL_CHECK_POSITION);
+    key_bad = key_bad && !(a.disabled & TL_CHECK_KEY);
+    tok_bad = tok_bad && !(a.disabled & TL_CHECK_TOKENS);
+  }
   code = root_bad ? TL_ROOT : hdr_bad ? TL_HEADER : pos_bad ? TL_POSITION : key_bad ? TL_KEY
                                                                           : tok_bad ? TL_TOKENS : 0;
   if (lane == 0 && code) atomicOr(&a.status[b], code);
@@ -554,7 +577,7 @@ __device__ __forceinline__ void load_chunk_item(const SegArgs& a, uint32_t w, ui
   const uint64_t digest = wave_sum64(leaf);
   if (lane == 0) {
     const uint64_t want = *(const uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t);
-    if (want != digest) atomicOr(&a.status[it.b], kSegFailBit);
+    if (want != digest && !(a.disabled & TL_CHECK_SEGMENT)) atomicOr(&a.status[it.b], kSegFailBit);
   }
 }
 
@@ -623,6 +646,7 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.ppb * ctx->geo.cps;
   a.total = (uint32_t)(n * a.n_sub);
   a.slab_major = 0;
+  a.disabled = g_disabled_checks;
   a.status = status;
 }
 
@@ -639,6 +663,7 @@ void fill_meta(MetaArgs& m, const tl_ctx* ctx, size_t n, const uint64_t* rec, co
   m.n = (uint32_t)n;
   m.status = status;
   m.out_status = out_status;
+  m.disabled = g_disabled_checks;
   __builtin_memcpy(m.tmpl, ctx->header_template, sizeof m.tmpl);
 }
 
@@ -784,3 +809,11 @@ extern "C" int tl_timing_read(int kernel, double* total_ms, uint64_t* count) {
   *count = ev.size();
   return st;
 }
+
+#ifdef TL_SABOTAGE
+extern "C" uint32_t tl_debug_disable_checks(uint32_t mask) {
+  const uint32_t prev = g_disabled_checks;
+  g_disabled_checks = mask;
+  return prev;
+}
+#endif

@@ -1,0 +1,134 @@
+// Host self-test of libtaliesin's C++ runtime (context, key chain, index,
+// argument validation), built with AddressSanitizer and UBSan on the CPU.
+// The kernel launchers are stubbed: no GPU is used.
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "internal.h"
+
+namespace tl {
+int launch_save(const tl_ctx*, void*, size_t, const tl_cache*, const tl_blocks*, const uint64_t*,
+                uint8_t*) { return TL_EDEVICE; }
+int launch_save_layers(const tl_ctx*, void*, size_t, const tl_cache*, const tl_blocks*, const uint64_t*,
+                       uint32_t, uint32_t) { return TL_EDEVICE; }
+int launch_save_seal(const tl_ctx*, void*, size_t, int64_t, const tl_blocks*, const uint64_t*,
+                     uint8_t*) { return TL_EDEVICE; }
+int launch_load(const tl_ctx*, void*, size_t, const uint64_t*, const uint64_t*, const tl_blocks*,
+                const tl_cache*, uint8_t*, uint32_t*) { return TL_EDEVICE; }
+}  // namespace tl
+
+static int failures = 0;
+#define EXPECT(c) do { if (!(c)) { fprintf(stderr, "FAIL %s:%d: %s\n", __FILE__, __LINE__, #c); ++failures; } } while (0)
+
+static uint64_t rng_state = 0x9E3779B97F4A7C15ull;
+static uint32_t rnd() {
+  rng_state ^= rng_state << 13; rng_state ^= rng_state >> 7; rng_state ^= rng_state << 17;
+  return (uint32_t)rng_state;
+}
+
+int main() {
+  // SHA-256: FIPS 180-2 Appendix B.1, both compression functions, and agreement on random lengths
+  uint8_t d0[32], d1[32];
+  EXPECT(tl_test_sha256("abc", 3, 0, d0) == TL_OK);
+  const uint8_t abc[32] = {0xba, 0x78, 0x16, 0xbf, 0x8f, 0x01, 0xcf, 0xea, 0x41, 0x41, 0x40, 0xde, 0x5d, 0xae, 0x22, 0x23,
+                           0xb0, 0x03, 0x61, 0xa3, 0x96, 0x17, 0x7a, 0x9c, 0xb4, 0x10, 0xff, 0x61, 0xf2, 0x00, 0x15, 0xad};
+  EXPECT(!memcmp(d0, abc, 32));
+  const bool shani = tl_test_sha256("", 0, 1, d1) == TL_OK;
+  std::vector<uint8_t> buf(5000);
+  for (auto& x : buf) x = (uint8_t)rnd();
+  for (size_t n = 0; n < 300 && shani; ++n) {
+    tl_test_sha256(buf.data(), n, 0, d0);
+    tl_test_sha256(buf.data(), n, 1, d1);
+    EXPECT(!memcmp(d0, d1, 32));
+  }
+
+  // identity gate and layout validation, including hostile sizes
+  tl_layout lay = {4, 4, 64, TL_DTYPE_BF16, 16, 1, nullptr, nullptr};
+  int st = 0;
+  EXPECT(!tl_ctx_create("", 0, "m", 1, &lay, &st) && st == TL_ENOIDENT);
+  EXPECT(!tl_ctx_create("t", 1, nullptr, 0, &lay, &st) && st == TL_ENOIDENT);
+  EXPECT(!tl_ctx_create("t", 1, "m", 1, nullptr, &st) && st == TL_EINVAL);
+  const tl_layout bad[] = {{0, 4, 64, 1, 16, 1, nullptr, nullptr},       {257, 4, 64, 1, 16, 1, nullptr, nullptr},
+                           {4, 4, 4, 1, 16, 1, nullptr, nullptr},        {4, 4, 64, 9, 16, 1, nullptr, nullptr},
+                           {4, 0xffffffffu, 0xffffffffu, 1, 0xffffffffu, 1, nullptr, nullptr},
+                           {4, 4, 64, 1, 16, 70000, nullptr, nullptr}};
+  for (const tl_layout& b : bad) EXPECT(!tl_ctx_create("t", 1, "m", 1, &b, &st) && st == TL_ELAYOUT);
+  const uint8_t groups[4] = {0, 1, 0, 9};
+  tl_layout g9 = lay;
+  g9.layer_group = groups;
+  EXPECT(!tl_ctx_create("t", 1, "m", 1, &g9, &st) && st == TL_ELAYOUT);
+
+  // many valid contexts, destroyed again
+  for (int i = 0; i < 200; ++i) {
+    const int32_t win[6] = {0, 1024, 0, 0, 16, 0};
+    const uint8_t grp[6] = {0, 1, 0, 0, 1, 0};
+    tl_layout l = {6, 1 + rnd() % 8, 32 * (1 + rnd() % 4), TL_DTYPE_BF16, 16, 1 + rnd() % 4, win, grp};
+    tl_ctx* c = tl_ctx_create("tenant", 6, "model", 5, &l, &st);
+    EXPECT(c && st == TL_OK);
+    tl_geometry geo;
+    EXPECT(tl_ctx_geometry(c, &geo) == TL_OK && geo.n_groups == 2 && geo.pages_per_block == l.pages_per_block);
+    EXPECT(geo.record_bytes == geo.payload_offset + (uint64_t)geo.n_slabs * geo.slab_bytes);
+    tl_ctx_destroy(c);
+  }
+  tl_ctx_destroy(nullptr);
+
+  tl_ctx* c = tl_ctx_create("tenant", 6, "model", 5, &lay, &st);
+  EXPECT(c);
+  // key chain: single document, capacity error, tail, explicit parent, threads
+  std::vector<uint32_t> toks(16 * 40 + 7);
+  for (auto& t : toks) t = rnd() % 32000;
+  std::vector<uint8_t> keys(32 * 40), keys2(32 * 40);
+  size_t nk = 0;
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, keys.data(), 40, &nk) == TL_OK && nk == 40);
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, keys2.data(), 39, &nk) == TL_ERANGE);
+  EXPECT(tl_block_keys(c, nullptr, nullptr, 0, 0, nullptr, 0, &nk) == TL_OK && nk == 0);
+  EXPECT(tl_block_keys(c, nullptr, nullptr, 8, 0, nullptr, 0, &nk) == TL_EINVAL);
+  std::vector<uint64_t> off = {0, 64 * 10, 64 * 25}, len = {64 * 10, 64 * 15 + 3, 64 * 15 + 28}, koff = {0, 10, 25}, nko(3);
+  EXPECT(tl_block_keys_batch(c, nullptr, toks.data(), off.data(), len.data(), 3, 0, keys2.data(), koff.data(), nko.data(), 3) == TL_OK);
+  EXPECT(nko[0] == 10 && nko[1] == 15 && nko[2] == 15);
+  EXPECT(!memcmp(keys.data(), keys2.data(), 32 * 10));  // the first document is the prefix of the first chain
+  // index: fill to capacity, overwrite, miss, full
+  tl_index* idx = tl_index_create(500);
+  std::vector<uint8_t> ik(32 * 600);
+  for (auto& x : ik) x = (uint8_t)rnd();
+  for (int i = 0; i < 500; ++i) EXPECT(tl_index_put(idx, &ik[32 * i], i) == TL_OK);
+  EXPECT(tl_index_put(idx, &ik[32 * 500], 1) == TL_EFULL);
+  EXPECT(tl_index_put(idx, &ik[0], 77) == TL_OK && tl_index_size(idx) == 500);
+  std::vector<uint64_t> h(600);
+  EXPECT(tl_index_get_batch(idx, ik.data(), 600, h.data()) == TL_OK);
+  EXPECT(h[0] == 77 && h[499] == 499 && h[550] == UINT64_MAX);
+  tl_index_destroy(idx);
+  EXPECT(!tl_index_create(0));
+
+  // argument validation in front of the launches (the stubbed launch returns TL_EDEVICE)
+  uint64_t lk[4] = {0}, lv[4] = {0};
+  tl_cache cache = {lk, lv, 8192, 128};
+  uint8_t kb[32];
+  uint64_t bi;
+  uint32_t tk[16];
+  int32_t tb[1];
+  tl_blocks blk = {kb, &bi, tk, tb};
+  uint64_t rp[1], rl[1];
+  uint8_t verd[1];
+  uint32_t ws[64];
+  EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &cache, verd, ws, sizeof ws) == TL_EDEVICE);
+  EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &cache, verd, ws, 3) == TL_ERANGE);
+  EXPECT(tl_save(c, nullptr, 1, &cache, &blk, rp, nullptr) == TL_EDEVICE);
+  tl_blocks no_tok = blk;
+  no_tok.d_tokens = nullptr;
+  EXPECT(tl_save(c, nullptr, 1, &cache, &no_tok, rp, nullptr) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 1, 1) == TL_EINVAL);
+  EXPECT(tl_save_seal(c, nullptr, 1, -5, &blk, rp, nullptr) == TL_EINVAL);
+  tl_cache narrow = cache;
+  narrow.page_stride = 4096;
+  EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &narrow, verd, ws, sizeof ws) == TL_EINVAL);
+  for (int s = 1; s >= -8; --s) EXPECT(tl_status_string(s) != nullptr);
+  for (int v = 0; v < 0x20; ++v) EXPECT(tl_verdict_string(v) != nullptr);
+  tl_ctx_destroy(c);
+  if (failures) return 1;
+  printf("host self-test ok (%s)\n", shani ? "with SHA extensions" : "portable SHA-256 only");
+  return 0;
+}

@@ -19,8 +19,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TEN, FP = b"tenant-a", b"model-fp-0001"
 
 
-def declared_functions():
-    src = open(os.path.join(ROOT, "include", "taliesin.h")).read()
+def declared_functions(header="taliesin.h"):
+    src = open(os.path.join(ROOT, "include", header)).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     return sorted(set(re.findall(r"\b(tl_[a-z0-9_]+)\s*\(", src)))
 
@@ -33,6 +33,17 @@ def test_every_declared_symbol_is_exported():
         assert hasattr(lib, n), n
     assert set(names) == set(T.EXPORTED)
     assert T.lib().tl_abi_version() == 1
+
+
+def test_sabotage_build_exports_both_headers_and_release_does_not():
+    from paper_2609_39358_amd import build as B
+
+    debug = declared_functions("taliesin_debug.h")
+    assert debug == ["tl_debug_disable_checks"]
+    sab = ctypes.CDLL(B.SABOTAGE_OUT)
+    for n in declared_functions() + debug:
+        assert hasattr(sab, n), n
+    assert not hasattr(ctypes.CDLL(T.LIB_PATH), "tl_debug_disable_checks")
 
 
 @pytest.mark.parametrize("impl", [0, 1])
