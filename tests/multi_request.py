@@ -1,7 +1,7 @@
-"""The multi-request restore pipeline on the GPU: base documents are saved
-once; every request computes its chained keys, looks them up in the index and
-restores the hits into a shared page pool, batch by batch; damaged records
-must be rejected. Used by the multi-request GPU tests."""
+"""The multi-request workload on the GPU: base documents are saved once; the
+package's restore pipeline then computes every request's chained keys, looks
+them up in the index and restores the hits into a shared page pool, batch by
+batch; damaged records must be rejected. Used by the multi-request GPU tests."""
 from __future__ import annotations
 
 from dataclasses import dataclass, field
@@ -12,8 +12,9 @@ import torch
 
 import workloads as wl
 from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import pipeline
 from paper_2609_39358_amd import taliesin as T
-from paper_2609_39358_amd.device import PagedCache, RecordStore
+from paper_2609_39358_amd.device import PagedCache
 from tests.gpu_case import DEV, FP, TEN, ctx_of, fill_cache, i32, i64, layout_of, log
 
 
@@ -44,7 +45,8 @@ class MultiRun:
         self.keys = np.concatenate(base_keys)
         self.bidx = np.tile(np.arange(self.bpd, dtype=np.uint64), len(w.base_docs))
         self.tokens = np.concatenate([d[:self.bpd * P].reshape(self.bpd, P) for d in w.base_docs])
-        self.store = RecordStore(self.n_stored, self.rb, DEV)
+        self.st = pipeline.Store(self.ctx, self.n_stored, DEV)
+        self.store = self.st.records
         st = torch.zeros(self.n_stored, dtype=torch.uint8, device=DEV)
         self._save_in = (torch.from_numpy(self.keys).to(DEV), i64(self.bidx),
                          i32(self.tokens.view(np.int32)), i32(self.src_table[None, :]))
@@ -53,7 +55,7 @@ class MultiRun:
         torch.cuda.synchronize()
         assert (st == ref.ACCEPT).all().item()
         # damage: bit flips in place, truncations as shorter reported lengths
-        self.lens = np.full(self.n_stored, self.rb, np.uint64)
+        self.lens = self.st.lens
         self.flip_bits: Dict[int, int] = {}
         for rid, frac in w.corrupt_flip:
             bit = wl.scale_bit(frac, self.rb)
@@ -61,54 +63,26 @@ class MultiRun:
             self.store.buf[rid, bit >> 3] ^= 1 << (bit & 7)
         for rid, frac in w.corrupt_trunc:
             self.lens[rid] = wl.scale_len(frac, self.rb)
-        self.index = T.tl_index_create(self.n_stored)
-        self.index.put_many(self.keys, range(self.n_stored))
+        self.st.add(self.keys, range(self.n_stored))
+        self.index = self.st.index
         self.dst = PagedCache(g.n_layers, pool_pages, self.lay.slab_bytes, DEV)
+        self.pipe = pipeline.RestorePipeline(self.st, self.dst)
 
     def run(self, check=None):
         """Restore every request's hits, admission batch by admission batch.
         `check(batch)` is called after each batch (pages still in the pool)."""
-        w, P = self.w, self.g.page_tokens
-        req_keys = T.tl_block_keys_batch(self.ctx, [q.tokens for q in w.requests])
-        batches = wl.admission_batches(w.requests, self.pool_pages)
-        base = self.store.buf.data_ptr()
-        ws = torch.empty(max(T.tl_workspace_bytes(self.ctx, self.pool_pages), 4), dtype=torch.uint8,
-                         device=DEV)
+        w = self.w
         out = []
-        for bi, reqs in enumerate(batches):
-            b = Batch(reqs)
-            keys, bidx, toks, rids = [], [], [], []
-            for r in reqs:
-                q = w.requests[r]
-                h = self.index.get_batch(req_keys[r])
-                hit = h != np.uint64(2**64 - 1)
-                n_hit = int(np.argmin(hit)) if not hit.all() else len(hit)
-                assert hit[:n_hit].all() and not hit[n_hit:].any()  # hits are exactly a prefix
-                assert n_hit == q.shared_blocks, (r, n_hit, q.shared_blocks)
-                for i in range(n_hit):
-                    b.blocks.append((r, i, int(h[i]), len(b.blocks)))
-                keys.append(req_keys[r][:n_hit])
-                bidx.append(np.arange(n_hit, dtype=np.uint64))
-                toks.append(q.tokens[:n_hit * P].reshape(n_hit, P))
-                rids.append(h[:n_hit].astype(np.int64))
-            n = len(b.blocks)
-            if n == 0:
-                b.verdicts = np.zeros(0, np.uint8)
-                out.append(b)
-                continue
-            rid = np.concatenate(rids)
-            ptrs = i64(np.uint64(base) + rid.astype(np.uint64) * np.uint64(self.rb))
-            lens = i64(self.lens[rid])
-            table = np.arange(n, dtype=np.int32)[None, :]
-            d_keys = torch.from_numpy(np.ascontiguousarray(np.concatenate(keys))).to(DEV)
-            d_bidx, d_tok = i64(np.concatenate(bidx)), i32(np.concatenate(toks).view(np.int32))
-            d_tab = i32(table)
-            verd = torch.zeros(n, dtype=torch.uint8, device=DEV)
-            log("batch %d: %d requests, %d blocks" % (bi, len(reqs), n))
-            T.tl_load(self.ctx, torch.cuda.current_stream(), n, ptrs, lens,
-                      T.make_blocks(d_keys, d_bidx, d_tok, d_tab), self.dst.tl(), verd, ws, ws.numel())
+        for bi, reqs in enumerate(wl.admission_batches(w.requests, self.pool_pages)):
+            res = self.pipe.restore([w.requests[r].tokens for r in reqs], reqs)
+            for r, h in zip(reqs, res.hits):
+                assert h == w.requests[r].shared_blocks, (r, h, w.requests[r].shared_blocks)
             torch.cuda.synchronize()
-            b.verdicts = verd.cpu().numpy()
+            b = Batch(reqs)
+            b.blocks = [(int(r), int(p), int(rid), page) for page, (r, p, rid) in
+                        enumerate(zip(res.request_of, res.positions, res.record_ids))]
+            b.verdicts = res.verdicts.cpu().numpy()
+            log("batch %d: %d requests, %d blocks" % (bi, len(reqs), len(b.blocks)))
             if check:
                 check(b)
             out.append(b)
