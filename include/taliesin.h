@@ -233,7 +233,10 @@ int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pag
  * block would have written is zero-filled; pages of -1 entries are untouched.
  * Distinct blocks must not name the same destination page.
  * d_workspace: device, >= tl_workspace_bytes(ctx, n_blocks), 4-byte aligned;
- * its contents need no initialisation. Sec. 2.2, Sec. 3, Sec. 5. */
+ * its contents need no initialisation. The call issues three kernels and no
+ * memset or allocation, so it can be captured into a HIP graph and replayed
+ * (the arrays are read at run time: their contents may change between
+ * replays). Sec. 2.2, Sec. 3, Sec. 5. */
 int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_record_ptrs,
             const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
             uint8_t* d_verdicts, void* d_workspace, size_t workspace_bytes);
