@@ -1,7 +1,8 @@
 // HIP kernels (gfx950) of libtaliesin: save and verified restore of paged KV.
 //
-// Work decomposition. A record holds one block: metadata, then 2L slabs
-// (slab s = 2*layer + kv is one page of one layer's K or V cache). Each slab
+// Work decomposition. A record holds one block: metadata, then 2*L*ppb slabs
+// (slab s = (2*layer + kv)*ppb + j is page j of the block in one layer's K or
+// V cache; ppb = pages per block). Each slab
 // is digested in chunks of at most 64 KiB; a chunk is R rows of 1024 bytes and
 // its digest is sum_j XXH64(column_j, seed = j) mod 2^64, where column j is the
 // 16-byte granule at offset 16*j of every row. One wavefront owns one
@@ -181,6 +182,12 @@ __device__ __forceinline__ uint64_t swz_xor(uint64_t v) {
   return (uint64_t)hi << 32 | lo;
 }
 
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+  const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+  return (uint64_t)hi << 32 | lo;
+}
+
 // Sum of v over the 64 lanes (mod 2^64), returned uniformly.
 __device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
   v += swz_xor<1>(v);
@@ -188,11 +195,7 @@ __device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
   v += swz_xor<4>(v);
   v += swz_xor<8>(v);
   v += swz_xor<16>(v);
-  const uint32_t lo0 = __builtin_amdgcn_readlane((int)(uint32_t)v, 0);
-  const uint32_t hi0 = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 0);
-  const uint32_t lo1 = __builtin_amdgcn_readlane((int)(uint32_t)v, 32);
-  const uint32_t hi1 = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 32);
-  return ((uint64_t)hi0 << 32 | lo0) + ((uint64_t)hi1 << 32 | lo1);
+  return readlane64(v, 0) + readlane64(v, 32);  // the two 32-lane halves
 }
 
 __device__ __forceinline__ uint32_t uniform(uint32_t x) { return __builtin_amdgcn_readfirstlane(x); }
@@ -222,7 +225,7 @@ struct MetaArgs {
   const uint64_t* len;       // load only
   const uint8_t* keys;       // [n][32]
   const uint64_t* bidx;      // [n]
-  const uint32_t* tokens;    // [n][P] or null (load)
+  const uint32_t* tokens;    // [n][block tokens] or null (load)
   const int32_t* tables;
   int64_t n_pages;
   uint32_t n;
@@ -312,10 +315,11 @@ __device__ __forceinline__ uint64_t copy_hash(const char* src, char* dst, uint32
     v4u x[B], y[B];
     load_batch<B>(x, s, 0);
     for (r = 0; r < full; r += 2 * B) {
+      // x holds rows [r, r+B); rows [r+B, r+2B) arrive in y meanwhile
       const bool has_y = r + B < full;
       if (has_y) load_batch<B>(y, s, r + B);
       store_hash_batch<B>(x, d, r, c);
-      if (!has_y) { r += B; break; }
+      if (!has_y) break;
       if (r + 2 * B < full) load_batch<B>(x, s, r + 2 * B);
       store_hash_batch<B>(y, d, r + B, c);
     }
@@ -383,8 +387,8 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
   }
 }
 
-// Assembles (save) or loads (load) one metadata tile into LDS, 4 bytes per
-// lane-step. Lanes 0..3 then run the four XXH64 accumulators over the tile.
+// Root checksum over one metadata tile already staged in LDS: lane k (k < 4)
+// runs XXH64 accumulator k over the k-th 8 bytes of every 32-byte stripe.
 __device__ __forceinline__ void hash_tile(const uint64_t* tile64, uint32_t n_bytes, uint32_t off,
                                           uint32_t lane, uint64_t& acc) {
   if (lane < 4) {
@@ -398,14 +402,8 @@ __device__ __forceinline__ void hash_tile(const uint64_t* tile64, uint32_t n_byt
 }
 
 __device__ __forceinline__ uint64_t finish_root(uint64_t acc, uint64_t len) {
-  const uint64_t v1 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 0) << 32) |
-                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 0);
-  const uint64_t v2 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 1) << 32) |
-                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 1);
-  const uint64_t v3 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 2) << 32) |
-                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 2);
-  const uint64_t v4 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(acc >> 32), 3) << 32) |
-                      (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)acc, 3);
+  const uint64_t v1 = readlane64(acc, 0), v2 = readlane64(acc, 1), v3 = readlane64(acc, 2),
+                 v4 = readlane64(acc, 3);
   uint64_t h = rotl64(v1, 1) + rotl64(v2, 7) + rotl64(v3, 12) + rotl64(v4, 18);
   h = xx_merge(h, v1);
   h = xx_merge(h, v2);
