@@ -252,6 +252,110 @@ int tl_index_put(tl_index* idx, const uint8_t key[TL_KEY_BYTES], uint64_t handle
 int tl_index_get_batch(const tl_index* idx, const uint8_t* keys, size_t n, uint64_t* handles_out);
 size_t tl_index_size(const tl_index* idx);
 
+/* ---- a1 + a2 on the device: key chains and a device index ----------------
+ * For engines whose token ids are already in HBM. The same chained keys as
+ * tl_block_keys (u32 token ids, B = 4 * tokens per block) are computed one
+ * chain per lane and looked up, as they are made, in an index held in device
+ * memory; tl_chain_stage turns the result into tl_load's inputs. A restore
+ * (tl_chain_lookup -> tl_chain_stage -> tl_load) then needs no host round
+ * trip and can be enqueued on one stream or captured into a graph.
+ * Sec. 2.2 (a later request that contains the same block loads its state
+ * instead of recomputing it), Sec. 5 (reuse of whole blocks at exact
+ * positions: a request's reuse ends at its first block with no stored state,
+ * since every later key covers that block). */
+
+/* Device index: open addressing with linear probing over `capacity` slots of
+ * 64 bytes (32-byte key, 64-bit handle) in caller-owned device memory of
+ * tl_dindex_bytes(capacity) bytes (256-byte aligned). The host handle holds
+ * no device memory of its own. Calls that use one index must be ordered
+ * (e.g. on one stream): a lookup that overlaps a put may miss keys the put
+ * is inserting. A key is placed within 1024 slots of its home slot. */
+typedef struct tl_dindex tl_dindex;
+
+/* per-key put status */
+#define TL_INDEX_STORED 0x01    /* the key is in the index; within one call the
+                                   highest-indexed duplicate's handle wins */
+#define TL_INDEX_FULL 0x20      /* no free slot within reach: not inserted */
+#define TL_INDEX_TAG_CLASH 0x21 /* a different key with the same first eight
+                                   bytes (bit 0 aside) holds the slot: not
+                                   inserted (about 2^-63 per pair of keys) */
+
+/* 256 + 64 * capacity, or 0 unless capacity is a power of two in [2, 2^31]. */
+size_t tl_dindex_bytes(size_t capacity);
+/* Wraps d_mem (device, 256-byte aligned, >= tl_dindex_bytes(capacity)) and
+ * enqueues a kernel on `stream` that empties it (no memset). NULL with
+ * *status = TL_EINVAL (bad capacity, NULL or misaligned memory), TL_ERANGE
+ * (mem_bytes too small), TL_EDEVICE, TL_ENOMEM. */
+tl_dindex* tl_dindex_create(void* d_mem, size_t mem_bytes, size_t capacity, void* stream,
+                            int* status);
+void tl_dindex_destroy(tl_dindex* idx); /* leaves d_mem to the caller; NULL is a no-op */
+/* Device workspace tl_dindex_put needs for n keys (4 bytes per key, rounded
+ * up to 256). */
+size_t tl_dindex_workspace_bytes(size_t n);
+/* Insert or overwrite n keys (device [n][32]) with handles (device [n]).
+ * d_status (device [n] or NULL) receives TL_INDEX_*. Three kernels, no
+ * memset; d_workspace needs no initialisation. */
+int tl_dindex_put(tl_dindex* idx, void* stream, size_t n, const uint8_t* d_keys,
+                  const uint64_t* d_handles, uint8_t* d_status, void* d_workspace,
+                  size_t workspace_bytes);
+/* d_handles_out[i] = handle of d_keys[i], or UINT64_MAX when absent. */
+int tl_dindex_get(const tl_dindex* idx, void* stream, size_t n, const uint8_t* d_keys,
+                  uint64_t* d_handles_out);
+/* d_out (device [2]) = occupied slots, longest probe distance of any key. */
+int tl_dindex_stats(const tl_dindex* idx, void* stream, uint64_t* d_out);
+
+/* Chains: chain c is token ids [tok_off[c], tok_off[c+1]) of d_tokens and
+ * owns output slots [slot_off[c], slot_off[c+1]); its block k (0-based) is
+ * slot slot_off[c] + k. Offsets are clamped to n_tokens / n_slots, so an
+ * inconsistent offset array yields fewer blocks, never an access outside the
+ * arrays: chain c has n_c = min(floor(tokens / tokens per block), slots)
+ * blocks. To pass the per-slot arrays to tl_load whole, the slot ranges
+ * should tile [0, n_slots). */
+typedef struct tl_chains {
+  const uint32_t* d_tokens;      /* token ids of every chain, back to back */
+  uint64_t n_tokens;             /* elements of d_tokens */
+  const uint64_t* d_tok_off;     /* [n_chains + 1] */
+  const uint64_t* d_slot_off;    /* [n_chains + 1] */
+  uint64_t n_slots;              /* elements (rows) of every per-slot array */
+  const uint8_t* d_parents;      /* [n_chains][32] key before each chain's
+                                    first block, or NULL: the namespace digest */
+  const uint64_t* d_first_block; /* [n_chains] position of each chain's first
+                                    block, or NULL: 0 (used by tl_chain_stage) */
+} tl_chains;
+
+#define TL_CHAIN_ALL_KEYS 1 /* flag: keep computing keys past the first miss */
+
+/* Keys and lookup, one lane per chain (fewer than 2^24 chains). Without an
+ * index: every block's key is written (slots [0, n_c) of each chain) and
+ * d_hits[c] = n_c. With an index: the chain stops at its first key that is
+ * not in the index; d_hits[c] = the number of leading blocks found, d_keys
+ * holds slots [0, min(hits + 1, n_c)) (the first missing key included, so the
+ * block can be saved under it after prefill) or [0, n_c) with
+ * TL_CHAIN_ALL_KEYS, and d_handles (device [n_slots], required with an
+ * index) gets the found handles for slots [0, hits) and UINT64_MAX for
+ * [hits, n_c). Other slots are not written. */
+int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                    const tl_dindex* idx, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,
+                    uint32_t* d_hits);
+
+/* tl_load's per-block inputs from a lookup, for every slot of every chain's
+ * range (n_slots blocks): slot k of chain c is a hit when k < d_hits[c] and
+ * its handle is below n_handles; then d_record_ptrs / d_record_lens get
+ * d_handle_ptrs[h] / d_handle_lens[h], else 0 / 0 (tl_load: TL_MISSING).
+ * d_block_index = first_block[c] + k; d_tokens_out (device
+ * [n_slots][tokens per block] or NULL) = the block's token ids (zeros past
+ * n_c); d_tables_out (device [n_groups][n_slots * pages_per_block] or NULL)
+ * = the page ids of d_tables_in (same shape; NULL: page j of slot q is
+ * q * pages_per_block + j in every group) for hits and -1 for every other
+ * slot, so that tl_load neither reads nor writes pages for it. The two may
+ * be the same array. d_keys from tl_chain_lookup serve as tl_blocks.d_keys
+ * unchanged. */
+int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                   const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_handle_ptrs,
+                   const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,
+                   uint64_t* d_record_lens, uint64_t* d_block_index, uint32_t* d_tokens_out,
+                   const int32_t* d_tables_in, int32_t* d_tables_out);
+
 /* ---- profiling ------------------------------------------------------------
  * Opt-in kernel timing for benchmarks: while enabled (process-wide), every
  * kernel launch is bracketed by two HIP events recorded on the launch stream.
@@ -264,7 +368,10 @@ size_t tl_index_size(const tl_index* idx);
 #define TL_KERNEL_LOAD_INIT 2
 #define TL_KERNEL_LOAD_MAIN 3
 #define TL_KERNEL_LOAD_FINAL 4
-#define TL_KERNEL_COUNT 5
+#define TL_KERNEL_CHAIN 5 /* tl_chain_lookup */
+#define TL_KERNEL_STAGE 6 /* tl_chain_stage */
+#define TL_KERNEL_INDEX 7 /* every tl_dindex_* kernel */
+#define TL_KERNEL_COUNT 8
 int tl_timing(int enable);
 int tl_timing_read(int kernel, double* total_ms, uint64_t* count);
 

@@ -217,6 +217,27 @@ def block_keys(parent: bytes, data: bytes, block_bytes: int) -> List[bytes]:
     return keys
 
 
+def index_put(index: dict, keys: Sequence[bytes], handles: Sequence[int]) -> dict:
+    """Key -> handle map (a store's lookup, Sec. 2.2): insert or overwrite, in
+    the order given, so that of equal keys in one batch the last one wins."""
+    for k, h in zip(keys, handles):
+        index[bytes(k)] = int(h)
+    return index
+
+
+def chain_walk(parent: bytes, data: bytes, block_bytes: int, index: dict) -> Tuple[List[bytes], int, List[int]]:
+    """Reuse of one request against a store (Sec. 2.2: a later request that
+    contains a stored block loads it; Sec. 5: only whole blocks at matching
+    positions, so once a block has no stored state, no later block of the
+    request can be reused either). Returns the request's block keys, the
+    number of leading blocks whose key is in `index`, and their handles."""
+    keys = block_keys(parent, data, block_bytes)
+    hits = 0
+    while hits < len(keys) and keys[hits] in index:
+        hits += 1
+    return keys, hits, [index[k] for k in keys[:hits]]
+
+
 # ------------------------------------------------------------------ checksums
 def xxh64(data: bytes, seed: int) -> int:
     return xxhash.xxh64_intdigest(bytes(data), seed=seed)

@@ -44,10 +44,10 @@ def build(verbose: bool = False, extra_hip_flags=(), out: str = OUT, build_dir: 
         o = os.path.join(build_dir, src + ".o")
         _run([cxx, *CXX_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)
-    o = os.path.join(build_dir, "kernels.hip.o")
-    _run([hipcc, *HIP_FLAGS, *extra_hip_flags, *inc, "-c", os.path.join(CSRC, "kernels.hip"), "-o", o],
-         verbose)
-    objs.append(o)
+    for src in ("kernels.hip", "chain.hip"):
+        o = os.path.join(build_dir, src + ".o")
+        _run([hipcc, *HIP_FLAGS, *extra_hip_flags, *inc, "-c", os.path.join(CSRC, src), "-o", o], verbose)
+        objs.append(o)
     tmp = out + ".tmp"
     _run([hipcc, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs], verbose)
     os.replace(tmp, out)

@@ -1,0 +1,604 @@
+// Device-side key chains and a device index (gfx950).
+//
+// The key of block k of a chain is SHA-256(key of block k-1 | the block's
+// token ids as u32 little-endian), rooted at the namespace digest or at a
+// caller-supplied parent key (Sec. 2.2: state is stored under a fingerprint
+// of the exact input bytes, the model and the tenant; Sec. 5: reuse is of
+// whole blocks at exact positions). A chain is inherently sequential, so one
+// lane walks one chain; the chip's parallelism is across chains. While there
+// are no more chains than SIMDs each chain gets a wavefront of its own (waves
+// on one SIMD share its vector ALU, and a chain's time is its own instruction
+// latency); beyond that, chains share wavefronts, up to 64.
+//
+// The walk probes the device index while it computes: the home slot of key k
+// (64 bytes, one cache line) is requested before key k+1 is computed and
+// inspected after, so the lookup latency hides behind the hash. Key k+1 is
+// kept only once key k is known to be a hit.
+//
+// Device index: linear probing over 64-byte slots
+//   word 0  tag = first 8 key bytes | 1 (0 = empty)
+//   word 1  writer (0 outside a put; the winning duplicate's index + 1 inside)
+//   word 2  handle
+//   word 3  0
+//   words 4..7  the key
+// after a 256-byte header (word 0 occupied slots, word 1 longest probe). A
+// put is three kernels, so that no lane ever waits on another: claim (find
+// the key's slot by tag, or take a free one with a compare-and-swap and
+// write the key), vote (each lane checks the full key in its slot, now
+// complete, and takes the maximum of its index into the writer word), and
+// publish (the winner writes the handle and clears the writer word).
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace {
+
+constexpr uint32_t kMaxProbe = 1024;  // slots a key may sit past its home slot
+constexpr uint32_t kNoSlot = 0xffffffffu;
+constexpr uint64_t kMiss = ~0ull;
+constexpr uint32_t kHeaderWords = 32;  // 256-byte header
+constexpr uint32_t kSlotWords = 8;
+
+// ---- SHA-256 compression (FIPS 180-4, 6.2.2) --------------------------------
+__device__ __forceinline__ uint32_t rotr(uint32_t x, uint32_t n) {
+  return __builtin_amdgcn_alignbit(x, x, n);
+}
+__device__ __forceinline__ uint32_t bsig0(uint32_t a) { return rotr(a, 2) ^ rotr(a, 13) ^ rotr(a, 22); }
+__device__ __forceinline__ uint32_t bsig1(uint32_t e) { return rotr(e, 6) ^ rotr(e, 11) ^ rotr(e, 25); }
+__device__ __forceinline__ uint32_t ssig0(uint32_t x) { return rotr(x, 7) ^ rotr(x, 18) ^ (x >> 3); }
+__device__ __forceinline__ uint32_t ssig1(uint32_t x) { return rotr(x, 17) ^ rotr(x, 19) ^ (x >> 10); }
+__device__ __forceinline__ uint32_t ch(uint32_t e, uint32_t f, uint32_t g) { return g ^ (e & (f ^ g)); }
+__device__ __forceinline__ uint32_t maj(uint32_t a, uint32_t b, uint32_t c) {
+  return (a & b) | (c & (a | b));
+}
+
+// Rounds R..63 with the working variables passed by value, so that the
+// unrolled rounds rename registers instead of moving them; K[R] is a
+// constant expression, hence an immediate.
+template <int R>
+__device__ __forceinline__ void rounds(uint32_t (&out)[8], uint32_t a, uint32_t b, uint32_t c,
+                                       uint32_t d, uint32_t e, uint32_t f, uint32_t g, uint32_t h,
+                                       uint32_t (&w)[16]) {
+  if constexpr (R == 64) {
+    out[0] = a; out[1] = b; out[2] = c; out[3] = d;
+    out[4] = e; out[5] = f; out[6] = g; out[7] = h;
+  } else {
+    constexpr uint32_t k = tl::kSha256K[R];
+    if constexpr (R >= 16)
+      w[R & 15] += ssig1(w[(R + 14) & 15]) + w[(R + 9) & 15] + ssig0(w[(R + 1) & 15]);
+    const uint32_t t1 = h + bsig1(e) + ch(e, f, g) + k + w[R & 15];
+    const uint32_t t2 = bsig0(a) + maj(a, b, c);
+    rounds<R + 1>(out, t1 + t2, a, b, c, d + t1, e, f, g, w);
+  }
+}
+
+__device__ __forceinline__ void compress(uint32_t (&st)[8], uint32_t (&w)[16]) {
+  uint32_t o[8];
+  rounds<0>(o, st[0], st[1], st[2], st[3], st[4], st[5], st[6], st[7], w);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) st[i] += o[i];
+}
+
+// Key of one block: SHA-256 over the previous key (32 bytes, i.e. the eight
+// big-endian words prev[]) followed by bt u32 token ids. The message is
+// 32 + 4*bt bytes, then 0x80, zeros and the 64-bit bit length, in nb
+// 64-byte blocks (nb is the same for every lane).
+__device__ __forceinline__ void block_key(uint32_t (&key)[8], const uint32_t (&prev)[8],
+                                          const uint32_t* tok, uint32_t bt, uint32_t nb,
+                                          uint32_t len_hi, uint32_t len_lo) {
+  uint32_t st[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) st[i] = tl::kSha256IV[i];
+  const uint32_t last = 16 * nb - 1;
+  for (uint32_t c = 0; c < nb; ++c) {
+    uint32_t w[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const uint32_t g = 16 * c + t;  // word index in the message
+      const uint32_t j = g - 8;       // token index (wraps for g < 8)
+      uint32_t v;
+      if (g < 8) v = prev[t & 7];
+      else if (j < bt) v = __builtin_bswap32(tok[j]);
+      else if (j == bt) v = 0x80000000u;
+      else if (g == last) v = len_lo;
+      else if (g == last - 1) v = len_hi;
+      else v = 0;
+      w[t] = v;
+    }
+    compress(st, w);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) key[i] = st[i];
+}
+
+// ---- device index ---------------------------------------------------------
+struct Dx {
+  uint64_t* mem;  // header, then slots
+  uint64_t mask;  // capacity - 1
+};
+
+__device__ __forceinline__ uint64_t* slot_ptr(const Dx& x, uint64_t s) {
+  return x.mem + kHeaderWords + s * kSlotWords;
+}
+
+// Key words as little-endian u64 from a byte array of 32 bytes.
+__device__ __forceinline__ void load_key(uint64_t (&k)[4], const uint8_t* p) {
+  const uint64_t* q = (const uint64_t*)p;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) k[i] = q[i];
+}
+
+// The same words from a chain key held as big-endian SHA-256 state words.
+__device__ __forceinline__ void key_words(uint64_t (&k)[4], const uint32_t (&h)[8]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    k[i] = (uint64_t)__builtin_bswap32(h[2 * i]) | (uint64_t)__builtin_bswap32(h[2 * i + 1]) << 32;
+}
+
+__device__ __forceinline__ uint64_t tag_of(const uint64_t (&k)[4]) { return k[0] | 1; }
+
+__device__ __forceinline__ uint64_t atomic_read(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__global__ __launch_bounds__(256) void k_dindex_clear(uint64_t* mem, uint64_t n_words) {
+  const uint64_t step = (uint64_t)gridDim.x * 256;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < n_words; i += step) mem[i] = 0;
+}
+
+struct PutArgs {
+  Dx x;
+  const uint8_t* keys;
+  const uint64_t* handles;
+  uint8_t* status;
+  uint32_t* target;  // workspace [n]
+  uint32_t n;
+};
+
+__global__ __launch_bounds__(256) void k_dindex_claim(PutArgs a) {
+  const uint32_t step = gridDim.x * 256;
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < a.n; i += step) {
+    uint64_t k[4];
+    load_key(k, a.keys + 32ull * i);
+    const uint64_t tag = tag_of(k);
+    const uint64_t home = k[1] & a.x.mask;
+    const uint32_t reach = a.x.mask < kMaxProbe ? (uint32_t)a.x.mask + 1 : kMaxProbe;
+    uint32_t target = kNoSlot;
+    for (uint32_t d = 0; d < reach; ++d) {
+      const uint64_t s = (home + d) & a.x.mask;
+      uint64_t* slot = slot_ptr(a.x, s);
+      uint64_t t = atomic_read(slot);
+      if (t == 0) {
+        t = atomicCAS((unsigned long long*)slot, 0ull, (unsigned long long)tag);
+        if (t == 0) {  // this lane owns the slot: it alone writes the key
+#pragma unroll
+          for (int q = 0; q < 4; ++q) slot[4 + q] = k[q];
+          atomicAdd((unsigned long long*)&a.x.mem[0], 1ull);
+          atomicMax((unsigned long long*)&a.x.mem[1], (unsigned long long)d);
+          target = (uint32_t)s;
+          break;
+        }
+      }
+      if (t == tag) {  // the key's slot (or a tag clash, found by the vote)
+        target = (uint32_t)s;
+        break;
+      }
+    }
+    a.target[i] = target;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_dindex_vote(PutArgs a) {
+  const uint32_t step = gridDim.x * 256;
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < a.n; i += step) {
+    const uint32_t s = a.target[i];
+    uint8_t st = TL_INDEX_FULL;
+    if (s != kNoSlot) {
+      uint64_t k[4];
+      load_key(k, a.keys + 32ull * i);
+      uint64_t* slot = slot_ptr(a.x, s);
+      const bool same = slot[4] == k[0] && slot[5] == k[1] && slot[6] == k[2] && slot[7] == k[3];
+      if (same) {
+        atomicMax((unsigned long long*)&slot[1], (unsigned long long)i + 1);
+        st = TL_INDEX_STORED;
+      } else {
+        st = TL_INDEX_TAG_CLASH;
+        a.target[i] = kNoSlot;
+      }
+    }
+    if (a.status) a.status[i] = st;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_dindex_publish(PutArgs a) {
+  const uint32_t step = gridDim.x * 256;
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < a.n; i += step) {
+    const uint32_t s = a.target[i];
+    if (s == kNoSlot) continue;
+    uint64_t* slot = slot_ptr(a.x, s);
+    if (atomic_read(&slot[1]) == (uint64_t)i + 1) {
+      slot[2] = a.handles[i];
+      slot[1] = 0;
+    }
+  }
+}
+
+// Handle of key k, or kMiss; probes at most maxp + 1 slots.
+__device__ __forceinline__ uint64_t probe_from(const Dx& x, const uint64_t (&k)[4], uint64_t maxp,
+                                               uint64_t d0) {
+  const uint64_t tag = tag_of(k);
+  const uint64_t home = k[1] & x.mask;
+  for (uint64_t d = d0; d <= maxp; ++d) {
+    const uint64_t* slot = slot_ptr(x, (home + d) & x.mask);
+    const uint64_t t = slot[0];
+    if (t == 0) return kMiss;
+    if (t == tag && slot[4] == k[0] && slot[5] == k[1] && slot[6] == k[2] && slot[7] == k[3])
+      return slot[2];
+  }
+  return kMiss;
+}
+
+struct GetArgs {
+  Dx x;
+  const uint8_t* keys;
+  uint64_t* out;
+  uint32_t n;
+};
+
+__global__ __launch_bounds__(256) void k_dindex_get(GetArgs a) {
+  const uint64_t maxp = a.x.mem[1];
+  const uint32_t step = gridDim.x * 256;
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < a.n; i += step) {
+    uint64_t k[4];
+    load_key(k, a.keys + 32ull * i);
+    a.out[i] = probe_from(a.x, k, maxp, 0);
+  }
+}
+
+__global__ void k_dindex_stats(const uint64_t* mem, uint64_t* out) {
+  if (threadIdx.x < 2) out[threadIdx.x] = mem[threadIdx.x];
+}
+
+// ---- chain walk -------------------------------------------------------------
+struct ChainArgs {
+  const uint32_t* tokens;
+  uint64_t n_tokens;
+  const uint64_t* tok_off;
+  const uint64_t* slot_off;
+  uint64_t n_slots;
+  const uint8_t* parents;
+  uint32_t n_chains;
+  uint32_t bt;    // tokens per block
+  uint32_t nb;    // SHA-256 blocks per key
+  uint32_t len_hi, len_lo;
+  uint32_t lanes; // chains per wavefront
+  uint32_t all_keys;
+  uint32_t ns[8]; // namespace digest as big-endian words
+  Dx x;           // x.mem == nullptr: keys only
+  uint8_t* keys;
+  uint64_t* handles;
+  uint32_t* hits;
+};
+
+struct Range {
+  uint64_t t0, s0, n;  // first token, first slot, blocks
+  uint64_t slots;      // slots in the chain's range
+};
+
+__device__ __forceinline__ Range chain_range(const uint64_t* tok_off, const uint64_t* slot_off,
+                                             uint64_t n_tokens, uint64_t n_slots, uint32_t bt,
+                                             uint32_t c) {
+  Range r;
+  const uint64_t a = tok_off[c], b = tok_off[c + 1];
+  r.t0 = a < n_tokens ? a : n_tokens;
+  const uint64_t t1 = b < r.t0 ? r.t0 : (b < n_tokens ? b : n_tokens);
+  const uint64_t p = slot_off[c], q = slot_off[c + 1];
+  r.s0 = p < n_slots ? p : n_slots;
+  const uint64_t s1 = q < r.s0 ? r.s0 : (q < n_slots ? q : n_slots);
+  r.slots = s1 - r.s0;
+  const uint64_t nk = (t1 - r.t0) / bt;
+  r.n = nk < r.slots ? nk : r.slots;
+  return r;
+}
+
+__device__ __forceinline__ void store_key(uint8_t* keys, uint64_t slot, const uint32_t (&h)[8]) {
+  uint32_t* p = (uint32_t*)(keys + 32 * slot);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) p[i] = __builtin_bswap32(h[i]);
+}
+
+// Resolves a lookup from the home slot's words (already loaded) and, past a
+// mismatch in a full slot, by probing on.
+__device__ __forceinline__ uint64_t resolve(const Dx& x, const uint64_t (&kw)[4],
+                                            const uint64_t (&sv)[8], uint64_t maxp) {
+  if (sv[0] == 0) return kMiss;
+  if (sv[0] == tag_of(kw) && sv[4] == kw[0] && sv[5] == kw[1] && sv[6] == kw[2] && sv[7] == kw[3])
+    return sv[2];
+  return probe_from(x, kw, maxp, 1);
+}
+
+__global__ __launch_bounds__(64) void k_chain(ChainArgs a) {
+  const uint32_t lane = threadIdx.x;
+  if (lane >= a.lanes) return;
+  const uint32_t c = blockIdx.x * a.lanes + lane;
+  if (c >= a.n_chains) return;
+  const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, c);
+  uint32_t cur[8];  // key of the previous block (the chain's parent at first)
+  if (a.parents) {
+    const uint32_t* p = (const uint32_t*)(a.parents + 32ull * c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = __builtin_bswap32(p[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = a.ns[i];
+  }
+  const bool lookup = a.x.mem != nullptr;
+  const uint64_t maxp = lookup ? a.x.mem[1] : 0;
+  uint64_t n_hit = 0;
+  bool pending = false, missed = false;
+  uint64_t kw[4] = {0, 0, 0, 0}, sv[8];
+  // Iteration k computes key k while the lookup of key k-1, issued at the end
+  // of iteration k-1, is in flight; key k is kept only if k-1 was a hit.
+  for (uint64_t k = 0; k <= r.n; ++k) {
+    uint32_t nk[8];
+    const bool compute = k < r.n && (!missed || a.all_keys);
+    if (compute) block_key(nk, cur, a.tokens + r.t0 + k * a.bt, a.bt, a.nb, a.len_hi, a.len_lo);
+    if (pending) {
+      const uint64_t hv = resolve(a.x, kw, sv, maxp);
+      if (hv == kMiss) {
+        missed = true;
+      } else {
+        a.handles[r.s0 + k - 1] = hv;
+        ++n_hit;
+      }
+      pending = false;
+    }
+    if (!compute || (missed && !a.all_keys)) break;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) cur[i] = nk[i];
+    store_key(a.keys, r.s0 + k, cur);
+    if (lookup && !missed) {
+      key_words(kw, cur);
+      const uint64_t* slot = slot_ptr(a.x, kw[1] & a.x.mask);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sv[i] = slot[i];
+      pending = true;
+    }
+  }
+  if (lookup) {
+    for (uint64_t j = n_hit; j < r.n; ++j) a.handles[r.s0 + j] = kMiss;
+  }
+  a.hits[c] = (uint32_t)(lookup ? n_hit : r.n);
+}
+
+// ---- staging of tl_load's inputs --------------------------------------------
+struct StageArgs {
+  const uint32_t* tokens;
+  uint64_t n_tokens;
+  const uint64_t* tok_off;
+  const uint64_t* slot_off;
+  uint64_t n_slots;
+  const uint64_t* first_block;
+  uint32_t n_chains;
+  uint32_t bt;
+  uint32_t ppb;
+  uint32_t n_groups;
+  const uint32_t* hits;
+  const uint64_t* handles;
+  const uint64_t* hptr;
+  const uint64_t* hlen;
+  uint64_t n_handles;
+  uint64_t* rec_ptrs;
+  uint64_t* rec_lens;
+  uint64_t* bidx;
+  uint32_t* tokens_out;
+  const int32_t* tables_in;  // null: page j of slot q is q * ppb + j
+  int32_t* tables_out;
+};
+
+__device__ __forceinline__ bool stage_hit(const StageArgs& a, uint64_t slot, uint64_t k,
+                                          uint64_t hits, uint64_t* h) {
+  if (k >= hits) return false;
+  *h = a.handles[slot];
+  return *h < a.n_handles;
+}
+
+// One wavefront per chain; lanes stride over the chain's slots.
+__global__ __launch_bounds__(64) void k_chain_stage(StageArgs a) {
+  const uint32_t lane = threadIdx.x;
+  for (uint32_t c = blockIdx.x; c < a.n_chains; c += gridDim.x) {
+    const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, c);
+    const uint64_t hits_raw = a.hits[c];
+    const uint64_t hits = hits_raw < r.n ? hits_raw : r.n;
+    const uint64_t first = a.first_block ? a.first_block[c] : 0;
+    for (uint64_t k = lane; k < r.slots; k += 64) {
+      const uint64_t q = r.s0 + k;
+      uint64_t h = 0;
+      const bool hit = stage_hit(a, q, k, hits, &h);
+      a.rec_ptrs[q] = hit ? a.hptr[h] : 0;
+      a.rec_lens[q] = hit ? a.hlen[h] : 0;
+      a.bidx[q] = first + k;
+    }
+    if (a.tokens_out) {
+      const uint64_t n_tok = r.slots * a.bt, have = r.n * a.bt;
+      uint32_t* dst = a.tokens_out + r.s0 * a.bt;
+      const uint32_t* src = a.tokens + r.t0;
+      for (uint64_t e = lane; e < n_tok; e += 64) dst[e] = e < have ? src[e] : 0;
+    }
+    if (a.tables_out) {
+      const uint64_t per = r.slots * a.ppb, row = a.n_slots * a.ppb;
+      for (uint64_t e = lane; e < per; e += 64) {
+        const uint64_t k = e / a.ppb, at = r.s0 * a.ppb + e;
+        uint64_t h = 0;
+        const bool hit = stage_hit(a, r.s0 + k, k, hits, &h);
+        for (uint32_t g = 0; g < a.n_groups; ++g) {
+          const uint64_t i = (uint64_t)g * row + at;
+          a.tables_out[i] = !hit ? -1 : (a.tables_in ? a.tables_in[i] : (int32_t)at);
+        }
+      }
+    }
+  }
+}
+
+int launched() { return hipGetLastError() == hipSuccess ? TL_OK : TL_EDEVICE; }
+
+uint32_t grid_for(uint64_t n, uint32_t per, uint32_t cap) {
+  const uint64_t g = (n + per - 1) / per;
+  return (uint32_t)(g < cap ? (g ? g : 1) : cap);
+}
+
+int sm_count() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+}  // namespace
+
+namespace tl {
+
+int launch_dindex_clear(void* mem, uint64_t capacity, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  const uint64_t words = kHeaderWords + capacity * kSlotWords;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_clear, dim3(grid_for(words, 256, 8192)), dim3(256), 0, s,
+                       (uint64_t*)mem, words);
+  }
+  return launched();
+}
+
+int launch_dindex_put(void* mem, uint64_t capacity, void* stream, size_t n, const uint8_t* d_keys,
+                      const uint64_t* d_handles, uint8_t* d_status, uint32_t* d_ws) {
+  hipStream_t s = (hipStream_t)stream;
+  PutArgs a;
+  a.x.mem = (uint64_t*)mem;
+  a.x.mask = capacity - 1;
+  a.keys = d_keys;
+  a.handles = d_handles;
+  a.status = d_status;
+  a.target = d_ws;
+  a.n = (uint32_t)n;
+  const uint32_t g = grid_for(n, 256, 1u << 16);
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_claim, dim3(g), dim3(256), 0, s, a);
+  }
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_vote, dim3(g), dim3(256), 0, s, a);
+  }
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_publish, dim3(g), dim3(256), 0, s, a);
+  }
+  return launched();
+}
+
+int launch_dindex_get(const void* mem, uint64_t capacity, void* stream, size_t n,
+                      const uint8_t* d_keys, uint64_t* d_out) {
+  hipStream_t s = (hipStream_t)stream;
+  GetArgs a;
+  a.x.mem = (uint64_t*)mem;
+  a.x.mask = capacity - 1;
+  a.keys = d_keys;
+  a.out = d_out;
+  a.n = (uint32_t)n;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_get, dim3(grid_for(n, 256, 1u << 16)), dim3(256), 0, s, a);
+  }
+  return launched();
+}
+
+int launch_dindex_stats(const void* mem, void* stream, uint64_t* d_out) {
+  hipStream_t s = (hipStream_t)stream;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_dindex_stats, dim3(1), dim3(64), 0, s, (const uint64_t*)mem, d_out);
+  }
+  return launched();
+}
+
+int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
+                 const void* index_mem, uint64_t capacity, uint32_t flags, uint8_t* d_keys,
+                 uint64_t* d_handles, uint32_t* d_hits) {
+  hipStream_t s = (hipStream_t)stream;
+  ChainArgs a;
+  a.tokens = ch->d_tokens;
+  a.n_tokens = ch->n_tokens;
+  a.tok_off = ch->d_tok_off;
+  a.slot_off = ch->d_slot_off;
+  a.n_slots = ch->n_slots;
+  a.parents = ch->d_parents;
+  a.n_chains = (uint32_t)n_chains;
+  a.bt = ctx->geo.block_tokens;
+  const uint64_t msg = 32ull + 4ull * a.bt;  // message bytes per key
+  a.nb = (uint32_t)((msg + 8) / 64 + 1);
+  a.len_hi = (uint32_t)((msg * 8) >> 32);
+  a.len_lo = (uint32_t)(msg * 8);
+  // one chain per wavefront while chains fit the SIMDs, else share
+  const uint64_t simds = 4ull * (uint64_t)sm_count();
+  uint64_t lanes = (n_chains + simds - 1) / simds;
+  a.lanes = (uint32_t)(lanes < 1 ? 1 : (lanes > 64 ? 64 : lanes));
+  a.all_keys = (flags & TL_CHAIN_ALL_KEYS) ? 1 : 0;
+  for (int i = 0; i < 8; ++i)
+    a.ns[i] = (uint32_t)ctx->ns[4 * i] << 24 | (uint32_t)ctx->ns[4 * i + 1] << 16 |
+              (uint32_t)ctx->ns[4 * i + 2] << 8 | ctx->ns[4 * i + 3];
+  a.x.mem = (uint64_t*)index_mem;
+  a.x.mask = index_mem ? capacity - 1 : 0;
+  a.keys = d_keys;
+  a.handles = d_handles;
+  a.hits = d_hits;
+  const uint32_t waves = (uint32_t)((n_chains + a.lanes - 1) / a.lanes);
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_CHAIN, stream);
+    hipLaunchKernelGGL(k_chain, dim3(waves), dim3(64), 0, s, a);
+  }
+  return launched();
+}
+
+int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
+                 const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_hptr,
+                 const uint64_t* d_hlen, uint64_t n_handles, uint64_t* d_ptrs, uint64_t* d_lens,
+                 uint64_t* d_bidx, uint32_t* d_tokens_out, const int32_t* d_tables_in,
+                 int32_t* d_tables_out) {
+  hipStream_t s = (hipStream_t)stream;
+  StageArgs a;
+  a.tokens = ch->d_tokens;
+  a.n_tokens = ch->n_tokens;
+  a.tok_off = ch->d_tok_off;
+  a.slot_off = ch->d_slot_off;
+  a.n_slots = ch->n_slots;
+  a.first_block = ch->d_first_block;
+  a.n_chains = (uint32_t)n_chains;
+  a.bt = ctx->geo.block_tokens;
+  a.ppb = ctx->geo.ppb;
+  a.n_groups = ctx->geo.n_groups;
+  a.hits = d_hits;
+  a.handles = d_handles;
+  a.hptr = d_hptr;
+  a.hlen = d_hlen;
+  a.n_handles = n_handles;
+  a.rec_ptrs = d_ptrs;
+  a.rec_lens = d_lens;
+  a.bidx = d_bidx;
+  a.tokens_out = d_tokens_out;
+  a.tables_in = d_tables_in;
+  a.tables_out = d_tables_out;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_STAGE, stream);
+    hipLaunchKernelGGL(k_chain_stage, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(64), 0, s, a);
+  }
+  return launched();
+}
+
+}  // namespace tl

@@ -354,6 +354,115 @@ int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_
                          d_verdicts, (uint32_t*)d_workspace);
 }
 
+// ---- device index and key chains ---------------------------------------------
+static bool dindex_capacity_ok(size_t cap) {
+  return cap >= 2 && cap <= (size_t(1) << 31) && (cap & (cap - 1)) == 0;
+}
+
+size_t tl_dindex_bytes(size_t capacity) {
+  return dindex_capacity_ok(capacity) ? 256 + 64 * capacity : 0;
+}
+
+tl_dindex* tl_dindex_create(void* d_mem, size_t mem_bytes, size_t capacity, void* stream,
+                            int* status) {
+  int st = TL_OK;
+  tl_dindex* idx = nullptr;
+  if (!d_mem || ((uintptr_t)d_mem & 255) || !dindex_capacity_ok(capacity)) {
+    st = TL_EINVAL;
+  } else if (mem_bytes < tl_dindex_bytes(capacity)) {
+    st = TL_ERANGE;
+  } else if (!(idx = new (std::nothrow) tl_dindex{d_mem, capacity})) {
+    st = TL_ENOMEM;
+  } else if ((st = tl::launch_dindex_clear(d_mem, capacity, stream)) != TL_OK) {
+    delete idx;
+    idx = nullptr;
+  }
+  if (status) *status = st;
+  return idx;
+}
+
+void tl_dindex_destroy(tl_dindex* idx) { delete idx; }
+
+size_t tl_dindex_workspace_bytes(size_t n) { return (4 * n + 255) / 256 * 256; }
+
+int tl_dindex_put(tl_dindex* idx, void* stream, size_t n, const uint8_t* d_keys,
+                  const uint64_t* d_handles, uint8_t* d_status, void* d_workspace,
+                  size_t workspace_bytes) {
+  if (!idx) return TL_EINVAL;
+  if (n == 0) return TL_OK;
+  if (n >= (size_t(1) << 31)) return TL_ERANGE;
+  if (!d_keys || !d_handles || !d_workspace) return TL_EINVAL;
+  if (((uintptr_t)d_keys | (uintptr_t)d_handles) & 7 || ((uintptr_t)d_workspace & 3)) return TL_EINVAL;
+  if (workspace_bytes < tl_dindex_workspace_bytes(n)) return TL_ERANGE;
+  return tl::launch_dindex_put(idx->mem, idx->capacity, stream, n, d_keys, d_handles, d_status,
+                               (uint32_t*)d_workspace);
+}
+
+int tl_dindex_get(const tl_dindex* idx, void* stream, size_t n, const uint8_t* d_keys,
+                  uint64_t* d_handles_out) {
+  if (!idx) return TL_EINVAL;
+  if (n == 0) return TL_OK;
+  if (n >= (size_t(1) << 31)) return TL_ERANGE;
+  if (!d_keys || !d_handles_out) return TL_EINVAL;
+  if (((uintptr_t)d_keys | (uintptr_t)d_handles_out) & 7) return TL_EINVAL;
+  return tl::launch_dindex_get(idx->mem, idx->capacity, stream, n, d_keys, d_handles_out);
+}
+
+int tl_dindex_stats(const tl_dindex* idx, void* stream, uint64_t* d_out) {
+  if (!idx || !d_out || ((uintptr_t)d_out & 7)) return TL_EINVAL;
+  return tl::launch_dindex_stats(idx->mem, stream, d_out);
+}
+
+static int check_chains(size_t n_chains, const tl_chains* ch) {
+  if (!ch || !ch->d_tok_off || !ch->d_slot_off) return TL_EINVAL;
+  if (n_chains >= (size_t(1) << 24)) return TL_ERANGE;
+  if (ch->n_tokens && !ch->d_tokens) return TL_EINVAL;
+  if (((uintptr_t)ch->d_tok_off | (uintptr_t)ch->d_slot_off | (uintptr_t)ch->d_first_block) & 7)
+    return TL_EINVAL;
+  if (((uintptr_t)ch->d_tokens | (uintptr_t)ch->d_parents) & 3) return TL_EINVAL;
+  return TL_OK;
+}
+
+int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                    const tl_dindex* idx, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,
+                    uint32_t* d_hits) {
+  if (!ctx) return TL_EINVAL;
+  if (n_chains == 0) return TL_OK;
+  int r = check_chains(n_chains, chains);
+  if (r) return r;
+  if (flags & ~uint32_t(TL_CHAIN_ALL_KEYS)) return TL_EINVAL;
+  if (!d_hits || ((uintptr_t)d_hits & 3)) return TL_EINVAL;
+  if (chains->n_slots && (!d_keys || ((uintptr_t)d_keys & 3))) return TL_EINVAL;
+  if (idx && chains->n_slots && (!d_handles || ((uintptr_t)d_handles & 7))) return TL_EINVAL;
+  return tl::launch_chain(ctx, stream, n_chains, chains, idx ? idx->mem : nullptr,
+                          idx ? idx->capacity : 0, flags, d_keys, d_handles, d_hits);
+}
+
+int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                   const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_handle_ptrs,
+                   const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,
+                   uint64_t* d_record_lens, uint64_t* d_block_index, uint32_t* d_tokens_out,
+                   const int32_t* d_tables_in, int32_t* d_tables_out) {
+  if (!ctx) return TL_EINVAL;
+  if (n_chains == 0) return TL_OK;
+  int r = check_chains(n_chains, chains);
+  if (r) return r;
+  if (!d_hits || ((uintptr_t)d_hits & 3)) return TL_EINVAL;
+  if (n_handles && (!d_handle_ptrs || !d_handle_lens)) return TL_EINVAL;
+  if (((uintptr_t)d_handle_ptrs | (uintptr_t)d_handle_lens) & 7) return TL_EINVAL;
+  if (chains->n_slots) {
+    if (!d_handles || !d_record_ptrs || !d_record_lens || !d_block_index) return TL_EINVAL;
+    if (((uintptr_t)d_handles | (uintptr_t)d_record_ptrs | (uintptr_t)d_record_lens |
+         (uintptr_t)d_block_index) & 7)
+      return TL_EINVAL;
+    if (((uintptr_t)d_tokens_out | (uintptr_t)d_tables_in | (uintptr_t)d_tables_out) & 3)
+      return TL_EINVAL;
+  }
+  return tl::launch_stage(ctx, stream, n_chains, chains, d_hits, d_handles, d_handle_ptrs,
+                          d_handle_lens, n_handles, d_record_ptrs, d_record_lens, d_block_index,
+                          d_tokens_out, d_tables_in, d_tables_out);
+}
+
 // ---- misc -------------------------------------------------------------------
 const char* tl_status_string(int s) {
   switch (s) {

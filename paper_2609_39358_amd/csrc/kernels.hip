@@ -678,21 +678,8 @@ std::vector<EventPair> g_events[TL_KERNEL_COUNT];
 
 template <typename F>
 void timed(int kernel, hipStream_t s, F&& launch) {
-  bool on;
-  {
-    std::lock_guard<std::mutex> g(g_timing_mu);
-    on = g_timing_on;
-  }
-  EventPair p{nullptr, nullptr};
-  if (on && hipEventCreate(&p.a) == hipSuccess && hipEventCreate(&p.b) == hipSuccess) {
-    (void)hipEventRecord(p.a, s);
-    launch();
-    (void)hipEventRecord(p.b, s);
-    std::lock_guard<std::mutex> g(g_timing_mu);
-    g_events[kernel].push_back(p);
-  } else {
-    launch();
-  }
+  tl::TimedLaunch t(kernel, s);
+  launch();
 }
 
 // Workgroups for a chunk kernel: one wavefront per work item, capped so the
@@ -775,6 +762,30 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
                        dim3(256), 0, s, f);
   });
   return launched();
+}
+
+TimedLaunch::TimedLaunch(int kernel, void* stream) : kernel_(kernel), stream_(stream) {
+  bool on;
+  {
+    std::lock_guard<std::mutex> g(g_timing_mu);
+    on = g_timing_on;
+  }
+  hipEvent_t a, b;
+  if (!on || hipEventCreate(&a) != hipSuccess) return;
+  if (hipEventCreate(&b) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return;
+  }
+  a_ = a;
+  b_ = b;
+  (void)hipEventRecord(a, (hipStream_t)stream_);
+}
+
+TimedLaunch::~TimedLaunch() {
+  if (!a_) return;
+  (void)hipEventRecord((hipEvent_t)b_, (hipStream_t)stream_);
+  std::lock_guard<std::mutex> g(g_timing_mu);
+  g_events[kernel_].push_back(EventPair{(hipEvent_t)a_, (hipEvent_t)b_});
 }
 
 }  // namespace tl

@@ -58,6 +58,13 @@ class tl_blocks(ctypes.Structure):
                 ("d_tokens", ctypes.c_void_p), ("d_tables", ctypes.c_void_p)]
 
 
+class tl_chains(ctypes.Structure):
+    _fields_ = [("d_tokens", ctypes.c_void_p), ("n_tokens", ctypes.c_uint64),
+                ("d_tok_off", ctypes.c_void_p), ("d_slot_off", ctypes.c_void_p),
+                ("n_slots", ctypes.c_uint64), ("d_parents", ctypes.c_void_p),
+                ("d_first_block", ctypes.c_void_p)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError("libtaliesin.so is not built (python -m paper_2609_39358_amd.build)")
@@ -88,6 +95,16 @@ def _load():
         "tl_index_put": (c.c_int, [P, P, c.c_uint64]),
         "tl_index_get_batch": (c.c_int, [P, P, c.c_size_t, P]),
         "tl_index_size": (c.c_size_t, [P]),
+        "tl_dindex_bytes": (c.c_size_t, [c.c_size_t]),
+        "tl_dindex_create": (P, [P, c.c_size_t, c.c_size_t, P, c.POINTER(c.c_int)]),
+        "tl_dindex_destroy": (None, [P]),
+        "tl_dindex_workspace_bytes": (c.c_size_t, [c.c_size_t]),
+        "tl_dindex_put": (c.c_int, [P, P, c.c_size_t, P, P, P, P, c.c_size_t]),
+        "tl_dindex_get": (c.c_int, [P, P, c.c_size_t, P, P]),
+        "tl_dindex_stats": (c.c_int, [P, P, P]),
+        "tl_chain_lookup": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, c.c_uint32, P, P, P]),
+        "tl_chain_stage": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, P, c.c_uint64, P, P,
+                                     P, P, P, P]),
         "tl_status_string": (c.c_char_p, [c.c_int]),
         "tl_verdict_string": (c.c_char_p, [c.c_int]),
         "tl_abi_version": (c.c_int, []),
@@ -107,9 +124,15 @@ EXPORTED = (
     "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
     "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_save_layers", "tl_save_seal", "tl_load", "tl_index_create",
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
+    "tl_dindex_bytes", "tl_dindex_create", "tl_dindex_destroy", "tl_dindex_workspace_bytes",
+    "tl_dindex_put", "tl_dindex_get", "tl_dindex_stats", "tl_chain_lookup", "tl_chain_stage",
     "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
     "tl_timing_read")
-KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4}
+KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4, "chain": 5,
+           "stage": 6, "index": 7}
+TL_INDEX_STORED, TL_INDEX_FULL, TL_INDEX_TAG_CLASH = 0x01, 0x20, 0x21
+TL_CHAIN_ALL_KEYS = 1
+MISS = 2**64 - 1
 
 
 def lib():
@@ -318,6 +341,78 @@ class Index:
 
 def tl_index_create(capacity: int) -> Index:
     return Index(capacity)
+
+
+# ------------------------------------------------------------------ device index and key chains
+class DeviceIndex:
+    """A tl_dindex over device memory given by the caller (a uint8 tensor of
+    at least tl_dindex_bytes(capacity) bytes, kept alive here)."""
+
+    def __init__(self, mem, capacity: int, stream=None):
+        self.capacity, self.mem = capacity, mem
+        st = ctypes.c_int(0)
+        nbytes = mem.numel() * mem.element_size() if hasattr(mem, "numel") else 0
+        self._h = _lib.tl_dindex_create(_addr(mem), nbytes, capacity, _stream(stream), ctypes.byref(st))
+        if not self._h:
+            raise TaliesinError(st.value, "tl_dindex_create")
+
+    @property
+    def handle(self) -> int:
+        return self._h
+
+    def put(self, stream, n: int, d_keys, d_handles, d_status, d_workspace, workspace_bytes: int):
+        _check(_lib.tl_dindex_put(self._h, _stream(stream), n, _addr(d_keys), _addr(d_handles),
+                                  _addr(d_status), _addr(d_workspace), workspace_bytes), "tl_dindex_put")
+
+    def get(self, stream, n: int, d_keys, d_out):
+        _check(_lib.tl_dindex_get(self._h, _stream(stream), n, _addr(d_keys), _addr(d_out)), "tl_dindex_get")
+
+    def stats(self, stream, d_out):
+        _check(_lib.tl_dindex_stats(self._h, _stream(stream), _addr(d_out)), "tl_dindex_stats")
+
+    def close(self):
+        if self._h:
+            _lib.tl_dindex_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def tl_dindex_bytes(capacity: int) -> int:
+    return int(_lib.tl_dindex_bytes(capacity))
+
+
+def tl_dindex_workspace_bytes(n: int) -> int:
+    return int(_lib.tl_dindex_workspace_bytes(n))
+
+
+def make_chains(d_tokens, n_tokens: int, d_tok_off, d_slot_off, n_slots: int, d_parents=None,
+                d_first_block=None) -> tl_chains:
+    c = tl_chains(_addr(d_tokens), n_tokens, _addr(d_tok_off), _addr(d_slot_off), n_slots, _addr(d_parents),
+                  _addr(d_first_block))
+    c._keep = (d_tokens, d_tok_off, d_slot_off, d_parents, d_first_block)
+    return c
+
+
+def tl_chain_lookup(ctx: Ctx, stream, n_chains: int, chains: tl_chains, index: Optional[DeviceIndex],
+                    flags: int, d_keys, d_handles, d_hits):
+    _check(_lib.tl_chain_lookup(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains),
+                                index.handle if index is not None else None, flags, _addr(d_keys),
+                                _addr(d_handles), _addr(d_hits)), "tl_chain_lookup")
+
+
+def tl_chain_stage(ctx: Ctx, stream, n_chains: int, chains: tl_chains, d_hits, d_handles, d_handle_ptrs,
+                   d_handle_lens, n_handles: int, d_record_ptrs, d_record_lens, d_block_index,
+                   d_tokens_out=None, d_tables_in=None, d_tables_out=None):
+    _check(_lib.tl_chain_stage(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains), _addr(d_hits),
+                               _addr(d_handles), _addr(d_handle_ptrs), _addr(d_handle_lens), n_handles,
+                               _addr(d_record_ptrs), _addr(d_record_lens), _addr(d_block_index),
+                               _addr(d_tokens_out), _addr(d_tables_in), _addr(d_tables_out)),
+           "tl_chain_stage")
 
 
 def sha256_selftest(data: bytes, impl: int) -> Optional[bytes]:

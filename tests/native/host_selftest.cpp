@@ -18,6 +18,16 @@ int launch_save_seal(const tl_ctx*, void*, size_t, int64_t, const tl_blocks*, co
                      uint8_t*) { return TL_EDEVICE; }
 int launch_load(const tl_ctx*, void*, size_t, const uint64_t*, const uint64_t*, const tl_blocks*,
                 const tl_cache*, uint8_t*, uint32_t*) { return TL_EDEVICE; }
+int launch_dindex_clear(void*, uint64_t, void*) { return TL_EDEVICE; }
+int launch_dindex_put(void*, uint64_t, void*, size_t, const uint8_t*, const uint64_t*, uint8_t*,
+                      uint32_t*) { return TL_EDEVICE; }
+int launch_dindex_get(const void*, uint64_t, void*, size_t, const uint8_t*, uint64_t*) { return TL_EDEVICE; }
+int launch_dindex_stats(const void*, void*, uint64_t*) { return TL_EDEVICE; }
+int launch_chain(const tl_ctx*, void*, size_t, const tl_chains*, const void*, uint64_t, uint32_t, uint8_t*,
+                 uint64_t*, uint32_t*) { return TL_EDEVICE; }
+int launch_stage(const tl_ctx*, void*, size_t, const tl_chains*, const uint32_t*, const uint64_t*,
+                 const uint64_t*, const uint64_t*, uint64_t, uint64_t*, uint64_t*, uint64_t*, uint32_t*,
+                 const int32_t*, int32_t*) { return TL_EDEVICE; }
 }  // namespace tl
 
 static int failures = 0;
@@ -125,6 +135,41 @@ int main() {
   tl_cache narrow = cache;
   narrow.page_stride = 4096;
   EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &narrow, verd, ws, sizeof ws) == TL_EINVAL);
+  // device index and key chains: sizes and argument checks
+  EXPECT(tl_dindex_bytes(1024) == 256 + 64 * 1024 && tl_dindex_bytes(1000) == 0 && tl_dindex_bytes(1) == 0);
+  EXPECT(tl_dindex_bytes((size_t)1 << 32) == 0 && tl_dindex_workspace_bytes(65) == 512);
+  alignas(256) static uint8_t imem[256 + 64 * 16];
+  EXPECT(!tl_dindex_create(imem, sizeof imem, 16, nullptr, &st) && st == TL_EDEVICE);  // the stubbed clear
+  EXPECT(!tl_dindex_create(imem + 8, sizeof imem, 16, nullptr, &st) && st == TL_EINVAL);
+  EXPECT(!tl_dindex_create(imem, sizeof imem - 1, 16, nullptr, &st) && st == TL_ERANGE);
+  EXPECT(!tl_dindex_create(imem, sizeof imem, 12, nullptr, &st) && st == TL_EINVAL);
+  tl_dindex fake = {imem, 16};
+  alignas(8) uint8_t dk[64];
+  uint64_t dh[2];
+  uint8_t dst8[2];
+  EXPECT(tl_dindex_put(&fake, nullptr, 2, dk, dh, dst8, ws, sizeof ws) == TL_EDEVICE);
+  EXPECT(tl_dindex_put(&fake, nullptr, 2, dk, dh, dst8, ws, 4) == TL_ERANGE);
+  EXPECT(tl_dindex_put(&fake, nullptr, 2, dk + 1, dh, dst8, ws, sizeof ws) == TL_EINVAL);
+  EXPECT(tl_dindex_put(&fake, nullptr, 0, nullptr, nullptr, nullptr, nullptr, 0) == TL_OK);
+  EXPECT(tl_dindex_get(&fake, nullptr, 2, dk, dh) == TL_EDEVICE && tl_dindex_get(nullptr, nullptr, 2, dk, dh) == TL_EINVAL);
+  EXPECT(tl_dindex_stats(&fake, nullptr, dh) == TL_EDEVICE && tl_dindex_stats(&fake, nullptr, nullptr) == TL_EINVAL);
+  uint64_t toff[3] = {0, 16, 40}, soff[3] = {0, 1, 2};
+  uint32_t hits[2];
+  tl_chains chn = {tk, 40, toff, soff, 2, nullptr, nullptr};
+  uint8_t ck[64];
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, 0, ck, nullptr, hits) == TL_EDEVICE);
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, &fake, 0, ck, nullptr, hits) == TL_EINVAL);  // handles needed
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, &fake, 0, ck, dh, hits) == TL_EDEVICE);
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, 2, ck, nullptr, hits) == TL_EINVAL);  // unknown flag
+  EXPECT(tl_chain_lookup(c, nullptr, (size_t)1 << 24, &chn, nullptr, 0, ck, nullptr, hits) == TL_ERANGE);
+  EXPECT(tl_chain_lookup(c, nullptr, 0, nullptr, nullptr, 0, nullptr, nullptr, nullptr) == TL_OK);
+  tl_chains no_off = chn;
+  no_off.d_slot_off = nullptr;
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &no_off, nullptr, 0, ck, nullptr, hits) == TL_EINVAL);
+  uint64_t sp[2], sl[2], sb[2];
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EDEVICE);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, nullptr, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, nullptr, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
   for (int s = 1; s >= -8; --s) EXPECT(tl_status_string(s) != nullptr);
   for (int v = 0; v < 0x20; ++v) EXPECT(tl_verdict_string(v) != nullptr);
   tl_ctx_destroy(c);

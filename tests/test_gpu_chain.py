@@ -1,0 +1,450 @@
+"""The device key chain, the device index and the device-side restore
+(tl_chain_lookup -> tl_chain_stage -> tl_load) against the oracle: keys equal
+the oracle's SHA-256 chain (pinned to hashlib), reuse counts equal its walk
+that stops at the first block with no stored state, the index behaves as a
+key -> handle map where the last duplicate of a batch wins, and the restore
+gives the verdicts and pages the oracle gives."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import taliesin as T
+from paper_2609_39358_amd.device import PagedCache, RecordStore
+from tests.gpu_case import DEV, FP, TEN, Case, host_layers, i32, i64, log
+
+pytestmark = pytest.mark.gpu
+SENT = 0xEE
+
+
+def ctx_bt(page_tokens, ppb=1, n_layers=1, groups=None):
+    """A context whose blocks hold page_tokens * ppb tokens (1 KiB rows per token)."""
+    ctx = T.tl_ctx_create(TEN, FP, n_layers, 4, 128, "bf16", page_tokens, None, groups, ppb)
+    return ctx, T.tl_ns_digest(ctx), page_tokens * ppb
+
+
+class Chains:
+    """Chains back to back on the device, with the oracle's view of them."""
+
+    def __init__(self, ctx, lengths, seed, bt, parents=None, slot_counts=None, first_block=None):
+        self.lengths, self.bt = list(lengths), bt
+        self.tokens = wl.tokens(max(sum(self.lengths), 1), seed)[:sum(self.lengths)]
+        self.tok_off = np.concatenate([[0], np.cumsum(self.lengths)]).astype(np.uint64)
+        nk = [L // bt for L in self.lengths] if slot_counts is None else list(slot_counts)
+        self.slot_off = np.concatenate([[0], np.cumsum(nk)]).astype(np.uint64)
+        self.n, self.n_slots = len(self.lengths), int(self.slot_off[-1])
+        self.parents = parents
+        self.first = first_block
+        self.d_tok = i32(self.tokens.view(np.int32)) if self.tokens.size else torch.zeros(1, dtype=torch.int32,
+                                                                                          device=DEV)
+        self.d_toff, self.d_soff = i64(self.tok_off), i64(self.slot_off)
+        self.d_par = None if parents is None else torch.from_numpy(np.frombuffer(b"".join(parents), np.uint8)
+                                                                   .copy()).to(DEV)
+        self.d_first = None if first_block is None else i64(first_block)
+        self.tl = T.make_chains(self.d_tok, int(self.tokens.size), self.d_toff, self.d_soff, self.n_slots,
+                                self.d_par, self.d_first)
+
+    def data(self, c):
+        return self.tokens[int(self.tok_off[c]):int(self.tok_off[c + 1])].tobytes()
+
+    def n_blocks(self, c):
+        return min(self.lengths[c] // self.bt, int(self.slot_off[c + 1] - self.slot_off[c]))
+
+    def lookup(self, ctx, index=None, flags=0):
+        keys = torch.full((max(self.n_slots, 1), 32), SENT, dtype=torch.uint8, device=DEV)
+        handles = torch.full((max(self.n_slots, 1),), 0x7777, dtype=torch.int64, device=DEV)
+        hits = torch.full((self.n,), 0xFFFFFFF, dtype=torch.int32, device=DEV)
+        T.tl_chain_lookup(ctx, torch.cuda.current_stream(), self.n, self.tl, index, flags, keys,
+                          handles if index is not None else None, hits)
+        torch.cuda.synchronize()
+        return keys.cpu().numpy(), handles.cpu().numpy().view(np.uint64), hits.cpu().numpy()
+
+
+def lengths_for(bt, n, seed):
+    rng = np.random.default_rng(seed)
+    fixed = [0, 1, max(bt - 1, 0), bt, bt + 1, 2 * bt, 7 * bt + 3]
+    rand = list(rng.integers(0, 40 * bt, size=n - len(fixed)))
+    return fixed + [int(x) for x in rand]
+
+
+@pytest.mark.parametrize("page_tokens,ppb", [(1, 1), (5, 1), (6, 1), (13, 1), (16, 1), (16, 3)])
+def test_chain_keys_equal_the_oracle_chain(page_tokens, ppb):
+    ctx, ns, bt = ctx_bt(page_tokens, ppb)
+    lengths = lengths_for(bt, 120, 10 + bt)
+    rng = np.random.default_rng(bt)
+    for parents in (None, [rng.integers(0, 256, 32, dtype=np.uint8).tobytes() for _ in lengths]):
+        ch = Chains(ctx, lengths, 3 + bt, bt, parents)
+        log("keys only: block tokens", bt, "chains", ch.n, "slots", ch.n_slots, "parents", parents is not None)
+        keys, _, hits = ch.lookup(ctx)
+        for c in range(ch.n):
+            want = ref.block_keys(ns if parents is None else parents[c], ch.data(c), 4 * bt)
+            assert hits[c] == len(want), c
+            s0 = int(ch.slot_off[c])
+            got = [keys[s0 + k].tobytes() for k in range(len(want))]
+            assert got == want, (c, bt)
+
+
+def test_chain_offsets_are_clamped():
+    ctx, ns, bt = ctx_bt(16)
+    lengths = [100, 64, 200, 50]
+    # slot ranges shorter and longer than the chains' full blocks
+    ch = Chains(ctx, lengths, 5, bt, slot_counts=[3, 6, 20, 1])
+    keys, _, hits = ch.lookup(ctx)
+    for c, cap in enumerate([3, 6, 20, 1]):
+        want = ref.block_keys(ns, ch.data(c), 4 * bt)[:cap]
+        assert hits[c] == len(want)
+        s0 = int(ch.slot_off[c])
+        assert [keys[s0 + k].tobytes() for k in range(len(want))] == want
+        assert (keys[s0 + len(want):s0 + cap] == SENT).all()  # slots past the chain's blocks untouched
+    # token offsets past the end of the token array: clamped, nothing read past it
+    toff = np.array([0, 100, 10**9, 10**9 + 5, 2**63], np.uint64)
+    ch.d_toff = i64(toff)
+    ch.tl = T.make_chains(ch.d_tok, int(ch.tokens.size), ch.d_toff, ch.d_soff, ch.n_slots)
+    keys, _, hits = ch.lookup(ctx)
+    assert hits[0] == 3 and hits[1] == min(int(ch.tokens.size - 100) // 16, 6) and hits[2] == 0 and hits[3] == 0
+    assert [keys[int(ch.slot_off[1]) + k].tobytes() for k in range(6)] == \
+        ref.block_keys(ns, ch.tokens[100:].tobytes(), 4 * bt)[:6]
+
+
+def new_index(capacity):
+    mem = torch.empty(T.tl_dindex_bytes(capacity), dtype=torch.uint8, device=DEV)
+    mem.fill_(0xA7)  # the create call must clear it
+    return T.DeviceIndex(mem, capacity, torch.cuda.current_stream())
+
+
+def dput(idx, keys, handles):
+    n = len(keys)
+    d_k = torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(n, 32).copy()).to(DEV)
+    d_h = i64(np.asarray(handles, np.uint64))
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    wsb = T.tl_dindex_workspace_bytes(n)
+    ws = torch.full((wsb,), 0xFF, dtype=torch.uint8, device=DEV)
+    idx.put(torch.cuda.current_stream(), n, d_k, d_h, st, ws, wsb)
+    torch.cuda.synchronize()
+    return st.cpu().numpy()
+
+
+def dget(idx, keys):
+    n = len(keys)
+    d_k = torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(n, 32).copy()).to(DEV)
+    out = torch.zeros(n, dtype=torch.int64, device=DEV)
+    idx.get(torch.cuda.current_stream(), n, d_k, out)
+    torch.cuda.synchronize()
+    return [int(x) for x in out.cpu().numpy().view(np.uint64)]
+
+
+def dstats(idx):
+    out = torch.zeros(2, dtype=torch.int64, device=DEV)
+    idx.stats(torch.cuda.current_stream(), out)
+    torch.cuda.synchronize()
+    return [int(x) for x in out.cpu()]
+
+
+def rand_keys(n, seed):
+    rng = np.random.default_rng(seed)
+    return [rng.integers(0, 256, 32, dtype=np.uint8).tobytes() for _ in range(n)]
+
+
+def test_device_index_is_a_map_where_the_last_duplicate_wins():
+    idx = new_index(1024)
+    keys = rand_keys(400, 1)
+    batch = keys + [keys[5], keys[7], keys[5]]  # duplicates inside one call
+    handles = list(range(1000, 1000 + len(batch)))
+    st = dput(idx, batch, handles)
+    assert (st == T.TL_INDEX_STORED).all()
+    want = ref.index_put({}, batch, handles)
+    absent = rand_keys(100, 2)
+    assert dget(idx, keys + absent) == [want[k] for k in keys] + [T.MISS] * 100
+    used, maxp = dstats(idx)
+    assert used == 400 and 0 <= maxp < 1024
+    # a second call overwrites and inserts
+    more = keys[:50] + absent[:30]
+    st = dput(idx, more, range(50 + 30))
+    assert (st == T.TL_INDEX_STORED).all()
+    ref.index_put(want, more, range(80))
+    assert dget(idx, keys + absent) == [want.get(k, T.MISS) for k in keys + absent]
+    assert dstats(idx)[0] == 430
+
+
+def test_device_index_full_and_tag_clash():
+    idx = new_index(64)
+    keys = rand_keys(100, 3)
+    st = dput(idx, keys, range(100))
+    stored = [k for k, s in zip(keys, st) if s == T.TL_INDEX_STORED]
+    assert len(stored) == 64 and ((st == T.TL_INDEX_STORED) | (st == T.TL_INDEX_FULL)).all()
+    got = dget(idx, keys)
+    for i, (k, s) in enumerate(zip(keys, st)):
+        assert got[i] == (i if s == T.TL_INDEX_STORED else T.MISS)
+    assert dstats(idx)[0] == 64
+    # same first 16 bytes (tag and home slot), different rest: reported, never merged
+    idx = new_index(256)
+    a = rand_keys(1, 4)[0]
+    b = a[:16] + bytes(x ^ 0x5A for x in a[16:])
+    c = bytes([a[0] ^ 1]) + a[1:16] + bytes(x ^ 0x33 for x in a[16:])  # differs in the tag's ignored bit
+    assert list(dput(idx, [a], [11])) == [T.TL_INDEX_STORED]
+    assert list(dput(idx, [b, c], [22, 33])) == [T.TL_INDEX_TAG_CLASH] * 2
+    assert dget(idx, [a, b, c]) == [11, T.MISS, T.MISS]
+    # same tag, other home slot: no clash
+    d = a[:8] + bytes(x ^ 0xFF for x in a[8:])
+    assert list(dput(idx, [d], [44])) == [T.TL_INDEX_STORED]
+    assert dget(idx, [a, d]) == [11, 44]
+    # within one call exactly one of two clashing keys gets in
+    idx = new_index(256)
+    st = dput(idx, [a, b], [1, 2])
+    assert sorted(st.tolist()) == [T.TL_INDEX_STORED, T.TL_INDEX_TAG_CLASH]
+    got = dget(idx, [a, b])
+    assert got == ([1, T.MISS] if st[0] == T.TL_INDEX_STORED else [T.MISS, 2])
+
+
+def stored_docs(ns, bt, n_docs, blocks_per_doc, seed):
+    docs = [wl.tokens(blocks_per_doc * bt, seed + d) for d in range(n_docs)]
+    keys = [ref.block_keys(ns, d.tobytes(), 4 * bt) for d in docs]
+    return docs, keys
+
+
+def requests_for(docs, bt, n, seed):
+    """Prefixes of stored documents with a divergent tail, whole documents and
+    unrelated requests; some end inside a block."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        d = docs[rng.integers(len(docs))]
+        kind = i % 4
+        if kind == 0:
+            out.append(d[:rng.integers(0, d.size + 1)])
+        elif kind == 1:
+            m = int(rng.integers(0, d.size // bt + 1)) * bt
+            out.append(np.concatenate([d[:m], wl.tokens(int(rng.integers(0, 5 * bt)), seed + 1000 + i)]))
+        elif kind == 2:
+            out.append(d.copy())
+        else:
+            out.append(wl.tokens(int(rng.integers(0, 6 * bt)), seed + 2000 + i))
+    return out
+
+
+@pytest.mark.parametrize("capacity,flags", [(1024, 0), (1024, 1), (512, 0)])
+def test_chain_lookup_equals_the_oracle_walk(capacity, flags):
+    ctx, ns, bt = ctx_bt(16)
+    docs, dkeys = stored_docs(ns, bt, 6, 70, 40)
+    flat = [k for ks in dkeys for k in ks]
+    # leave out some blocks (holes) so that reuse ends inside a document
+    holes = {3 * 70 + 20, 5 * 70 + 0, 1 * 70 + 69}
+    put_keys = [k for i, k in enumerate(flat) if i not in holes]
+    put_h = [i for i in range(len(flat)) if i not in holes]
+    idx = new_index(capacity)
+    assert (dput(idx, put_keys, put_h) == T.TL_INDEX_STORED).all()
+    index = ref.index_put({}, put_keys, put_h)
+    log("index", capacity, "slots,", len(put_keys), "keys, longest probe", dstats(idx)[1])
+    reqs = requests_for(docs, bt, 160, 41)
+    lengths = [r.size for r in reqs]
+    ch = Chains(ctx, lengths, 0, bt)
+    ch.tokens[:] = np.concatenate(reqs) if reqs else ch.tokens
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    keys, handles, hits = ch.lookup(ctx, idx, flags)
+    total_hits = 0
+    for c in range(ch.n):
+        want_keys, want_hits, want_h = ref.chain_walk(ns, ch.data(c), 4 * bt, index)
+        s0 = int(ch.slot_off[c])
+        nk = len(want_keys)
+        assert hits[c] == want_hits, c
+        assert list(handles[s0:s0 + want_hits]) == want_h
+        assert (handles[s0 + want_hits:s0 + nk] == np.uint64(T.MISS)).all()
+        kept = nk if flags else min(want_hits + 1, nk)
+        assert [keys[s0 + k].tobytes() for k in range(kept)] == want_keys[:kept]
+        assert (keys[s0 + kept:s0 + nk] == SENT).all()
+        total_hits += want_hits
+    assert total_hits > 500  # the walk really reused blocks
+
+
+def test_stage_builds_load_inputs():
+    # two layer groups and two pages per block: tables are [2][slots * 2]
+    ctx, ns, bt = ctx_bt(16, ppb=2, n_layers=2, groups=[0, 1])
+    docs, dkeys = stored_docs(ns, bt, 3, 12, 50)
+    flat = [k for ks in dkeys for k in ks]
+    n_rec = len(flat)
+    idx = new_index(256)
+    handles_put = list(range(n_rec))
+    handles_put[7] = n_rec + 5  # a handle past the handle arrays: not a hit
+    dput(idx, flat, handles_put)
+    reqs = requests_for(docs, bt, 24, 51)
+    first = np.arange(len(reqs), dtype=np.uint64) * 1000
+    ch = Chains(ctx, [r.size for r in reqs], 0, bt, first_block=first)
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    keys, handles, hits = ch.lookup(ctx, idx)
+    S = ch.n_slots
+    hptr = i64(np.arange(n_rec, dtype=np.uint64) * 4096 + 0x100000)
+    hlen = i64(np.arange(n_rec, dtype=np.uint64) + 77)
+    d_hits = i32(hits.astype(np.int32))
+    d_handles = i64(handles)
+    ptrs = torch.full((S,), -5, dtype=torch.int64, device=DEV)
+    lens = torch.full((S,), -5, dtype=torch.int64, device=DEV)
+    bidx = torch.full((S,), -5, dtype=torch.int64, device=DEV)
+    toks = torch.full((S, bt), -5, dtype=torch.int32, device=DEV)
+    tin = i32(np.random.default_rng(1).integers(0, 10**6, size=(2, S * 2)))
+    tout = torch.full((2, S * 2), -9, dtype=torch.int32, device=DEV)
+    tout2 = torch.full((2, S * 2), -9, dtype=torch.int32, device=DEV)
+    for t_in, t_out in ((tin, tout), (None, tout2)):
+        T.tl_chain_stage(ctx, torch.cuda.current_stream(), ch.n, ch.tl, d_hits, d_handles, hptr, hlen, n_rec,
+                         ptrs, lens, bidx, toks, t_in, t_out)
+    torch.cuda.synchronize()
+    ptrs, lens, bidx = (x.cpu().numpy().view(np.uint64) for x in (ptrs, lens, bidx))
+    toks, tin, tout, tout2 = (x.cpu().numpy() for x in (toks, tin, tout, tout2))
+    for c in range(ch.n):
+        s0, nb = int(ch.slot_off[c]), ch.n_blocks(c)
+        data = np.frombuffer(ch.data(c), np.uint32)
+        for k in range(int(ch.slot_off[c + 1]) - s0):
+            q = s0 + k
+            h = int(handles[q]) if k < hits[c] else None
+            hit = h is not None and h < n_rec
+            assert ptrs[q] == (h * 4096 + 0x100000 if hit else 0) and lens[q] == (h + 77 if hit else 0)
+            assert bidx[q] == first[c] + k
+            want_t = data[k * bt:(k + 1) * bt] if k < nb else np.zeros(bt, np.uint32)
+            assert np.array_equal(toks[q].view(np.uint32), want_t)
+            for g in range(2):
+                for j in range(2):
+                    e = q * 2 + j
+                    assert tout[g, e] == (tin[g, e] if hit else -1)
+                    assert tout2[g, e] == (e if hit else -1)
+    assert (hits > 0).sum() > 5
+
+
+def test_device_restore_matches_the_oracle():
+    """Save one document, index its records on the device, then restore a
+    batch of requests with no host step between lookup and load."""
+    geom = wl.Geometry(3, 4, 64, 16)
+    c = Case(geom, 20, 24, 24, seed=60)
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    rb = c.lay.record_bytes
+    store.buf[4, c.lay.payload_offset + 1234] ^= 0x20  # record 4 is damaged
+    bt = c.lay.page_tokens
+    doc = c.tokens.reshape(-1)
+    idx = new_index(128)
+    dput(idx, [k.tobytes() for k in c.keys], range(c.n))
+    index = ref.index_put({}, [k.tobytes() for k in c.keys], range(c.n))
+    reqs = [doc.copy(), doc[:7 * bt + 3], np.concatenate([doc[:12 * bt], wl.tokens(40, 61)]), wl.tokens(50, 62),
+            doc[:0]]
+    ch = Chains(c.ctx, [r.size for r in reqs], 0, bt)
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    S = ch.n_slots
+    keys = torch.empty((S, 32), dtype=torch.uint8, device=DEV)
+    handles = torch.empty(S, dtype=torch.int64, device=DEV)
+    hits = torch.empty(ch.n, dtype=torch.int32, device=DEV)
+    ptrs, lens, bidx = (torch.empty(S, dtype=torch.int64, device=DEV) for _ in range(3))
+    toks = torch.empty((S, bt), dtype=torch.int32, device=DEV)
+    tab = torch.empty((1, S), dtype=torch.int32, device=DEV)
+    pool = PagedCache(geom.n_layers, S, c.stride, DEV)
+    for t in pool.k + pool.v:
+        t.fill_(0x3C)
+    verd = torch.zeros(S, dtype=torch.uint8, device=DEV)
+    ws_b = T.tl_workspace_bytes(c.ctx, S)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.current_stream()
+    T.tl_chain_lookup(c.ctx, s, ch.n, ch.tl, idx, 0, keys, handles, hits)
+    T.tl_chain_stage(c.ctx, s, ch.n, ch.tl, hits, handles, store.ptrs, store.lens, c.n, ptrs, lens, bidx, toks,
+                     None, tab)
+    T.tl_load(c.ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab), pool.tl(), verd, ws, ws_b)
+    torch.cuda.synchronize()
+    verd = verd.cpu().numpy()
+    pk, pv = host_layers(pool)
+    sk, sv = host_layers(c.src)
+    slab = c.lay.slab_bytes
+    n_acc = n_rej = 0
+    for r in range(ch.n):
+        _, want_hits, want_h = ref.chain_walk(c.ns, ch.data(r), 4 * bt, index)
+        assert int(hits.cpu()[r]) == want_hits
+        s0 = int(ch.slot_off[r])
+        for k in range(int(ch.slot_off[r + 1]) - s0):
+            q = s0 + k
+            if k >= want_hits:
+                assert verd[q] == ref.MISSING
+                for l in range(geom.n_layers):
+                    assert (pk[l][q] == 0x3C).all() and (pv[l][q] == 0x3C).all()  # untouched
+                continue
+            rid = want_h[k]
+            rec = store.buf[rid].cpu().numpy().tobytes()
+            want_v = ref.verify(c.lay, c.ns, rec, c.keys[rid].tobytes(), k, c.tokens[rid], range(c.lay.n_slabs))
+            assert verd[q] == want_v, (r, k)
+            for l in range(geom.n_layers):
+                p = int(c.t_src[0][rid])
+                if want_v == ref.ACCEPT:
+                    assert np.array_equal(pk[l][q][:slab], sk[l][p][:slab])
+                    assert np.array_equal(pv[l][q][:slab], sv[l][p][:slab])
+                    n_acc += 1
+                else:
+                    assert not pk[l][q][:slab].any() and not pv[l][q][:slab].any()
+                    n_rej += 1
+    assert n_acc > 0 and n_rej > 0
+
+
+def test_device_restore_in_a_graph_replays_with_new_requests():
+    geom = wl.Geometry(2, 4, 64, 16)
+    c = Case(geom, 16, 16, 16, seed=70)
+    c.make_src()
+    store, st = c.save()
+    bt = c.lay.page_tokens
+    doc = c.tokens.reshape(-1)
+    idx = new_index(64)
+    dput(idx, [k.tobytes() for k in c.keys], range(c.n))
+    index = ref.index_put({}, [k.tobytes() for k in c.keys], range(c.n))
+    lengths = [8 * bt + 5, 10 * bt, 6 * bt]
+    ch = Chains(c.ctx, lengths, 0, bt)
+    S = ch.n_slots
+    keys = torch.empty((S, 32), dtype=torch.uint8, device=DEV)
+    handles = torch.empty(S, dtype=torch.int64, device=DEV)
+    hits = torch.empty(ch.n, dtype=torch.int32, device=DEV)
+    ptrs, lens, bidx = (torch.empty(S, dtype=torch.int64, device=DEV) for _ in range(3))
+    toks = torch.empty((S, bt), dtype=torch.int32, device=DEV)
+    tab = torch.empty((1, S), dtype=torch.int32, device=DEV)
+    pool = PagedCache(geom.n_layers, S, c.stride, DEV)
+    verd = torch.zeros(S, dtype=torch.uint8, device=DEV)
+    ws_b = T.tl_workspace_bytes(c.ctx, S)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    blk = T.make_blocks(keys, bidx, toks, tab)
+
+    def path(s):
+        T.tl_chain_lookup(c.ctx, s, ch.n, ch.tl, idx, 0, keys, handles, hits)
+        T.tl_chain_stage(c.ctx, s, ch.n, ch.tl, hits, handles, store.ptrs, store.lens, c.n, ptrs, lens, bidx,
+                         toks, None, tab)
+        T.tl_load(c.ctx, s, S, ptrs, lens, blk, pool.tl(), verd, ws, ws_b)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        path(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        path(s)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(7)
+    for step in range(4):
+        # new request contents of the same lengths: prefixes of the document
+        # that diverge at a random block
+        parts = []
+        for L in lengths:
+            m = int(rng.integers(0, L // bt + 1))
+            parts.append(np.concatenate([doc[:m * bt], wl.tokens(L - m * bt, 100 + step * 7 + L)]))
+        ch.d_tok.copy_(torch.from_numpy(np.concatenate(parts).view(np.int32)))
+        ch.tokens[:] = np.concatenate(parts)
+        for t in pool.k + pool.v:
+            t.fill_(step)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got_h, got_v, got_pages = hits.cpu().numpy().copy(), verd.cpu().numpy().copy(), host_layers(pool)
+        for t in pool.k + pool.v:
+            t.fill_(step)
+        path(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert np.array_equal(got_h, hits.cpu().numpy()) and np.array_equal(got_v, verd.cpu().numpy())
+        want_pages = host_layers(pool)
+        for a, b in zip(got_pages[0] + got_pages[1], want_pages[0] + want_pages[1]):
+            assert np.array_equal(a, b)
+        want = [ref.chain_walk(c.ns, ch.data(r), 4 * bt, index)[1] for r in range(ch.n)]
+        assert list(got_h) == want, step
+        log("replay", step, "hits", want)

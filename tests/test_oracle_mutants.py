@@ -120,3 +120,40 @@ def test_missing_segment_check_caught(monkeypatch):
     monkeypatch.setattr(ref, "verify", lax)
     with pytest.raises(AssertionError):
         pins.test_every_single_bit_flip_is_rejected(32)
+
+
+def _walk_skipping_holes(parent, data, block_bytes, index):
+    # wrong: counts every stored block, not only the leading run
+    keys = ref.block_keys(parent, data, block_bytes)
+    hit = [k for k in keys if k in index]
+    return keys, len(hit), [index[k] for k in hit]
+
+
+def _walk_off_by_one(parent, data, block_bytes, index):
+    keys, hits, handles = _real_walk(parent, data, block_bytes, index)
+    return keys, min(hits + 1, len(keys)), handles
+
+
+_real_walk = ref.chain_walk
+
+
+@pytest.mark.parametrize("mutant", [_walk_skipping_holes, _walk_off_by_one])
+def test_reuse_walk_mutants_caught(monkeypatch, mutant):
+    from tests import test_oracle_reuse as reuse
+    monkeypatch.setattr(ref, "chain_walk", mutant)
+    with pytest.raises(AssertionError):
+        reuse.test_walk_against_brute_force_on_every_subset()
+        reuse.test_hole_ends_reuse_even_if_later_blocks_are_stored()
+
+
+def test_first_duplicate_wins_caught(monkeypatch):
+    from tests import test_oracle_reuse as reuse
+
+    def first_wins(index, keys, handles):
+        for k, h in zip(keys, handles):
+            index.setdefault(bytes(k), int(h))
+        return index
+
+    monkeypatch.setattr(ref, "index_put", first_wins)
+    with pytest.raises(AssertionError):
+        reuse.test_index_put_last_duplicate_wins_and_overwrites()
