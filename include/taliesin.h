@@ -338,6 +338,30 @@ int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_c
                     const tl_dindex* idx, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,
                     uint32_t* d_hits);
 
+/* Block fingerprints for a token index: d_out[b] = SHA-256(namespace digest
+ * | u64 little-endian d_block_index[b] | the block's token ids) for n blocks
+ * (device d_tokens [n][tokens per block], d_block_index [n], d_out [n][32]).
+ * A token index is a tl_dindex from these fingerprints to the handles of the
+ * stored blocks (the same handles as in the key index). */
+int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
+                          const uint64_t* d_block_index, uint8_t* d_out);
+
+/* Same results as tl_chain_lookup with flags 0 (d_hits, d_handles for slots
+ * [0, n_c), d_keys for slots [0, min(hits + 1, n_c))), computed for all
+ * blocks of a chain at once instead of one after another: the token index
+ * `tok_idx` proposes for each block the chain key of a stored block with the
+ * same tokens at the same position (d_handle_keys [n_handles][32]: the key
+ * of each handle's record), every block hashes its tokens onto its
+ * predecessor's proposal, and the proposals are confirmed in order; at the
+ * first block whose proposal is missing or differs the chain goes on one
+ * block after another. A stale or incomplete token index costs time, never
+ * correctness. Other key slots of a chain's range hold unspecified bytes.
+ * Positions are d_first_block[c] + k, as in tl_chain_stage. One workgroup per
+ * chain; fewer than 2^24 chains. */
+int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                        const tl_dindex* idx, const tl_dindex* tok_idx, const uint8_t* d_handle_keys,
+                        uint64_t n_handles, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits);
+
 /* tl_load's per-block inputs from a lookup, for every slot of every chain's
  * range (n_slots blocks): slot k of chain c is a hit when k < d_hits[c] and
  * its handle is below n_handles; then d_record_ptrs / d_record_lens get

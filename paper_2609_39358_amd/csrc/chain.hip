@@ -79,13 +79,15 @@ __device__ __forceinline__ void compress(uint32_t (&st)[8], uint32_t (&w)[16]) {
   for (int i = 0; i < 8; ++i) st[i] += o[i];
 }
 
-// Key of one block: SHA-256 over the previous key (32 bytes, i.e. the eight
-// big-endian words prev[]) followed by bt u32 token ids. The message is
-// 32 + 4*bt bytes, then 0x80, zeros and the 64-bit bit length, in nb
-// 64-byte blocks (nb is the same for every lane).
-__device__ __forceinline__ void block_key(uint32_t (&key)[8], const uint32_t (&prev)[8],
-                                          const uint32_t* tok, uint32_t bt, uint32_t nb,
-                                          uint32_t len_hi, uint32_t len_lo) {
+// SHA-256 of PW big-endian prefix words followed by bt u32 token ids (as
+// little-endian bytes): the message is 4*PW + 4*bt bytes, then 0x80, zeros
+// and the 64-bit bit length, in nb 64-byte blocks (the same for every lane).
+// PW = 8 gives a chain key (the previous key, then the block's tokens);
+// PW = 10 a block fingerprint (namespace digest and position, then tokens).
+template <int PW>
+__device__ __forceinline__ void sha_tokens(uint32_t (&out)[8], const uint32_t (&pre)[PW],
+                                           const uint32_t* tok, uint32_t bt, uint32_t nb,
+                                           uint32_t len_hi, uint32_t len_lo) {
   uint32_t st[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) st[i] = tl::kSha256IV[i];
@@ -95,9 +97,9 @@ __device__ __forceinline__ void block_key(uint32_t (&key)[8], const uint32_t (&p
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       const uint32_t g = 16 * c + t;  // word index in the message
-      const uint32_t j = g - 8;       // token index (wraps for g < 8)
+      const uint32_t j = g - PW;      // token index (wraps for g < PW)
       uint32_t v;
-      if (g < 8) v = prev[t & 7];
+      if (t < PW && g < PW) v = pre[t < PW ? t : 0];
       else if (j < bt) v = __builtin_bswap32(tok[j]);
       else if (j == bt) v = 0x80000000u;
       else if (g == last) v = len_lo;
@@ -108,7 +110,16 @@ __device__ __forceinline__ void block_key(uint32_t (&key)[8], const uint32_t (&p
     compress(st, w);
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) key[i] = st[i];
+  for (int i = 0; i < 8; ++i) out[i] = st[i];
+}
+
+// Message geometry of sha_tokens for PW prefix words and bt tokens.
+struct MsgLen {
+  uint32_t nb, hi, lo;
+};
+inline MsgLen msg_len(uint32_t pw, uint32_t bt) {
+  const uint64_t bytes = 4ull * pw + 4ull * bt;
+  return MsgLen{(uint32_t)((bytes + 8) / 64 + 1), (uint32_t)((bytes * 8) >> 32), (uint32_t)(bytes * 8)};
 }
 
 // ---- device index ---------------------------------------------------------
@@ -260,24 +271,20 @@ __global__ void k_dindex_stats(const uint64_t* mem, uint64_t* out) {
 }
 
 // ---- chain walk -------------------------------------------------------------
-struct ChainArgs {
+// Inputs shared by the walks.
+struct ChainIn {
   const uint32_t* tokens;
   uint64_t n_tokens;
   const uint64_t* tok_off;
   const uint64_t* slot_off;
   uint64_t n_slots;
   const uint8_t* parents;
+  const uint64_t* first_block;
   uint32_t n_chains;
-  uint32_t bt;    // tokens per block
-  uint32_t nb;    // SHA-256 blocks per key
-  uint32_t len_hi, len_lo;
-  uint32_t lanes; // chains per wavefront
-  uint32_t all_keys;
-  uint32_t ns[8]; // namespace digest as big-endian words
-  Dx x;           // x.mem == nullptr: keys only
-  uint8_t* keys;
-  uint64_t* handles;
-  uint32_t* hits;
+  uint32_t bt;     // tokens per block
+  MsgLen key;      // chain key message
+  MsgLen fp;       // fingerprint message
+  uint32_t ns[8];  // namespace digest as big-endian words
 };
 
 struct Range {
@@ -301,6 +308,26 @@ __device__ __forceinline__ Range chain_range(const uint64_t* tok_off, const uint
   return r;
 }
 
+__device__ __forceinline__ Range chain_range(const ChainIn& in, uint32_t c) {
+  return chain_range(in.tok_off, in.slot_off, in.n_tokens, in.n_slots, in.bt, c);
+}
+
+__device__ __forceinline__ void parent_words(uint32_t (&h)[8], const ChainIn& in, uint32_t c) {
+  if (in.parents) {
+    const uint32_t* p = (const uint32_t*)(in.parents + 32ull * c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = __builtin_bswap32(p[i]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = in.ns[i];
+  }
+}
+
+__device__ __forceinline__ void chain_key(uint32_t (&out)[8], const ChainIn& in, const uint32_t (&prev)[8],
+                                          const uint32_t* tok) {
+  sha_tokens<8>(out, prev, tok, in.bt, in.key.nb, in.key.hi, in.key.lo);
+}
+
 __device__ __forceinline__ void store_key(uint8_t* keys, uint64_t slot, const uint32_t (&h)[8]) {
   uint32_t* p = (uint32_t*)(keys + 32 * slot);
 #pragma unroll
@@ -317,58 +344,219 @@ __device__ __forceinline__ uint64_t resolve(const Dx& x, const uint64_t (&kw)[4]
   return probe_from(x, kw, maxp, 1);
 }
 
-__global__ __launch_bounds__(64) void k_chain(ChainArgs a) {
-  const uint32_t lane = threadIdx.x;
-  if (lane >= a.lanes) return;
-  const uint32_t c = blockIdx.x * a.lanes + lane;
-  if (c >= a.n_chains) return;
-  const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, c);
-  uint32_t cur[8];  // key of the previous block (the chain's parent at first)
-  if (a.parents) {
-    const uint32_t* p = (const uint32_t*)(a.parents + 32ull * c);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) cur[i] = __builtin_bswap32(p[i]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) cur[i] = a.ns[i];
-  }
-  const bool lookup = a.x.mem != nullptr;
-  const uint64_t maxp = lookup ? a.x.mem[1] : 0;
+// Sequential walk over blocks [k0, r.n) of one chain, `cur` holding the key
+// of block k0 - 1. Stores every key it keeps and, with an index (x.mem set),
+// the handle of every hit; stops after the first miss unless all_keys.
+// Iteration k computes key k while the lookup of key k-1, issued at the end
+// of iteration k-1, is in flight; key k is kept only if k-1 was a hit (or
+// all_keys). Returns the number of hits from k0 on.
+__device__ uint64_t seq_walk(const ChainIn& in, const Dx& x, bool all_keys, const Range& r,
+                             uint64_t k0, uint32_t (&cur)[8], uint8_t* keys, uint64_t* handles) {
+  const bool lookup = x.mem != nullptr;
+  const uint64_t maxp = lookup ? x.mem[1] : 0;
   uint64_t n_hit = 0;
   bool pending = false, missed = false;
   uint64_t kw[4] = {0, 0, 0, 0}, sv[8];
-  // Iteration k computes key k while the lookup of key k-1, issued at the end
-  // of iteration k-1, is in flight; key k is kept only if k-1 was a hit.
-  for (uint64_t k = 0; k <= r.n; ++k) {
+  for (uint64_t k = k0; k <= r.n; ++k) {
     uint32_t nk[8];
-    const bool compute = k < r.n && (!missed || a.all_keys);
-    if (compute) block_key(nk, cur, a.tokens + r.t0 + k * a.bt, a.bt, a.nb, a.len_hi, a.len_lo);
+    const bool compute = k < r.n && (!missed || all_keys);
+    if (compute) chain_key(nk, in, cur, in.tokens + r.t0 + k * in.bt);
     if (pending) {
-      const uint64_t hv = resolve(a.x, kw, sv, maxp);
+      const uint64_t hv = resolve(x, kw, sv, maxp);
       if (hv == kMiss) {
         missed = true;
       } else {
-        a.handles[r.s0 + k - 1] = hv;
+        handles[r.s0 + k - 1] = hv;
         ++n_hit;
       }
       pending = false;
     }
-    if (!compute || (missed && !a.all_keys)) break;
+    if (!compute || (missed && !all_keys)) break;
 #pragma unroll
     for (int i = 0; i < 8; ++i) cur[i] = nk[i];
-    store_key(a.keys, r.s0 + k, cur);
+    store_key(keys, r.s0 + k, cur);
     if (lookup && !missed) {
       key_words(kw, cur);
-      const uint64_t* slot = slot_ptr(a.x, kw[1] & a.x.mask);
+      const uint64_t* slot = slot_ptr(x, kw[1] & x.mask);
 #pragma unroll
       for (int i = 0; i < 8; ++i) sv[i] = slot[i];
       pending = true;
     }
   }
-  if (lookup) {
+  return lookup ? n_hit : r.n - k0;
+}
+
+struct ChainArgs {
+  ChainIn in;
+  uint32_t lanes;  // chains per wavefront
+  uint32_t all_keys;
+  Dx x;            // x.mem == nullptr: keys only
+  uint8_t* keys;
+  uint64_t* handles;
+  uint32_t* hits;
+};
+
+__global__ __launch_bounds__(64) void k_chain(ChainArgs a) {
+  const uint32_t lane = threadIdx.x;
+  if (lane >= a.lanes) return;
+  const uint32_t c = blockIdx.x * a.lanes + lane;
+  if (c >= a.in.n_chains) return;
+  const Range r = chain_range(a.in, c);
+  uint32_t cur[8];
+  parent_words(cur, a.in, c);
+  const uint64_t n_hit = seq_walk(a.in, a.x, a.all_keys != 0, r, 0, cur, a.keys, a.handles);
+  if (a.x.mem) {
     for (uint64_t j = n_hit; j < r.n; ++j) a.handles[r.s0 + j] = kMiss;
   }
-  a.hits[c] = (uint32_t)(lookup ? n_hit : r.n);
+  a.hits[c] = (uint32_t)n_hit;
+}
+
+// ---- block fingerprints and the verified parallel walk -----------------------
+// Fingerprint of a block: SHA-256(namespace digest | u64 LE position | token
+// ids), the key of the token index that proposes, for a block of a request,
+// the chain key of a stored block with the same tokens at the same position.
+__device__ __forceinline__ void fingerprint(uint32_t (&out)[8], const ChainIn& in, uint64_t pos,
+                                            const uint32_t* tok) {
+  uint32_t pre[10];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) pre[i] = in.ns[i];
+  pre[8] = __builtin_bswap32((uint32_t)pos);
+  pre[9] = __builtin_bswap32((uint32_t)(pos >> 32));
+  sha_tokens<10>(out, pre, tok, in.bt, in.fp.nb, in.fp.hi, in.fp.lo);
+}
+
+struct FpArgs {
+  ChainIn in;
+  const uint32_t* tokens;  // [n][bt]
+  const uint64_t* pos;     // [n]
+  uint8_t* out;            // [n][32]
+  uint32_t n;
+};
+
+__global__ __launch_bounds__(256) void k_fingerprint(FpArgs a) {
+  const uint32_t step = gridDim.x * 256;
+  for (uint32_t b = blockIdx.x * 256 + threadIdx.x; b < a.n; b += step) {
+    uint32_t f[8];
+    fingerprint(f, a.in, a.pos[b], a.tokens + (uint64_t)b * a.in.bt);
+    store_key(a.out, b, f);
+  }
+}
+
+constexpr uint32_t kParThreads = 256;
+
+struct ParArgs {
+  ChainIn in;
+  Dx x;                  // key index
+  Dx t;                  // token index: fingerprint -> handle
+  const uint8_t* hkeys;  // [n_handles][32] chain key of each handle's record
+  uint64_t n_handles;
+  uint8_t* keys;
+  uint64_t* handles;
+  uint32_t* hits;
+};
+
+// One workgroup per chain, kParThreads blocks per tile. For block k the
+// token index proposes cand_k, the key a stored block with the same tokens at
+// the same position has; every block then computes c_k = SHA-256(cand_{k-1} |
+// tokens_k) (cand_{-1} = the chain's parent) and looks c_k up in the key
+// index, all independently. If cand_j = c_j for every j < k, induction from
+// c_0 (computed from the true parent) makes c_0..c_k the true chain keys, so
+// the walk is exact up to the first block m where c_m is not in the index
+// (reuse ends at m) or cand_m != c_m (c_m is true and a hit, but c_{m+1} is
+// not known: the chain goes on sequentially from m+1). Results equal the
+// sequential walk's; candidates only decide how much of it runs in parallel.
+__global__ __launch_bounds__(256) void k_chain_par(ParArgs a) {
+  __shared__ uint32_t cand[kParThreads + 1][8];  // [0]: candidate of the block before the tile
+  __shared__ uint32_t has[kParThreads + 1];
+  __shared__ uint32_t first;  // (thread << 2) | flag of the tile's first flagged block
+  __shared__ uint64_t seq_hits;
+  const uint32_t tid = threadIdx.x;
+  const uint64_t maxp = a.x.mem[1], tmaxp = a.t.mem[1];
+  for (uint32_t c = blockIdx.x; c < a.in.n_chains; c += gridDim.x) {
+    const Range r = chain_range(a.in, c);
+    const uint64_t pos0 = a.in.first_block ? a.in.first_block[c] : 0;
+    uint64_t stop = r.n;
+    uint32_t kind = 0;
+    if (tid == 0) {
+      uint32_t p[8];
+      parent_words(p, a.in, c);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) cand[0][i] = p[i];
+      has[0] = 1;
+    }
+    for (uint64_t t0 = 0; t0 < r.n; t0 += kParThreads) {
+      const uint64_t k = t0 + tid;
+      const bool live = k < r.n;
+      const uint32_t* tok = a.in.tokens + r.t0 + k * a.in.bt;
+      if (tid == 0) first = 0xffffffffu;
+      uint32_t hc = 0;
+      if (live) {
+        uint32_t f[8];
+        fingerprint(f, a.in, pos0 + k, tok);
+        uint64_t fw[4];
+        key_words(fw, f);
+        const uint64_t h = probe_from(a.t, fw, tmaxp, 0);
+        if (h < a.n_handles) {
+          const uint32_t* hk = (const uint32_t*)(a.hkeys + 32 * h);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) cand[tid + 1][i] = __builtin_bswap32(hk[i]);
+          hc = 1;
+        }
+      }
+      has[tid + 1] = hc;
+      __syncthreads();
+      if (live && has[tid]) {
+        uint32_t prev[8], ck[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) prev[i] = cand[tid][i];
+        chain_key(ck, a.in, prev, tok);
+        store_key(a.keys, r.s0 + k, ck);
+        uint64_t kw[4];
+        key_words(kw, ck);
+        const uint64_t hv = probe_from(a.x, kw, maxp, 0);
+        a.handles[r.s0 + k] = hv;
+        bool same = hc != 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) same = same && cand[tid + 1][i] == ck[i];
+        const uint32_t flag = hv == kMiss ? 1u : (same ? 0u : 2u);
+        if (flag) atomicMin(&first, tid << 2 | flag);
+      }
+      // (a block without a candidate for its predecessor is never the first
+      // flagged one: that predecessor is flagged, in this tile or before)
+      __syncthreads();
+      const uint32_t f = first;
+      if (f != 0xffffffffu) {
+        stop = t0 + (f >> 2);
+        kind = f & 3;
+      }
+      if (stop != r.n) break;  // uniform: every thread read the same `first`
+      __syncthreads();
+      if (tid == 0) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) cand[0][i] = cand[kParThreads][i];
+        has[0] = has[kParThreads];
+      }
+      __syncthreads();
+    }
+    uint64_t n_hit = kind == 1 ? stop : r.n;
+    if (kind == 2) {
+      // block stop is a hit with a true key, but its candidate differs:
+      // continue the chain sequentially from stop + 1
+      if (tid == 0) {
+        const uint32_t l = (uint32_t)(stop % kParThreads);
+        uint32_t prev[8], cur[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) prev[i] = cand[l][i];
+        chain_key(cur, a.in, prev, a.in.tokens + r.t0 + stop * a.in.bt);
+        seq_hits = stop + 1 + seq_walk(a.in, a.x, false, r, stop + 1, cur, a.keys, a.handles);
+      }
+      __syncthreads();
+      n_hit = seq_hits;
+    }
+    for (uint64_t j = n_hit + tid; j < r.n; j += kParThreads) a.handles[r.s0 + j] = kMiss;
+    if (tid == 0) a.hits[c] = (uint32_t)n_hit;
+    __syncthreads();  // LDS is reused by the next chain
+  }
 }
 
 // ---- staging of tl_load's inputs --------------------------------------------
@@ -526,31 +714,38 @@ int launch_dindex_stats(const void* mem, void* stream, uint64_t* d_out) {
   return launched();
 }
 
+namespace {
+ChainIn chain_in(const tl_ctx* ctx, size_t n_chains, const tl_chains* ch) {
+  ChainIn in;
+  in.tokens = ch ? ch->d_tokens : nullptr;
+  in.n_tokens = ch ? ch->n_tokens : 0;
+  in.tok_off = ch ? ch->d_tok_off : nullptr;
+  in.slot_off = ch ? ch->d_slot_off : nullptr;
+  in.n_slots = ch ? ch->n_slots : 0;
+  in.parents = ch ? ch->d_parents : nullptr;
+  in.first_block = ch ? ch->d_first_block : nullptr;
+  in.n_chains = (uint32_t)n_chains;
+  in.bt = ctx->geo.block_tokens;
+  in.key = msg_len(8, in.bt);
+  in.fp = msg_len(10, in.bt);
+  for (int i = 0; i < 8; ++i)
+    in.ns[i] = (uint32_t)ctx->ns[4 * i] << 24 | (uint32_t)ctx->ns[4 * i + 1] << 16 |
+               (uint32_t)ctx->ns[4 * i + 2] << 8 | ctx->ns[4 * i + 3];
+  return in;
+}
+}  // namespace
+
 int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
                  const void* index_mem, uint64_t capacity, uint32_t flags, uint8_t* d_keys,
                  uint64_t* d_handles, uint32_t* d_hits) {
   hipStream_t s = (hipStream_t)stream;
   ChainArgs a;
-  a.tokens = ch->d_tokens;
-  a.n_tokens = ch->n_tokens;
-  a.tok_off = ch->d_tok_off;
-  a.slot_off = ch->d_slot_off;
-  a.n_slots = ch->n_slots;
-  a.parents = ch->d_parents;
-  a.n_chains = (uint32_t)n_chains;
-  a.bt = ctx->geo.block_tokens;
-  const uint64_t msg = 32ull + 4ull * a.bt;  // message bytes per key
-  a.nb = (uint32_t)((msg + 8) / 64 + 1);
-  a.len_hi = (uint32_t)((msg * 8) >> 32);
-  a.len_lo = (uint32_t)(msg * 8);
+  a.in = chain_in(ctx, n_chains, ch);
   // one chain per wavefront while chains fit the SIMDs, else share
   const uint64_t simds = 4ull * (uint64_t)sm_count();
   uint64_t lanes = (n_chains + simds - 1) / simds;
   a.lanes = (uint32_t)(lanes < 1 ? 1 : (lanes > 64 ? 64 : lanes));
   a.all_keys = (flags & TL_CHAIN_ALL_KEYS) ? 1 : 0;
-  for (int i = 0; i < 8; ++i)
-    a.ns[i] = (uint32_t)ctx->ns[4 * i] << 24 | (uint32_t)ctx->ns[4 * i + 1] << 16 |
-              (uint32_t)ctx->ns[4 * i + 2] << 8 | ctx->ns[4 * i + 3];
   a.x.mem = (uint64_t*)index_mem;
   a.x.mask = index_mem ? capacity - 1 : 0;
   a.keys = d_keys;
@@ -561,6 +756,47 @@ int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
   {
     TimedLaunch t(TL_KERNEL_CHAIN, stream);
     hipLaunchKernelGGL(k_chain, dim3(waves), dim3(64), 0, s, a);
+  }
+  return launched();
+}
+
+int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
+                     const void* index_mem, uint64_t capacity, const void* tok_mem,
+                     uint64_t tok_capacity, const uint8_t* d_handle_keys, uint64_t n_handles,
+                     uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits) {
+  hipStream_t s = (hipStream_t)stream;
+  ParArgs a;
+  a.in = chain_in(ctx, n_chains, ch);
+  a.x.mem = (uint64_t*)index_mem;
+  a.x.mask = capacity - 1;
+  a.t.mem = (uint64_t*)tok_mem;
+  a.t.mask = tok_capacity - 1;
+  a.hkeys = d_handle_keys;
+  a.n_handles = d_handle_keys ? n_handles : 0;
+  a.keys = d_keys;
+  a.handles = d_handles;
+  a.hits = d_hits;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_CHAIN, stream);
+    hipLaunchKernelGGL(k_chain_par, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(kParThreads), 0, s, a);
+  }
+  return launched();
+}
+
+int launch_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
+                        const uint64_t* d_pos, uint8_t* d_out) {
+  hipStream_t s = (hipStream_t)stream;
+  FpArgs a;
+  a.in = chain_in(ctx, 0, nullptr);
+  a.tokens = d_tokens;
+  a.pos = d_pos;
+  a.out = d_out;
+  a.n = (uint32_t)n;
+  (void)hipGetLastError();
+  {
+    TimedLaunch t(TL_KERNEL_INDEX, stream);
+    hipLaunchKernelGGL(k_fingerprint, dim3(grid_for(n, 256, 1u << 16)), dim3(256), 0, s, a);
   }
   return launched();
 }

@@ -438,6 +438,31 @@ int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_c
                           idx ? idx->capacity : 0, flags, d_keys, d_handles, d_hits);
 }
 
+int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
+                          const uint64_t* d_block_index, uint8_t* d_out) {
+  if (!ctx) return TL_EINVAL;
+  if (n == 0) return TL_OK;
+  if (n >= (size_t(1) << 31)) return TL_ERANGE;
+  if (!d_tokens || !d_block_index || !d_out) return TL_EINVAL;
+  if (((uintptr_t)d_tokens | (uintptr_t)d_out) & 3 || ((uintptr_t)d_block_index & 7)) return TL_EINVAL;
+  return tl::launch_fingerprints(ctx, stream, n, d_tokens, d_block_index, d_out);
+}
+
+int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
+                        const tl_dindex* idx, const tl_dindex* tok_idx, const uint8_t* d_handle_keys,
+                        uint64_t n_handles, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits) {
+  if (!ctx) return TL_EINVAL;
+  if (n_chains == 0) return TL_OK;
+  int r = check_chains(n_chains, chains);
+  if (r) return r;
+  if (!idx || !tok_idx || !d_hits || ((uintptr_t)d_hits & 3)) return TL_EINVAL;
+  if (n_handles && (!d_handle_keys || ((uintptr_t)d_handle_keys & 3))) return TL_EINVAL;
+  if (chains->n_slots && (!d_keys || !d_handles || ((uintptr_t)d_keys & 3) || ((uintptr_t)d_handles & 7)))
+    return TL_EINVAL;
+  return tl::launch_chain_par(ctx, stream, n_chains, chains, idx->mem, idx->capacity, tok_idx->mem,
+                              tok_idx->capacity, d_handle_keys, n_handles, d_keys, d_handles, d_hits);
+}
+
 int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
                    const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_handle_ptrs,
                    const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,

@@ -105,6 +105,8 @@ def _load():
         "tl_chain_lookup": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, c.c_uint32, P, P, P]),
         "tl_chain_stage": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, P, c.c_uint64, P, P,
                                      P, P, P, P]),
+        "tl_block_fingerprints": (c.c_int, [P, P, c.c_size_t, P, P, P]),
+        "tl_chain_lookup_par": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, c.c_uint64, P, P, P]),
         "tl_status_string": (c.c_char_p, [c.c_int]),
         "tl_verdict_string": (c.c_char_p, [c.c_int]),
         "tl_abi_version": (c.c_int, []),
@@ -126,6 +128,7 @@ EXPORTED = (
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
     "tl_dindex_bytes", "tl_dindex_create", "tl_dindex_destroy", "tl_dindex_workspace_bytes",
     "tl_dindex_put", "tl_dindex_get", "tl_dindex_stats", "tl_chain_lookup", "tl_chain_stage",
+    "tl_block_fingerprints", "tl_chain_lookup_par",
     "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
     "tl_timing_read")
 KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4, "chain": 5,
@@ -403,6 +406,18 @@ def tl_chain_lookup(ctx: Ctx, stream, n_chains: int, chains: tl_chains, index: O
     _check(_lib.tl_chain_lookup(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains),
                                 index.handle if index is not None else None, flags, _addr(d_keys),
                                 _addr(d_handles), _addr(d_hits)), "tl_chain_lookup")
+
+
+def tl_block_fingerprints(ctx: Ctx, stream, n: int, d_tokens, d_block_index, d_out):
+    _check(_lib.tl_block_fingerprints(ctx.handle, _stream(stream), n, _addr(d_tokens), _addr(d_block_index),
+                                      _addr(d_out)), "tl_block_fingerprints")
+
+
+def tl_chain_lookup_par(ctx: Ctx, stream, n_chains: int, chains: tl_chains, index: DeviceIndex,
+                        token_index: DeviceIndex, d_handle_keys, n_handles: int, d_keys, d_handles, d_hits):
+    _check(_lib.tl_chain_lookup_par(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains), index.handle,
+                                    token_index.handle, _addr(d_handle_keys), n_handles, _addr(d_keys),
+                                    _addr(d_handles), _addr(d_hits)), "tl_chain_lookup_par")
 
 
 def tl_chain_stage(ctx: Ctx, stream, n_chains: int, chains: tl_chains, d_hits, d_handles, d_handle_ptrs,

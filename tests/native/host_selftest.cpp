@@ -25,6 +25,11 @@ int launch_dindex_get(const void*, uint64_t, void*, size_t, const uint8_t*, uint
 int launch_dindex_stats(const void*, void*, uint64_t*) { return TL_EDEVICE; }
 int launch_chain(const tl_ctx*, void*, size_t, const tl_chains*, const void*, uint64_t, uint32_t, uint8_t*,
                  uint64_t*, uint32_t*) { return TL_EDEVICE; }
+int launch_chain_par(const tl_ctx*, void*, size_t, const tl_chains*, const void*, uint64_t, const void*,
+                     uint64_t, const uint8_t*, uint64_t, uint8_t*, uint64_t*, uint32_t*) { return TL_EDEVICE; }
+int launch_fingerprints(const tl_ctx*, void*, size_t, const uint32_t*, const uint64_t*, uint8_t*) {
+  return TL_EDEVICE;
+}
 int launch_stage(const tl_ctx*, void*, size_t, const tl_chains*, const uint32_t*, const uint64_t*,
                  const uint64_t*, const uint64_t*, uint64_t, uint64_t*, uint64_t*, uint64_t*, uint32_t*,
                  const int32_t*, int32_t*) { return TL_EDEVICE; }
@@ -166,6 +171,13 @@ int main() {
   tl_chains no_off = chn;
   no_off.d_slot_off = nullptr;
   EXPECT(tl_chain_lookup(c, nullptr, 2, &no_off, nullptr, 0, ck, nullptr, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, ck, dh, hits) == TL_EDEVICE);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, nullptr, ck, 2, ck, dh, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, nullptr, 2, ck, dh, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, ck, nullptr, hits) == TL_EINVAL);
+  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, dh, ck) == TL_EDEVICE);
+  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, nullptr, ck) == TL_EINVAL);
+  EXPECT(tl_block_fingerprints(c, nullptr, 0, nullptr, nullptr, nullptr) == TL_OK);
   uint64_t sp[2], sl[2], sb[2];
   EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EDEVICE);
   EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, nullptr, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);

@@ -448,3 +448,129 @@ def test_device_restore_in_a_graph_replays_with_new_requests():
         want = [ref.chain_walk(c.ns, ch.data(r), 4 * bt, index)[1] for r in range(ch.n)]
         assert list(got_h) == want, step
         log("replay", step, "hits", want)
+
+
+def fingerprints(ctx, toks2d, pos):
+    n = toks2d.shape[0]
+    out = torch.empty((max(n, 1), 32), dtype=torch.uint8, device=DEV)
+    T.tl_block_fingerprints(ctx, torch.cuda.current_stream(), n, i32(toks2d.view(np.int32)), i64(pos), out)
+    torch.cuda.synchronize()
+    return [out[b].cpu().numpy().tobytes() for b in range(n)]
+
+
+def test_fingerprints_follow_their_definition():
+    import hashlib
+    for pt, ppb in ((16, 1), (5, 1), (16, 3)):
+        ctx, ns, bt = ctx_bt(pt, ppb)
+        toks = wl.tokens(37 * bt, 80 + bt).reshape(37, bt)
+        pos = np.random.default_rng(bt).integers(0, 2**63, 37, dtype=np.uint64)
+        got = fingerprints(ctx, toks, pos)
+        for b in range(37):
+            assert got[b] == hashlib.sha256(ns + int(pos[b]).to_bytes(8, "little") + toks[b].tobytes()).digest()
+
+
+class TwoIndexes:
+    """Key index and token index over stored documents (handle = record id)."""
+
+    def __init__(self, ctx, ns, bt, docs, skip=(), token_skip=(), decoys=(), cap=4096):
+        self.keys, self.toks, self.pos = [], [], []
+        for d in list(docs) + list(decoys):
+            ks = ref.block_keys(ns, d.tobytes(), 4 * bt)
+            self.keys += ks
+            self.toks += [d[i * bt:(i + 1) * bt] for i in range(len(ks))]
+            self.pos += list(range(len(ks)))
+        n = len(self.keys)
+        keep = [i for i in range(n) if i not in set(skip)]
+        self.idx = new_index(cap)
+        assert (dput(self.idx, [self.keys[i] for i in keep], keep) == T.TL_INDEX_STORED).all()
+        self.index = ref.index_put({}, [self.keys[i] for i in keep], keep)
+        tkeep = [i for i in range(n) if i not in set(token_skip)]
+        fps = fingerprints(ctx, np.stack(self.toks), np.array(self.pos, np.uint64))
+        self.tidx = new_index(cap)
+        assert (dput(self.tidx, [fps[i] for i in tkeep], tkeep) == T.TL_INDEX_STORED).all()
+        self.d_hkeys = torch.from_numpy(np.frombuffer(b"".join(self.keys), np.uint8).reshape(n, 32).copy()).to(DEV)
+        self.n = n
+
+
+def par_lookup(ctx, ch, two):
+    S = max(ch.n_slots, 1)
+    keys = torch.full((S, 32), SENT, dtype=torch.uint8, device=DEV)
+    handles = torch.full((S,), 0x7777, dtype=torch.int64, device=DEV)
+    hits = torch.full((ch.n,), 0xFFFFFFF, dtype=torch.int32, device=DEV)
+    T.tl_chain_lookup_par(ctx, torch.cuda.current_stream(), ch.n, ch.tl, two.idx, two.tidx, two.d_hkeys, two.n,
+                          keys, handles, hits)
+    torch.cuda.synchronize()
+    return keys.cpu().numpy(), handles.cpu().numpy().view(np.uint64), hits.cpu().numpy()
+
+
+def check_walk(ch, ns, bt, index, keys, handles, hits, parents=None):
+    total = 0
+    for c in range(ch.n):
+        parent = ns if parents is None else parents[c]
+        want_keys, want_hits, want_h = ref.chain_walk(parent, ch.data(c), 4 * bt, index)
+        s0, nk = int(ch.slot_off[c]), len(want_keys)
+        assert hits[c] == want_hits, (c, hits[c], want_hits)
+        assert list(handles[s0:s0 + want_hits]) == want_h
+        assert (handles[s0 + want_hits:s0 + nk] == np.uint64(T.MISS)).all()
+        kept = min(want_hits + 1, nk)
+        assert [keys[s0 + k].tobytes() for k in range(kept)] == want_keys[:kept], c
+        total += want_hits
+    return total
+
+
+@pytest.mark.parametrize("case", ["complete", "token_holes", "decoys", "key_holes"])
+def test_parallel_walk_equals_the_oracle_walk(case):
+    ctx, ns, bt = ctx_bt(16)
+    docs, _ = stored_docs(ns, bt, 5, 600, 90)  # longer than a tile of 256 blocks
+    n_doc = 600
+    kw = {}
+    if case == "token_holes":
+        kw["token_skip"] = set(range(3, 5 * n_doc, 7))
+    if case == "key_holes":
+        kw["skip"] = {2 * n_doc + 300, 4 * n_doc + 255, 4 * n_doc + 256}
+    if case == "decoys":
+        # same tokens as doc 0 from block 1 on, after another first block: the
+        # decoy's fingerprints equal doc 0's and, put last, win the token index
+        dec = docs[0].copy()
+        dec[:bt] = wl.tokens(bt, 91)
+        dec2 = docs[1].copy()
+        dec2[300 * bt:301 * bt] ^= 1  # diverges at block 300, same tokens after it
+        kw["decoys"] = [dec, dec2]
+    two = TwoIndexes(ctx, ns, bt, docs, cap=8192, **kw)
+    reqs = requests_for(docs, bt, 60, 92)
+    ch = Chains(ctx, [r.size for r in reqs], 0, bt)
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    keys, handles, hits = par_lookup(ctx, ch, two)
+    total = check_walk(ch, ns, bt, two.index, keys, handles, hits)
+    # and the sequential walk agrees slot for slot where both are specified
+    k2, h2, hits2 = ch.lookup(ctx, two.idx)
+    assert np.array_equal(hits, hits2)
+    log(case, "hits", total, "of", ch.n_slots, "slots")
+    assert total > 3000
+
+
+def test_parallel_walk_with_parents_and_positions():
+    ctx, ns, bt = ctx_bt(16)
+    rng = np.random.default_rng(3)
+    par = rng.integers(0, 256, 32, dtype=np.uint8).tobytes()
+    doc = wl.tokens(300 * bt, 93)
+    keys = ref.block_keys(par, doc.tobytes(), 4 * bt)
+    # stored blocks sit at positions 1000.. (a continuation of an earlier prefix)
+    idx, tidx = new_index(1024), new_index(1024)
+    dput(idx, keys, range(300))
+    fps = fingerprints(ctx, doc.reshape(300, bt), np.arange(1000, 1300, dtype=np.uint64))
+    dput(tidx, fps, range(300))
+    d_hk = torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(300, 32).copy()).to(DEV)
+    reqs = [doc[:280 * bt + 5], doc[:10 * bt], doc.copy()]
+    ch = Chains(ctx, [r.size for r in reqs], 0, bt, parents=[par] * 3,
+                first_block=np.array([1000, 1000, 999], np.uint64))
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    two = type("Two", (), {"idx": idx, "tidx": tidx, "d_hkeys": d_hk, "n": 300})()
+    k, h, hits = par_lookup(ctx, ch, two)
+    index = ref.index_put({}, keys, range(300))
+    check_walk(ch, ns, bt, index, k, h, hits, parents=[par] * 3)
+    # the third chain's positions are off by one: no candidates, the walk
+    # still finds every block sequentially
+    assert list(hits) == [280, 10, 300]
