@@ -120,7 +120,40 @@ def multi_request_leg(T, PagedCache, wl, dev):
            "tokens_avoided_per_s": (blocks - rejected) * P / total, "per_batch": per}
     log("multi-request: %d batches, %d blocks (%d rejected) in %.1f ms, %.0f GB/s incl. keys+lookup %.1f ms"
         % (len(batches), blocks, rejected, total * 1e3, out["GBps"], host_s * 1e3))
-    del pool, store, pipe
+    # the same store and pool through the device pipeline: token ids already in
+    # HBM, keys and lookup by the verified parallel walk, no host step per batch
+    dstore = pipeline.DeviceStore(ctx, n_st, dev, records=store.records)
+    store.records.lens.copy_(torch.from_numpy(store.lens.view(np.int64)).to(dev))
+    dstore.add(torch.from_numpy(keys).to(dev), torch.from_numpy(toks.view(np.int32).copy()).to(dev),
+               torch.from_numpy(np.tile(np.arange(bpd, dtype=np.int64), len(w.base_docs))).to(dev),
+               torch.arange(n_st, dtype=torch.int64, device=dev))
+    dpipe = pipeline.DeviceRestorePipeline(dstore, pool)
+    dbatches = wl.admission_batches(w.requests, pool_pages, whole_prompts=True)
+    d_toks = [torch.from_numpy(np.concatenate([w.requests[r].tokens for r in reqs]).view(np.int32)).to(dev)
+              for reqs in dbatches]
+    d_lens = [[w.requests[r].tokens.size for r in reqs] for reqs in dbatches]
+    dpipe.restore(d_toks[0][:d_lens[0][0]], d_lens[0][:1])  # warm-up
+    torch.cuda.synchronize()
+    T.tl_timing(True)
+    for k in ("chain", "stage", "load_init", "load_main", "load_final"):
+        T.tl_timing_read(k)
+    t0 = time.perf_counter()
+    dres = [dpipe.restore(d_toks[i], d_lens[i]) for i in range(len(dbatches))]
+    torch.cuda.synchronize()
+    dtotal = time.perf_counter() - t0
+    kms = {k: T.tl_timing_read(k)[0] for k in ("chain", "stage", "load_init", "load_main", "load_final")}
+    T.tl_timing(False)
+    d_hits = sum(int(r.hits.sum().item()) for r in dres)
+    d_rej = sum(int(((r.verdicts != T.ACCEPT) & (r.verdicts != T.MISSING)).sum().item()) for r in dres)
+    assert d_hits == blocks and d_rej == rejected, (d_hits, blocks, d_rej, rejected)
+    out["device_path"] = {
+        "batches": len(dbatches), "blocks_restored": d_hits, "blocks_rejected": d_rej, "ms": dtotal * 1e3,
+        "GBps": moved / dtotal / 1e9, "tokens_avoided_per_s": (d_hits - d_rej) * P / dtotal,
+        "keys_lookup_ms": kms["chain"], "stage_ms": kms["stage"],
+        "load_ms": kms["load_init"] + kms["load_main"] + kms["load_final"]}
+    log("multi-request, device path: %d batches in %.1f ms, %.0f GB/s; keys+lookup %.3f ms, staging %.3f ms"
+        % (len(dbatches), dtotal * 1e3, moved / dtotal / 1e9, kms["chain"], kms["stage"]))
+    del pool, store, pipe, dstore, dpipe, dres, d_toks
     torch.cuda.empty_cache()
     return out
 

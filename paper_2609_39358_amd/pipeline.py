@@ -96,3 +96,108 @@ class RestorePipeline:
                   self.pool.tl(), verd, self.ws, self.ws_bytes)
         res._keep = (d_ptrs, d_lens, d_keys, d_pos, d_tok, d_tab)
         return res
+
+
+def _pow2_at_least(n: int) -> int:
+    c = 2
+    while c < n:
+        c *= 2
+    return c
+
+
+class DeviceStore:
+    """Records in HBM with a device key index and a device token index (both
+    map to the record's slot) and each slot's key, so that a restore of
+    device-resident requests needs no host step (Sec. 2.2)."""
+
+    def __init__(self, ctx: T.Ctx, capacity: int, device="cuda", stream=None,
+                 records: RecordStore = None):
+        self.ctx, self.capacity = ctx, capacity
+        self.records = records if records is not None else RecordStore(capacity, ctx.record_bytes, device)
+        cap = _pow2_at_least(2 * capacity)  # load factor <= 1/2
+        stream = stream or torch.cuda.current_stream()
+        self._kmem = torch.empty(T.tl_dindex_bytes(cap), dtype=torch.uint8, device=device)
+        self._tmem = torch.empty(T.tl_dindex_bytes(cap), dtype=torch.uint8, device=device)
+        self.key_index = T.DeviceIndex(self._kmem, cap, stream)
+        self.token_index = T.DeviceIndex(self._tmem, cap, stream)
+        self.slot_keys = torch.zeros((capacity, 32), dtype=torch.uint8, device=device)
+        self.device = device
+
+    @property
+    def lens(self) -> torch.Tensor:
+        return self.records.lens
+
+    def add(self, d_keys: torch.Tensor, d_tokens: torch.Tensor, d_positions: torch.Tensor,
+            d_slots: torch.Tensor, stream=None):
+        """Index n saved blocks: keys [n][32] u8, tokens [n][block tokens] i32,
+        positions [n] i64, slots [n] i64 (all device)."""
+        stream = stream or torch.cuda.current_stream()
+        n = d_keys.shape[0]
+        if n == 0:
+            return
+        self.slot_keys.index_copy_(0, d_slots, d_keys)
+        fps = torch.empty((n, 32), dtype=torch.uint8, device=self.device)
+        T.tl_block_fingerprints(self.ctx, stream, n, d_tokens, d_positions, fps)
+        wsb = T.tl_dindex_workspace_bytes(n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
+        st = torch.empty(n, dtype=torch.uint8, device=self.device)
+        for idx, k in ((self.key_index, d_keys), (self.token_index, fps)):
+            idx.put(stream, n, k, d_slots, st, ws, wsb)
+            if not bool((st == T.TL_INDEX_STORED).all()):
+                raise RuntimeError("device index refused keys (full or tag clash)")
+
+
+@dataclass
+class DeviceBatch:
+    n_slots: int
+    hits: torch.Tensor       # [n_chains] leading blocks found (device)
+    verdicts: torch.Tensor   # [n_slots] (device); TL_MISSING for slots that are not hits
+    slot_off: np.ndarray     # [n_chains + 1] host copy
+
+
+class DeviceRestorePipeline:
+    """Restores a batch of device-resident requests into pool pages: slot q
+    (block k of request c at slot_off[c] + k) owns pages q*ppb .. q*ppb+ppb-1
+    of the pool, the layout of an engine that allocates pages for whole
+    prompts. One verified parallel key walk, one staging kernel and one
+    tl_load, all on `stream` with no host synchronisation."""
+
+    def __init__(self, store: DeviceStore, pool: PagedCache, stream=None):
+        self.store, self.pool = store, pool
+        self.ctx = store.ctx
+        self.stream = stream or torch.cuda.current_stream()
+        self.bt = self.ctx.block_bytes // 4
+
+    def restore(self, d_tokens: torch.Tensor, lengths: Sequence[int], d_first_block=None) -> DeviceBatch:
+        dev, s, ctx, bt = self.pool.k[0].device, self.stream, self.ctx, self.bt
+        lengths = [int(x) for x in lengths]
+        tok_off = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+        slot_off = np.concatenate([[0], np.cumsum([L // bt for L in lengths])]).astype(np.int64)
+        n, S = len(lengths), int(slot_off[-1])
+        if S * ctx.pages_per_block > self.pool.n_pages:
+            raise ValueError("batch needs %d pages, pool has %d" % (S * ctx.pages_per_block, self.pool.n_pages))
+        d_toff = torch.from_numpy(tok_off).to(dev, non_blocking=True)
+        d_soff = torch.from_numpy(slot_off).to(dev, non_blocking=True)
+        chains = T.make_chains(d_tokens, int(tok_off[-1]), d_toff, d_soff, S, None, d_first_block)
+        hits = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+        verd = torch.empty(max(S, 1), dtype=torch.uint8, device=dev)
+        out = DeviceBatch(S, hits[:n], verd[:S], slot_off)
+        if n == 0:
+            return out
+        Sx = max(S, 1)
+        keys = torch.empty((Sx, 32), dtype=torch.uint8, device=dev)
+        handles = torch.empty(Sx, dtype=torch.int64, device=dev)
+        ptrs, lens, bidx = (torch.empty(Sx, dtype=torch.int64, device=dev) for _ in range(3))
+        toks = torch.empty((Sx, bt), dtype=torch.int32, device=dev)
+        tab = torch.empty((ctx.n_groups, Sx * ctx.pages_per_block), dtype=torch.int32, device=dev)
+        st = self.store
+        T.tl_chain_lookup_par(ctx, s, n, chains, st.key_index, st.token_index, st.slot_keys, st.capacity, keys,
+                              handles, hits)
+        T.tl_chain_stage(ctx, s, n, chains, hits, handles, st.records.ptrs, st.records.lens, st.capacity, ptrs,
+                         lens, bidx, toks, None, tab)
+        if S:
+            ws_b = T.tl_workspace_bytes(ctx, S)
+            ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
+            T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab), self.pool.tl(), verd, ws, ws_b)
+            out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, tab, ws)
+        return out

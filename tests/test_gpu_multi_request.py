@@ -78,3 +78,102 @@ def test_multi_request_full_size():
     assert seen["blocks"] == total_shared
     log("restored %d blocks in %d batches, %d rejected" % (seen["blocks"], len(batches), seen["rejected"]))
     assert seen["rejected"] > 0
+
+
+def device_run(run):
+    """The same stored records, indexed on the device, restored by the device
+    pipeline (verified parallel key walk, staging, tl_load; no host step)."""
+    import torch
+
+    from paper_2609_39358_amd import pipeline
+    from tests.gpu_case import DEV, i32, i64
+    st = pipeline.DeviceStore(run.ctx, run.n_stored, DEV, records=run.store)
+    run.store.lens.copy_(torch.from_numpy(run.lens.view(np.int64)).to(DEV))  # the truncations
+    st.add(torch.from_numpy(run.keys).to(DEV), i32(run.tokens.view(np.int32)), i64(run.bidx),
+           torch.arange(run.n_stored, dtype=torch.int64, device=DEV))
+    return pipeline.DeviceRestorePipeline(st, run.dst)
+
+
+def device_batches(run, pipe, check):
+    import torch
+
+    from tests.gpu_case import DEV
+    from tests.multi_request import Batch
+    w, P = run.w, run.g.page_tokens
+    out = []
+    for bi, reqs in enumerate(wl.admission_batches(w.requests, run.pool_pages, whole_prompts=True)):
+        for t in run.dst.k + run.dst.v:
+            t.fill_(0x5D)
+        toks = np.concatenate([w.requests[r].tokens for r in reqs])
+        d_tok = torch.from_numpy(toks.view(np.int32)).to(DEV)
+        res = pipe.restore(d_tok, [w.requests[r].tokens.size for r in reqs])
+        torch.cuda.synchronize()
+        hits = res.hits.cpu().numpy()
+        verd = res.verdicts.cpu().numpy()
+        assert list(hits) == [w.requests[r].shared_blocks for r in reqs]
+        b = Batch(list(reqs))
+        for c, r in enumerate(reqs):
+            s0 = int(res.slot_off[c])
+            q = w.requests[r]
+            for k in range(q.full_blocks):
+                if k < hits[c]:
+                    b.blocks.append((r, k, q.base * run.bpd + k, s0 + k))
+                else:
+                    assert verd[s0 + k] == ref.MISSING
+        b.verdicts = np.array([verd[blk[3]] for blk in b.blocks], np.uint8)
+        log("device batch %d: %d requests, %d slots, %d restored" % (bi, len(reqs), res.n_slots, len(b.blocks)))
+        check(b, res)
+        out.append(b)
+    return out
+
+
+def test_device_pipeline_reduced_full_oracle():
+    geom = wl.Geometry(2, 2, 64, 16)
+    w = wl.multi_request(n_requests=16, n_base=3, base_tokens=512, median=200, lo=40, hi=512,
+                         corrupt_frac=0.10, geom=geom, seed=21)
+    run = MultiRun(w, pool_pages=96, seed=21)
+    pipe = device_run(run)
+    slab = run.lay.slab_bytes
+
+    def check(b, res):
+        # every slot's pages as the oracle restores the batch: hits get the
+        # record (or zeros if rejected), other slots keep their bytes
+        hk = [np.full((run.pool_pages, run.dst.page_stride), 0x5D, np.uint8) for _ in range(geom.n_layers)]
+        hv = [x.copy() for x in hk]
+        recs, keys, bidx, toks, pages = [], [], [], [], []
+        for r, i, rid, page in b.blocks:
+            recs.append(run.store.buf[rid].cpu().numpy().tobytes()[:int(run.lens[rid])])
+            q = w.requests[r]
+            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * 16].tobytes(), 64)[i])
+            bidx.append(i)
+            toks.append(q.tokens[i * 16:(i + 1) * 16])
+            pages.append(page)
+        vo = ref.restore(run.lay, run.ns, recs, keys, bidx, toks, np.array(pages)[None, :], hk, hv)
+        assert [int(x) for x in b.verdicts] == vo
+        for l in range(geom.n_layers):
+            assert np.array_equal(run.dst.k[l].cpu().numpy(), hk[l])
+            assert np.array_equal(run.dst.v[l].cpu().numpy(), hv[l])
+
+    batches = device_batches(run, pipe, check)
+    assert len(batches) >= 2 and sum(int((b.verdicts != ref.ACCEPT).sum()) for b in batches) > 0
+
+
+def test_device_pipeline_full_size():
+    w = wl.multi_request(seed=3)
+    run = MultiRun(w, pool_pages=32768, seed=3)
+    damaged = {r for r, _ in w.corrupt_flip} | {r for r, _ in w.corrupt_trunc}
+    want = {rid: run.oracle_verdict(rid) for rid in sorted(damaged)}
+    pipe = device_run(run)
+    seen = {"blocks": 0, "rejected": 0}
+
+    def check(b, res):
+        for (req, pos, rid, page), v in zip(b.blocks, b.verdicts):
+            assert int(v) == want.get(rid, ref.ACCEPT), (req, pos, rid)
+        run.check_pages(b, damaged)
+        seen["blocks"] += len(b.blocks)
+        seen["rejected"] += int((b.verdicts != ref.ACCEPT).sum())
+
+    batches = device_batches(run, pipe, check)
+    assert seen["blocks"] == sum(q.shared_blocks for q in w.requests)
+    log("device pipeline: %d blocks in %d batches, %d rejected" % (seen["blocks"], len(batches), seen["rejected"]))
+    assert seen["rejected"] > 0

@@ -179,6 +179,7 @@ class Request:
     n_tokens: int
     shared_blocks: int  # leading full blocks identical to the base document
     tokens: np.ndarray = field(repr=False, default=None)
+    full_blocks: int = 0  # full blocks of the prompt
 
 
 @dataclass
@@ -211,7 +212,7 @@ def multi_request(n_requests=256, n_base=8, base_tokens=32768, median=4096, sigm
         sh = min(int(np.floor(fracs[i] * full)), base_tokens // P)
         fresh = tokens(n - sh * P, seed, 1000 + i)
         toks = np.concatenate([base_docs[bases[i]][: sh * P], fresh]).astype("<u4")
-        reqs.append(Request(int(bases[i]), n, sh, toks))
+        reqs.append(Request(int(bases[i]), n, sh, toks, full))
     n_stored = n_base * (base_tokens // P)
     n_bad = int(np.floor(corrupt_frac * n_stored))
     rc = rng(seed, 5)
@@ -236,12 +237,12 @@ def scale_len(frac: float, record_len: int) -> int:
     return min(int(frac * record_len), record_len - 1)
 
 
-def admission_batches(reqs: Sequence[Request], pages_per_batch: int) -> List[List[int]]:
-    """Greedy admission order: consecutive requests whose shared blocks fit one
-    destination page pool."""
+def admission_batches(reqs: Sequence[Request], pages_per_batch: int, whole_prompts: bool = False) -> List[List[int]]:
+    """Greedy admission order: consecutive requests whose shared blocks (or,
+    with whole_prompts, all full blocks) fit one destination page pool."""
     batches, cur, used = [], [], 0
     for i, q in enumerate(reqs):
-        need = q.shared_blocks
+        need = q.full_blocks if whole_prompts else q.shared_blocks
         if cur and used + need > pages_per_batch:
             batches.append(cur)
             cur, used = [], 0
