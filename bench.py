@@ -158,6 +158,88 @@ def multi_request_leg(T, PagedCache, wl, dev):
     return out
 
 
+def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
+    """Save and restore of the other workloads (tiny, mid, hybrid) in the same
+    library calls. Load bytes count what the load must move: every block's
+    metadata and the slabs its tables restore (read, then written), so the
+    hybrid workload's sliding-window layers count only for the 4 window
+    pages. The tiny workload fits in the 256 MB last-level cache and the mid
+    one is dominated by launch and tail latency; only the hybrid figure is
+    an HBM roofline fraction."""
+    import numpy as np
+    import torch
+
+    out = {}
+    stream = torch.cuda.current_stream()
+    for ci in (0, 1, 4):
+        cfg = wl.CONFIGS[ci]
+        g = cfg.geom
+        P = g.page_tokens
+        n = cfg.n_tokens // P
+        tokens = wl.tokens(cfg.n_tokens, cfg.seed)
+        ctx = T.tl_ctx_create(b"bench-tenant", b"model-%d" % ci, g.n_layers, g.n_kv_heads, g.head_dim, g.dtype,
+                              P, list(g.layer_window) or None, list(g.layer_group) or None)
+        rb, slab = ctx.record_bytes, ctx.slab_bytes
+        src = PagedCache(g.n_layers, cfg.src_pages, slab, dev)
+        for l in range(g.n_layers):
+            for kv, t in ((0, src.k[l]), (1, src.v[l])):
+                t.copy_(wl.kv_layer_torch(cfg.src_pages, g, cfg.seed, l, kv, dev).view(torch.uint8)
+                        .reshape(cfg.src_pages, -1))
+        keys = torch.from_numpy(T.tl_block_keys(ctx, tokens)).to(dev)
+        bidx = torch.arange(n, dtype=torch.int64, device=dev)
+        toks = torch.from_numpy(tokens[:n * P].view(np.int32).reshape(n, P).copy()).to(dev)
+        t_src = np.tile(wl.page_table(n, cfg.src_pages, cfg.seed, 0), (g.n_groups, 1))
+        t_dst1 = wl.page_table(n, cfg.dst_pages, cfg.seed, 1)
+        t_dst = wl.hybrid_tables(cfg, t_dst1) if g.n_groups > 1 else t_dst1[None, :]
+        store = RecordStore(n, rb, dev)
+        sblk = T.make_blocks(keys, bidx, toks, torch.from_numpy(np.ascontiguousarray(t_src)).to(dev))
+        st = torch.zeros(n, dtype=torch.uint8, device=dev)
+
+        def timed(f):
+            f()
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                f()
+                torch.cuda.synchronize()
+                ts.append(time.perf_counter() - t0)
+            return sorted(ts)[len(ts) // 2] * 1e3
+
+        save_ms = timed(lambda: T.tl_save(ctx, stream, n, src.tl(), sblk, store.ptrs, st))
+        assert (st == T.ACCEPT).all().item()
+        del src, sblk
+        torch.cuda.empty_cache()
+        dst = PagedCache(g.n_layers, cfg.dst_pages, slab, dev)
+        lblk = T.make_blocks(keys, bidx, toks, torch.from_numpy(np.ascontiguousarray(t_dst)).to(dev))
+        wsb = T.tl_workspace_bytes(ctx, n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        verd = torch.zeros(n, dtype=torch.uint8, device=dev)
+        T.tl_timing(True)
+        load_ms = timed(lambda: T.tl_load(ctx, stream, n, store.ptrs, store.lens, lblk, dst.tl(), verd, ws, wsb))
+        main_ms, cnt = T.tl_timing_read("load_main")
+        for k in T.KERNELS:
+            T.tl_timing_read(k)
+        T.tl_timing(False)
+        assert (verd == T.ACCEPT).all().item()
+        groups = [g.group(l) for l in range(g.n_layers)]
+        slabs_read = sum(2 * sum(1 for l in range(g.n_layers) if t_dst[groups[l]][b] >= 0) for b in range(n))
+        load_bytes = n * ctx.payload_offset + 2 * slabs_read * slab
+        save_bytes = n * (rb + ctx.n_slabs * slab)
+        out[cfg.name] = {
+            "blocks": n, "record_bytes": rb, "slabs_restored": slabs_read, "load_bytes": load_bytes,
+            "load_ms": load_ms, "load_GBps": load_bytes / (load_ms * 1e-3) / 1e9,
+            "load_main_ms": main_ms / max(cnt, 1), "save_ms": save_ms,
+            "save_GBps": save_bytes / (save_ms * 1e-3) / 1e9}
+        if ci == 4:
+            out[cfg.name]["hbm_frac"] = out[cfg.name]["load_GBps"] / HBM_PEAK_GBPS
+        log("%s: save %.3f ms (%.0f GB/s), load %.3f ms for %.2f GB (%.0f GB/s)"
+            % (cfg.name, save_ms, out[cfg.name]["save_GBps"], load_ms, load_bytes / 1e9, out[cfg.name]["load_GBps"]))
+        del store, dst, lblk, ws
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -170,6 +252,7 @@ def main():
     ap.add_argument("--no-host-tier", action="store_true")
     ap.add_argument("--no-paper-blocks", action="store_true")
     ap.add_argument("--no-multi-request", action="store_true")
+    ap.add_argument("--no-other-configs", action="store_true")
     ap.add_argument("--host-tier-blocks", type=int, default=1024)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -459,13 +542,18 @@ def main():
         log("cpu oracle: %.2f GB/s over %.1f s" % (cpu["value"], cdt))
 
     # ---- multi-request reuse: keys + lookup + verified restore per admission batch
+    del store, dst, ws, verd, stage  # the corpus legs are done
+    idx.close()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     mr = None
     if not args.no_multi_request:
-        del store, dst, ws, verd, stage
-        idx.close()
-        torch.cuda.synchronize()
-        torch.cuda.empty_cache()
         mr = multi_request_leg(T, PagedCache, wl, dev)
+
+    # ---- the other workloads (tiny, mid, hybrid)
+    others = None
+    if not args.no_other_configs:
+        others = other_configs_leg(T, PagedCache, RecordStore, wl, dev)
 
     out = {
         "metric": METRIC, "value": gbps, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
@@ -486,6 +574,7 @@ def main():
         "host_tier": host_tier,
         "paper_blocks": pb,
         "multi_request": mr,
+        "other_configs": others,
         "copy_ceiling": copy,
         "kernel_source_sha256_16": kernel_source_hash(),
     }
