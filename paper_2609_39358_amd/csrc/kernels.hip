@@ -59,10 +59,17 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 #define TL_SEG_WAVES 4      // wavefronts per workgroup in the save chunk kernel
 #endif
 #ifndef TL_BATCH_ROWS
-#define TL_BATCH_ROWS 8     // rows each lane has in flight per batch
+#define TL_BATCH_ROWS 16    // load: rows each lane has in flight per batch
 #endif
 #ifndef TL_PREFETCH
-#define TL_PREFETCH 1       // load the next batch before hashing this one
+#define TL_PREFETCH 1       // load: fetch the next batch before hashing this one
+#endif
+#ifndef TL_SAVE_BATCH_ROWS
+#define TL_SAVE_BATCH_ROWS 64  // save: rows per batch; a whole 64 KiB chunk of a scattered
+                               // page in flight at once
+#endif
+#ifndef TL_SAVE_PREFETCH
+#define TL_SAVE_PREFETCH 0
 #endif
 #ifndef TL_NT_LOAD
 #define TL_NT_LOAD 1        // non-temporal (streaming) loads of the source
@@ -296,13 +303,29 @@ __device__ __forceinline__ void store_hash_batch(const v4u (&x)[B], gv4u* d, uin
   for (int i = 0; i < B; i += 2) c.stripe(x[i], x[i + 1]);
 }
 
+// Rows left after the main batches: one batch of each halved size that fits
+// (a chunk has at most 64 rows, so each size runs at most once).
+template <int B>
+__device__ __forceinline__ void tail_batches(const gv4u* s, gv4u* d, uint32_t rows, uint32_t& r,
+                                             Column& c) {
+  if constexpr (B >= 2) {
+    if (rows - r >= B) {
+      v4u x[B];
+      load_batch<B>(x, s, r);
+      store_hash_batch<B>(x, d, r, c);
+      r += B;
+    }
+    tail_batches<B / 2>(s, d, rows, r, c);
+  }
+}
+
 // Copy `rows` rows of 1 KiB from src to dst and return this lane's column
 // digest (seed = lane). Lane j moves granule j of every row. Rows go in
-// batches of B; with prefetching, the next batch's loads are in flight while
-// the current batch is stored and hashed.
+// batches of B; with prefetching (PF), the next batch's loads are in flight
+// while the current batch is stored and hashed.
+template <int B, int PF>
 __device__ __forceinline__ uint64_t copy_hash(const char* src, char* dst, uint32_t rows,
                                               uint32_t lane) {
-  constexpr int B = TL_BATCH_ROWS;
   static_assert(B % 2 == 0, "batches hold whole stripes");
   const gv4u* s = (const gv4u*)src + lane;
   gv4u* d = (gv4u*)dst + lane;
@@ -310,28 +333,29 @@ __device__ __forceinline__ uint64_t copy_hash(const char* src, char* dst, uint32
   c.init(lane);
   const uint32_t full = rows / B * B;
   uint32_t r = 0;
-#if TL_PREFETCH
-  if (full) {
-    v4u x[B], y[B];
-    load_batch<B>(x, s, 0);
-    for (r = 0; r < full; r += 2 * B) {
-      // x holds rows [r, r+B); rows [r+B, r+2B) arrive in y meanwhile
-      const bool has_y = r + B < full;
-      if (has_y) load_batch<B>(y, s, r + B);
-      store_hash_batch<B>(x, d, r, c);
-      if (!has_y) break;
-      if (r + 2 * B < full) load_batch<B>(x, s, r + 2 * B);
-      store_hash_batch<B>(y, d, r + B, c);
+  if constexpr (PF) {
+    if (full) {
+      v4u x[B], y[B];
+      load_batch<B>(x, s, 0);
+      for (r = 0; r < full; r += 2 * B) {
+        // x holds rows [r, r+B); rows [r+B, r+2B) arrive in y meanwhile
+        const bool has_y = r + B < full;
+        if (has_y) load_batch<B>(y, s, r + B);
+        store_hash_batch<B>(x, d, r, c);
+        if (!has_y) break;
+        if (r + 2 * B < full) load_batch<B>(x, s, r + 2 * B);
+        store_hash_batch<B>(y, d, r + B, c);
+      }
+      r = full;
     }
-    r = full;
+  } else {
+    for (; r < full; r += B) {
+      v4u x[B];
+      load_batch<B>(x, s, r);
+      store_hash_batch<B>(x, d, r, c);
+    }
   }
-#else
-  for (; r < full; r += B) {
-    v4u x[B];
-    load_batch<B>(x, s, r);
-    store_hash_batch<B>(x, d, r, c);
-  }
-#endif
+  tail_batches<B / 2>(s, d, rows, r, c);
   for (; r + 2 <= rows; r += 2) {
     const v4u x0 = ld16(s + (uint64_t)r * 64), x1 = ld16(s + (uint64_t)(r + 1) * 64);
     st16(d + (uint64_t)r * 64, x0);
@@ -381,7 +405,8 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
       zero_rows(out, it.rows, lane);  // k_save_meta zeroes the metadata
       continue;
     }
-    const uint64_t leaf = copy_hash(page_chunk(a, it), out, it.rows, lane);
+    const uint64_t leaf =
+        copy_hash<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(page_chunk(a, it), out, it.rows, lane);
     const uint64_t digest = wave_sum64(leaf);
     if (lane == 0) *(uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t) = digest;
   }
@@ -571,7 +596,8 @@ __device__ __forceinline__ void load_chunk_item(const SegArgs& a, uint32_t w, ui
   if (!page_in_range(it.page, a.n_pages)) return;  // -1: not restored; else BADARG
   const uint64_t rec = a.rec[it.b];
   if (rec == 0 || (rec & 15) || a.len[it.b] != a.g.record_bytes) return;
-  const uint64_t leaf = copy_hash(record_chunk(a, rec, it), page_chunk(a, it), it.rows, lane);
+  const uint64_t leaf = copy_hash<TL_BATCH_ROWS, TL_PREFETCH>(record_chunk(a, rec, it), page_chunk(a, it),
+                                                              it.rows, lane);
   const uint64_t digest = wave_sum64(leaf);
   if (lane == 0) {
     const uint64_t want = *(const uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t);
