@@ -442,8 +442,6 @@ __global__ __launch_bounds__(256) void k_fingerprint(FpArgs a) {
   }
 }
 
-constexpr uint32_t kParThreads = 256;
-
 struct ParArgs {
   ChainIn in;
   Dx x;                  // key index
@@ -455,7 +453,8 @@ struct ParArgs {
   uint32_t* hits;
 };
 
-// One workgroup per chain, kParThreads blocks per tile. For block k the
+// One workgroup per chain, kParThreads blocks per tile (1024 while chains
+// are few enough to leave CUs idle, else 256). For block k the
 // token index proposes cand_k, the key a stored block with the same tokens at
 // the same position has; every block then computes c_k = SHA-256(cand_{k-1} |
 // tokens_k) (cand_{-1} = the chain's parent) and looks c_k up in the key
@@ -465,7 +464,8 @@ struct ParArgs {
 // (reuse ends at m) or cand_m != c_m (c_m is true and a hit, but c_{m+1} is
 // not known: the chain goes on sequentially from m+1). Results equal the
 // sequential walk's; candidates only decide how much of it runs in parallel.
-__global__ __launch_bounds__(256) void k_chain_par(ParArgs a) {
+template <uint32_t kParThreads>
+__global__ __launch_bounds__(kParThreads) void k_chain_par(ParArgs a) {
   __shared__ uint32_t cand[kParThreads + 1][8];  // [0]: candidate of the block before the tile
   __shared__ uint32_t has[kParThreads + 1];
   __shared__ uint32_t first;  // (thread << 2) | flag of the tile's first flagged block
@@ -779,7 +779,9 @@ int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_
   (void)hipGetLastError();
   {
     TimedLaunch t(TL_KERNEL_CHAIN, stream);
-    hipLaunchKernelGGL(k_chain_par, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(kParThreads), 0, s, a);
+    const dim3 grid(grid_for(n_chains, 1, 1u << 16));
+    if (n_chains <= (size_t)sm_count() * 4) hipLaunchKernelGGL(k_chain_par<1024>, grid, dim3(1024), 0, s, a);
+    else hipLaunchKernelGGL(k_chain_par<256>, grid, dim3(256), 0, s, a);
   }
   return launched();
 }

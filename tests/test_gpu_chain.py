@@ -521,8 +521,8 @@ def check_walk(ch, ns, bt, index, keys, handles, hits, parents=None):
 @pytest.mark.parametrize("case", ["complete", "token_holes", "decoys", "key_holes"])
 def test_parallel_walk_equals_the_oracle_walk(case):
     ctx, ns, bt = ctx_bt(16)
-    docs, _ = stored_docs(ns, bt, 5, 600, 90)  # longer than a tile of 256 blocks
-    n_doc = 600
+    n_doc = 1300  # longer than a tile (1,024 blocks while chains are few)
+    docs, _ = stored_docs(ns, bt, 5, n_doc, 90)
     kw = {}
     if case == "token_holes":
         kw["token_skip"] = set(range(3, 5 * n_doc, 7))
@@ -534,9 +534,9 @@ def test_parallel_walk_equals_the_oracle_walk(case):
         dec = docs[0].copy()
         dec[:bt] = wl.tokens(bt, 91)
         dec2 = docs[1].copy()
-        dec2[300 * bt:301 * bt] ^= 1  # diverges at block 300, same tokens after it
+        dec2[1100 * bt:1101 * bt] ^= 1  # diverges at block 1100, same tokens after it
         kw["decoys"] = [dec, dec2]
-    two = TwoIndexes(ctx, ns, bt, docs, cap=8192, **kw)
+    two = TwoIndexes(ctx, ns, bt, docs, cap=16384, **kw)
     reqs = requests_for(docs, bt, 60, 92)
     ch = Chains(ctx, [r.size for r in reqs], 0, bt)
     ch.tokens[:] = np.concatenate(reqs)
@@ -574,3 +574,17 @@ def test_parallel_walk_with_parents_and_positions():
     # the third chain's positions are off by one: no candidates, the walk
     # still finds every block sequentially
     assert list(hits) == [280, 10, 300]
+
+
+def test_parallel_walk_many_chains():
+    """More chains than four per CU: 256-block tiles, chains of several tiles."""
+    ctx, ns, bt = ctx_bt(16)
+    docs, _ = stored_docs(ns, bt, 4, 700, 95)
+    two = TwoIndexes(ctx, ns, bt, docs, cap=8192, token_skip=set(range(5, 2800, 97)))
+    reqs = requests_for(docs, bt, 1100, 96)
+    ch = Chains(ctx, [r.size for r in reqs], 0, bt)
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    keys, handles, hits = par_lookup(ctx, ch, two)
+    total = check_walk(ch, ns, bt, two.index, keys, handles, hits)
+    assert max(hits) > 600 and total > 100000
