@@ -158,6 +158,37 @@ def multi_request_leg(T, PagedCache, wl, dev):
     return out
 
 
+def _oracle_slice(task):
+    """One worker of the multi-core CPU baseline: the oracle's verify+restore
+    of records [lo, hi) of the sample held in shared memory. Runs in a process
+    forked before the parent touched the GPU; uses no GPU."""
+    from multiprocessing import shared_memory
+
+    import numpy as np
+
+    from oracle import taliesin_ref as ref
+
+    shm_name, lo, hi, rb, lay_args, ns, keys, toks = task
+    shm = shared_memory.SharedMemory(name=shm_name)
+    # the parent owns the segment and unlinks it; keep this process's resource
+    # tracker from trying to remove it again
+    from multiprocessing import resource_tracker
+    resource_tracker.unregister(shm._name, "shared_memory")
+    try:
+        arr = np.ndarray((hi, rb), np.uint8, buffer=shm.buf)
+        t0, c0 = time.perf_counter(), time.process_time()
+        lay = ref.Layout(*lay_args)
+        m = hi - lo
+        recs = [arr[b].tobytes() for b in range(lo, hi)]
+        hk = [np.zeros((m, lay.slab_bytes), np.uint8) for _ in range(lay.n_layers)]
+        hv = [np.zeros((m, lay.slab_bytes), np.uint8) for _ in range(lay.n_layers)]
+        vs = ref.restore(lay, ns, recs, keys, np.arange(lo, hi), toks, np.arange(m, dtype=np.int32)[None, :], hk, hv)
+        del arr, recs
+        return vs, time.perf_counter() - t0, time.process_time() - c0
+    finally:
+        shm.close()
+
+
 def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
     """Save and restore of the other workloads (tiny, mid, hybrid) in the same
     library calls. Load bytes count what the load must move: every block's
@@ -248,6 +279,7 @@ def main():
     ap.add_argument("--save-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=1536)
+    ap.add_argument("--cpu-workers", type=int, default=64)
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--no-host-tier", action="store_true")
     ap.add_argument("--no-paper-blocks", action="store_true")
@@ -269,6 +301,14 @@ def main():
     import workloads as wl
     from paper_2609_39358_amd import taliesin as T
     from paper_2609_39358_amd.device import PagedCache, RecordStore
+
+    # worker processes for the multi-core CPU baseline: forked now, before
+    # this process touches the GPU
+    pool, n_workers = None, 0
+    if not args.no_cpu_baseline:
+        import multiprocessing as mp
+        n_workers = min(len(os.sched_getaffinity(0)), args.cpu_workers)
+        pool = mp.get_context("fork").Pool(n_workers)
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda"
@@ -534,12 +574,40 @@ def main():
         ru1 = resource.getrusage(resource.RUSAGE_SELF)
         assert vs == [ref.ACCEPT] * m
         cpu_s = (ru1.ru_utime - ru0.ru_utime) + (ru1.ru_stime - ru0.ru_stime)
-        cpu = {"value": m * (rb + payload) / cdt / 1e9, "unit": "GB/s",
-               "cores": max(1, round(cpu_s / cdt)), "kind": "oracle",
-               "sample": "verify+restore of %d of %d blocks (%.2f GB of records) on the host, "
-                         "single process" % (m, n, m * rb / 1e9),
-               "seconds": cdt, "tokens_avoided_per_s": m * P / cdt}
-        log("cpu oracle: %.2f GB/s over %.1f s" % (cpu["value"], cdt))
+        single = {"value": m * (rb + payload) / cdt / 1e9, "unit": "GB/s",
+                  "cores": max(1, round(cpu_s / cdt)), "seconds": cdt, "tokens_avoided_per_s": m * P / cdt}
+        log("cpu oracle, one process: %.2f GB/s over %.1f s" % (single["value"], cdt))
+        del recs, hk, hv
+        # the same sample split over one forked worker per host core
+        from multiprocessing import shared_memory
+        shm = shared_memory.SharedMemory(create=True, size=m * rb)
+        try:
+            arr = np.ndarray((m, rb), np.uint8, buffer=shm.buf)
+            arr[:] = store.buf[:m].cpu().numpy()
+            bounds = np.linspace(0, m, n_workers + 1).astype(int)
+            lay_args = (g.n_layers, g.n_kv_heads, g.head_dim, 1, P)
+            tasks = [(shm.name, int(lo), int(hi), rb, lay_args, ns, [k.tobytes() for k in keys0[lo:hi]],
+                      tokens[lo * P:hi * P].reshape(hi - lo, P)) for lo, hi in zip(bounds[:-1], bounds[1:])
+                     if hi > lo]
+            t0 = time.perf_counter()
+            res = pool.map(_oracle_slice, tasks)
+            wall = time.perf_counter() - t0
+            del arr
+        finally:
+            shm.close()
+            shm.unlink()
+        assert all(v == ref.ACCEPT for vs, _, _ in res for v in vs)
+        cpu_all = sum(c for _, _, c in res)
+        cpu = {"value": m * (rb + payload) / wall / 1e9, "unit": "GB/s", "cores": len(tasks), "kind": "oracle",
+               "sample": "verify+restore of %d of %d blocks (%.2f GB of records) on the host, split over %d "
+                         "worker processes (one per core); wall time includes each worker's copy of its "
+                         "records out of shared memory" % (m, n, m * rb / 1e9, len(tasks)),
+               "seconds": wall, "cpu_seconds": cpu_all, "tokens_avoided_per_s": m * P / wall,
+               "single_process": single}
+        log("cpu oracle, %d processes: %.2f GB/s over %.2f s (%.1f CPU s)" % (len(tasks), cpu["value"], wall, cpu_all))
+    if pool is not None:
+        pool.terminate()
+        pool.join()
 
     # ---- multi-request reuse: keys + lookup + verified restore per admission batch
     del store, dst, ws, verd, stage  # the corpus legs are done
