@@ -588,3 +588,126 @@ def test_parallel_walk_many_chains():
     keys, handles, hits = par_lookup(ctx, ch, two)
     total = check_walk(ch, ns, bt, two.index, keys, handles, hits)
     assert max(hits) > 600 and total > 100000
+
+
+def _device_path_case(seed):
+    geom = wl.Geometry(2, 4, 64, 16)
+    c = Case(geom, 24, 24, 24, seed=seed)
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    bt = c.lay.page_tokens
+    keys = [k.tobytes() for k in c.keys]
+    return c, store, bt, keys
+
+
+class DevicePath:
+    """Buffers and the three calls of a device restore (parallel walk)."""
+
+    def __init__(self, c, store, ch, idx, tidx, d_hk):
+        S, bt = ch.n_slots, c.lay.page_tokens
+        self.c, self.store, self.ch, self.idx, self.tidx, self.d_hk = c, store, ch, idx, tidx, d_hk
+        self.keys = torch.empty((S, 32), dtype=torch.uint8, device=DEV)
+        self.handles = torch.empty(S, dtype=torch.int64, device=DEV)
+        self.hits = torch.empty(ch.n, dtype=torch.int32, device=DEV)
+        self.ptrs, self.lens, self.bidx = (torch.empty(S, dtype=torch.int64, device=DEV) for _ in range(3))
+        self.toks = torch.empty((S, bt), dtype=torch.int32, device=DEV)
+        self.tab = torch.empty((1, S), dtype=torch.int32, device=DEV)
+        self.pool = PagedCache(c.geom.n_layers, S, c.stride, DEV)
+        self.verd = torch.zeros(S, dtype=torch.uint8, device=DEV)
+        self.ws_b = T.tl_workspace_bytes(c.ctx, S)
+        self.ws = torch.empty(self.ws_b, dtype=torch.uint8, device=DEV)
+        self.blk = T.make_blocks(self.keys, self.bidx, self.toks, self.tab)
+        self.S = S
+
+    def run(self, s):
+        c, ch = self.c, self.ch
+        T.tl_chain_lookup_par(c.ctx, s, ch.n, ch.tl, self.idx, self.tidx, self.d_hk, c.n, self.keys, self.handles,
+                              self.hits)
+        T.tl_chain_stage(c.ctx, s, ch.n, ch.tl, self.hits, self.handles, self.store.ptrs, self.store.lens, c.n,
+                         self.ptrs, self.lens, self.bidx, self.toks, None, self.tab)
+        T.tl_load(c.ctx, s, self.S, self.ptrs, self.lens, self.blk, self.pool.tl(), self.verd, self.ws, self.ws_b)
+
+
+def _indexes(c, keys, handles):
+    idx, tidx = new_index(128), new_index(128)
+    dput(idx, keys, handles)
+    fps = fingerprints(c.ctx, c.tokens, np.arange(c.n, dtype=np.uint64))
+    dput(tidx, fps, range(c.n))
+    d_hk = torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(c.n, 32).copy()).to(DEV)
+    return idx, tidx, d_hk
+
+
+def test_parallel_device_restore_in_a_graph():
+    c, store, bt, keys = _device_path_case(71)
+    doc = c.tokens.reshape(-1)
+    idx, tidx, d_hk = _indexes(c, keys, range(c.n))
+    index = ref.index_put({}, keys, range(c.n))
+    lengths = [20 * bt + 5, 24 * bt, 9 * bt]
+    ch = Chains(c.ctx, lengths, 0, bt)
+    dp = DevicePath(c, store, ch, idx, tidx, d_hk)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        dp.run(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        dp.run(s)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(8)
+    for step in range(4):
+        parts = []
+        for L in lengths:
+            m = int(rng.integers(0, L // bt + 1))
+            parts.append(np.concatenate([doc[:m * bt], wl.tokens(L - m * bt, 200 + step * 7 + L)]))
+        ch.tokens[:] = np.concatenate(parts)
+        ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+        for t in dp.pool.k + dp.pool.v:
+            t.fill_(step + 1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (dp.hits.cpu().numpy().copy(), dp.verd.cpu().numpy().copy(), host_layers(dp.pool))
+        for t in dp.pool.k + dp.pool.v:
+            t.fill_(step + 1)
+        dp.run(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        assert np.array_equal(got[0], dp.hits.cpu().numpy()) and np.array_equal(got[1], dp.verd.cpu().numpy())
+        want_pages = host_layers(dp.pool)
+        for a, b in zip(got[2][0] + got[2][1], want_pages[0] + want_pages[1]):
+            assert np.array_equal(a, b)
+        want = [ref.chain_walk(c.ns, ch.data(r), 4 * bt, index)[1] for r in range(ch.n)]
+        assert list(got[0]) == want, step
+        log("parallel replay", step, "hits", want)
+
+
+def test_forged_index_entry_fails_closed():
+    """A key-index entry that points a key at another block's record (the
+    index is not trusted): the walk reports the hit, the load refuses it and
+    zeroes its pages; every other block is restored."""
+    c, store, bt, keys = _device_path_case(72)
+    handles = list(range(c.n))
+    handles[6] = 9  # block 6's key -> record of block 9
+    idx, tidx, d_hk = _indexes(c, keys, handles)
+    ch = Chains(c.ctx, [c.n * bt], 0, bt)
+    ch.tokens[:] = c.tokens.reshape(-1)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    dp = DevicePath(c, store, ch, idx, tidx, d_hk)
+    for t in dp.pool.k + dp.pool.v:
+        t.fill_(0x77)
+    dp.run(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert int(dp.hits.cpu()[0]) == c.n
+    verd = dp.verd.cpu().numpy()
+    rec9 = store.buf[9].cpu().numpy().tobytes()
+    want6 = ref.verify(c.lay, c.ns, rec9, keys[6], 6, c.tokens[6], range(c.lay.n_slabs))
+    assert want6 == ref.POSITION and verd[6] == want6
+    assert all(verd[b] == ref.ACCEPT for b in range(c.n) if b != 6)
+    pk, pv = host_layers(dp.pool)
+    sk, sv = host_layers(c.src)
+    slab = c.lay.slab_bytes
+    for l in range(c.geom.n_layers):
+        assert not pk[l][6][:slab].any() and not pv[l][6][:slab].any()
+        p = int(c.t_src[0][5])
+        assert np.array_equal(pk[l][5][:slab], sk[l][p][:slab])
