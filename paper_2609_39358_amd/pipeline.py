@@ -127,6 +127,26 @@ class DeviceStore:
     def lens(self) -> torch.Tensor:
         return self.records.lens
 
+    def save_blocks(self, src: PagedCache, d_tables: torch.Tensor, d_keys: torch.Tensor, d_tokens: torch.Tensor,
+                    d_positions: torch.Tensor, d_slots: torch.Tensor, stream=None) -> torch.Tensor:
+        """Save n blocks of a paged cache (after their prefill) into record
+        slots d_slots and index them (Sec. 2.2: state is written once, after the
+        runtime computes it). Tables [n_groups][n * pages_per_block] name each
+        block's pages in src. Returns the device save status [n]."""
+        stream = stream or torch.cuda.current_stream()
+        n = d_keys.shape[0]
+        status = torch.zeros(max(n, 1), dtype=torch.uint8, device=self.device)
+        if n == 0:
+            return status[:0]
+        ptrs = self.records.ptrs.index_select(0, d_slots)
+        T.tl_save(self.ctx, stream, n, src.tl(), T.make_blocks(d_keys, d_positions, d_tokens, d_tables), ptrs,
+                  status)
+        if not bool((status[:n] == T.ACCEPT).all()):
+            raise RuntimeError("save refused some blocks (bad page ids)")
+        self.records.lens.index_fill_(0, d_slots, self.ctx.record_bytes)
+        self.add(d_keys, d_tokens, d_positions, d_slots, stream)
+        return status[:n]
+
     def add(self, d_keys: torch.Tensor, d_tokens: torch.Tensor, d_positions: torch.Tensor,
             d_slots: torch.Tensor, stream=None):
         """Index n saved blocks: keys [n][32] u8, tokens [n][block tokens] i32,

@@ -711,3 +711,49 @@ def test_forged_index_entry_fails_closed():
         assert not pk[l][6][:slab].any() and not pv[l][6][:slab].any()
         p = int(c.t_src[0][5])
         assert np.array_equal(pk[l][5][:slab], sk[l][p][:slab])
+
+
+def test_reuse_loop_on_the_device():
+    """Fig. 1 on the device: a first request finds nothing; its prefill is
+    saved and indexed once; a later request that shares its first 25 blocks
+    restores exactly those, bit-identical, and leaves the rest to prefill."""
+    from paper_2609_39358_amd import pipeline
+    from tests.gpu_case import ctx_of, fill_cache, layout_of
+    geom = wl.Geometry(2, 4, 64, 16)
+    ctx, lay = ctx_of(geom), layout_of(geom)
+    ns, bt = ref.namespace_digest(TEN, FP, lay), 16
+    store = pipeline.DeviceStore(ctx, 64, DEV)
+    pool_a = PagedCache(geom.n_layers, 64, lay.slab_bytes, DEV)
+    a = wl.tokens(40 * bt + 5, 300)
+    res = pipeline.DeviceRestorePipeline(store, pool_a).restore(i32(a.view(np.int32)), [a.size])
+    torch.cuda.synchronize()
+    assert res.hits.cpu().tolist() == [0] and (res.verdicts.cpu().numpy() == ref.MISSING).all()
+    # prefill of request A writes its 40 blocks into pool pages 0..39
+    fill_cache(pool_a, geom, 301)
+    # keys of all 40 blocks on the device (no index: every key), equal to the oracle's
+    ch = Chains(ctx, [a.size], 0, bt)
+    ch.tokens[:] = a
+    ch.d_tok.copy_(torch.from_numpy(a.view(np.int32)))
+    keys, _, hits = ch.lookup(ctx)
+    assert hits.tolist() == [40]
+    want = ref.block_keys(ns, a.tobytes(), 4 * bt)
+    assert [keys[k].tobytes() for k in range(40)] == want
+    st = store.save_blocks(pool_a, i32(np.arange(40)[None, :]), torch.from_numpy(keys[:40].copy()).to(DEV),
+                           i32(a[:40 * bt].view(np.int32).reshape(40, bt)), i64(np.arange(40)),
+                           torch.arange(40, dtype=torch.int64, device=DEV))
+    assert (st.cpu().numpy() == ref.ACCEPT).all()
+    # request B shares A's first 25 blocks
+    b = np.concatenate([a[:25 * bt], wl.tokens(300, 302)])
+    pool_b = PagedCache(geom.n_layers, 64, lay.slab_bytes, DEV)
+    for t in pool_b.k + pool_b.v:
+        t.fill_(0x42)
+    res = pipeline.DeviceRestorePipeline(store, pool_b).restore(i32(b.view(np.int32)), [b.size])
+    torch.cuda.synchronize()
+    index = ref.index_put({}, want, range(40))
+    assert res.hits.cpu().tolist() == [ref.chain_walk(ns, b.tobytes(), 4 * bt, index)[1]] == [25]
+    v = res.verdicts.cpu().numpy()
+    assert (v[:25] == ref.ACCEPT).all() and (v[25:] == ref.MISSING).all()
+    for l in range(geom.n_layers):
+        for ta, tb in ((pool_a.k[l], pool_b.k[l]), (pool_a.v[l], pool_b.v[l])):
+            assert torch.equal(tb[:25], ta[:25])  # the restored state is the saved state
+            assert (tb[25:] == 0x42).all()  # the rest is left to prefill
