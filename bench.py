@@ -286,6 +286,8 @@ def main():
     ap.add_argument("--no-multi-request", action="store_true")
     ap.add_argument("--no-other-configs", action="store_true")
     ap.add_argument("--host-tier-blocks", type=int, default=1024)
+    ap.add_argument("--no-disk-tier", action="store_true")
+    ap.add_argument("--disk-tier-blocks", type=int, default=512)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one MI355X: this build has no multi-GPU path "
@@ -554,6 +556,50 @@ def main():
         del hrec
         log("host tier: %.1f GB/s of records (plain H2D copy %.1f GB/s)" % (host_tier["GBps"], host_tier["h2d_copy_GBps"]))
 
+    # ---- disk tier: records in a file, streamed through two pinned buffers
+    disk = None
+    if not args.no_disk_tier:
+        import tempfile
+
+        from paper_2609_39358_amd import pipeline
+        m = min(args.disk_tier_blocks, n)
+        fd, path = tempfile.mkstemp(prefix="taliesin_records_", suffix=".bin")
+        os.close(fd)
+        try:
+            f = T.RecordFile(path, rb, create=True, n_threads=16)
+            hbuf = torch.empty((m, rb), dtype=torch.uint8, pin_memory=True)
+            hbuf.copy_(store.buf[:m])
+            torch.cuda.synchronize()
+            ids = np.arange(m, dtype=np.uint64)
+            f.write(ids, hbuf)
+            f.drop_cache()
+            t0 = time.perf_counter()
+            f.read(ids, hbuf)  # a plain cold read of the same records
+            read_s = time.perf_counter() - t0
+            del hbuf
+            fr = pipeline.FileRestore(ctx, f, dst, batch=64)
+            dblk = (d_keys0[:m], d_bidx[:m], d_tokens[:m], d_tdst[:, :m])
+            res = {}
+            for kind in ("disk", "page_cache"):
+                if kind == "disk":
+                    f.drop_cache()
+                t0 = time.perf_counter()
+                v = fr.restore(ids, *dblk)
+                res[kind] = time.perf_counter() - t0
+                assert (v == T.ACCEPT).all().item()
+            disk = {"blocks": m, "record_GB": m * rb / 1e9, "batch_blocks": 64,
+                    "cold_read_GBps": m * rb / read_s / 1e9,
+                    "restore_from_disk_GBps": m * rb / res["disk"] / 1e9,
+                    "restore_from_page_cache_GBps": m * rb / res["page_cache"] / 1e9,
+                    "tokens_avoided_per_s": m * P / res["disk"]}
+            disk["frac_of_cold_read"] = disk["restore_from_disk_GBps"] / disk["cold_read_GBps"]
+            f.close()
+            log("disk tier: restore %.2f GB/s from disk (plain cold read %.2f GB/s), %.1f GB/s from the page cache"
+                % (disk["restore_from_disk_GBps"], disk["cold_read_GBps"], disk["restore_from_page_cache_GBps"]))
+            del fr
+        finally:
+            os.unlink(path)
+
     # ---- CPU baseline: the oracle on a bounded sample of the same workload
     cpu = None
     if not args.no_cpu_baseline:
@@ -640,6 +686,7 @@ def main():
         "save": save,
         "host_ms": host,
         "host_tier": host_tier,
+        "disk_tier": disk,
         "paper_blocks": pb,
         "multi_request": mr,
         "other_configs": others,

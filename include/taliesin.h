@@ -55,6 +55,7 @@ extern "C" {
 #define TL_ENOMEM (-5)    /* host allocation failed */
 #define TL_EFULL (-6)     /* index is full */
 #define TL_ERANGE (-7)    /* workspace too small, buffer capacity too small */
+#define TL_EIO (-8)       /* a file operation failed */
 
 /* ---- per-block verdicts (tl_load) and save status (tl_save) ----------
  * When several checks fail, the smallest code wins. */
@@ -379,6 +380,33 @@ int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_ch
                    const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,
                    uint64_t* d_record_lens, uint64_t* d_block_index, uint32_t* d_tokens_out,
                    const int32_t* d_tables_in, int32_t* d_tables_out);
+
+/* ---- record files: the disk tier ------------------------------------------
+ * Records of one context kept back to back in one file (record id i at byte
+ * offset i * record_bytes). Batches of whole records move between the file
+ * and caller memory (host memory; for a restore, pinned memory that tl_load
+ * reads directly) on up to n_threads threads of positional reads or writes.
+ * Sec. 4.3: saved blocks stay on disk and are streamed in for a restore and
+ * dropped after use. Calls on one tl_file may run from several host threads
+ * when their record ranges do not overlap. */
+typedef struct tl_file tl_file;
+#define TL_FILE_WRITE 1  /* open for reading and writing */
+#define TL_FILE_CREATE 2 /* create or truncate */
+/* NULL and *status = TL_EINVAL (bad arguments, n_threads outside [1, 256]),
+ * TL_EIO (open failed), TL_ENOMEM. */
+tl_file* tl_file_open(const char* path, uint64_t record_bytes, int flags, int n_threads, int* status);
+int tl_file_close(tl_file* f); /* TL_EIO if close fails; NULL is a no-op */
+uint64_t tl_file_records(const tl_file* f); /* whole records in the file, 0 on error */
+/* dst[i*record_bytes ...] = record record_ids[i], i < n. TL_ERANGE (nothing
+ * read) if an id is past the end of the file; TL_EIO if a read fails (dst
+ * then holds partial data). */
+int tl_file_read(const tl_file* f, const uint64_t* record_ids, size_t n, void* dst);
+/* record record_ids[i] = src[i*record_bytes ...]; TL_EINVAL if the file was
+ * opened read-only; TL_EIO if a write fails. */
+int tl_file_write(tl_file* f, const uint64_t* record_ids, size_t n, const void* src);
+/* Flush written records to the device and drop the file's cached pages, so
+ * that later reads come from the disk. */
+int tl_file_drop_cache(tl_file* f);
 
 /* ---- profiling ------------------------------------------------------------
  * Opt-in kernel timing for benchmarks: while enabled (process-wide), every

@@ -40,7 +40,7 @@ def build(verbose: bool = False, extra_hip_flags=(), out: str = OUT, build_dir: 
     os.makedirs(build_dir, exist_ok=True)
     inc = ["-I", INCLUDE, "-I", CSRC]
     objs = []
-    for src in ("ctx.cpp", "sha256.cpp"):
+    for src in ("ctx.cpp", "sha256.cpp", "file_io.cpp"):
         o = os.path.join(build_dir, src + ".o")
         _run([cxx, *CXX_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", o], verbose)
         objs.append(o)

@@ -499,6 +499,7 @@ const char* tl_status_string(int s) {
     case TL_ENOMEM: return "out of host memory";
     case TL_EFULL: return "index full";
     case TL_ERANGE: return "size out of range";
+    case TL_EIO: return "file operation failed";
     default: return "unknown status";
   }
 }

@@ -221,3 +221,52 @@ class DeviceRestorePipeline:
             T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab), self.pool.tl(), verd, ws, ws_b)
             out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, tab, ws)
         return out
+
+
+class FileRestore:
+    """Restores records streamed from a record file (the disk tier, Sec. 4.3)
+    through two pinned host buffers of `batch` records: while the GPU restores
+    batch i straight out of one buffer (tl_load reads pinned host memory
+    directly), this thread reads batch i+1 into the other. Host memory stays
+    bounded at 2 * batch records and no device memory holds records."""
+
+    def __init__(self, ctx: T.Ctx, file: "T.RecordFile", pool: PagedCache, batch: int, stream=None):
+        self.ctx, self.file, self.pool, self.batch = ctx, file, pool, batch
+        self.stream = stream or torch.cuda.current_stream()
+        dev = pool.k[0].device
+        rb = ctx.record_bytes
+        self.bufs = [torch.empty((batch, rb), dtype=torch.uint8, pin_memory=True) for _ in range(2)]
+        self.ptrs = [torch.tensor([b.data_ptr() + i * rb for i in range(batch)], dtype=torch.int64, device=dev)
+                     for b in self.bufs]
+        self.lens = torch.full((batch,), rb, dtype=torch.int64, device=dev)
+        self.done = [torch.cuda.Event(), torch.cuda.Event()]
+        self.ws_bytes = T.tl_workspace_bytes(ctx, batch)
+        self.ws = [torch.empty(max(self.ws_bytes, 4), dtype=torch.uint8, device=dev) for _ in range(2)]
+        self.dev = dev
+
+    def restore(self, record_ids, d_keys, d_positions, d_tokens, d_tables) -> torch.Tensor:
+        """Record record_ids[b] restores block b (keys [n][32], positions [n],
+        tokens [n][block tokens] or None, tables [n_groups][n * ppb]; device).
+        Returns the device verdicts [n] (valid after the stream syncs)."""
+        ids = np.asarray(record_ids, dtype=np.uint64)
+        n, B, ppb = ids.size, self.batch, self.ctx.pages_per_block
+        verd = torch.empty(max(n, 1), dtype=torch.uint8, device=self.dev)
+        spans = [(lo, min(lo + B, n)) for lo in range(0, n, B)]
+        keep = []  # per-batch arrays the enqueued loads read, alive until the end
+        if spans:
+            self.file.read(ids[spans[0][0]:spans[0][1]], self.bufs[0])
+        for i, (lo, hi) in enumerate(spans):
+            k = i & 1
+            tabs = d_tables[:, lo * ppb:hi * ppb].contiguous()
+            blk = T.make_blocks(d_keys[lo:hi], d_positions[lo:hi], None if d_tokens is None else d_tokens[lo:hi],
+                                tabs)
+            keep.append((tabs, blk))
+            T.tl_load(self.ctx, self.stream, hi - lo, self.ptrs[k], self.lens, blk, self.pool.tl(), verd[lo:hi],
+                      self.ws[k], self.ws_bytes)
+            self.done[k].record(self.stream)
+            if i + 1 < len(spans):
+                nlo, nhi = spans[i + 1]
+                self.done[k ^ 1].synchronize()  # the load that last read the other buffer is finished
+                self.file.read(ids[nlo:nhi], self.bufs[k ^ 1])
+        self.stream.synchronize()
+        return verd[:n]

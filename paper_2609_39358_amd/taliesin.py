@@ -19,7 +19,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 # TALIESIN_LIB may point at another build of the same library (e.g. a tuning variant)
 LIB_PATH = os.environ.get("TALIESIN_LIB") or os.path.join(_HERE, "libtaliesin.so")
 
-TL_OK, TL_EINVAL, TL_ELAYOUT, TL_ENOIDENT, TL_EDEVICE, TL_ENOMEM, TL_EFULL, TL_ERANGE = 0, -1, -2, -3, -4, -5, -6, -7
+TL_OK, TL_EINVAL, TL_ELAYOUT, TL_ENOIDENT, TL_EDEVICE, TL_ENOMEM, TL_EFULL, TL_ERANGE, TL_EIO = 0, -1, -2, -3, -4, -5, -6, -7, -8
 ACCEPT, MISSING, BADARG, TRUNCATED, OVERLONG = 0x01, 0x10, 0x11, 0x12, 0x13
 ROOT, HEADER, POSITION, KEY, TOKENS, SEGMENT = 0x14, 0x15, 0x16, 0x17, 0x18, 0x19
 DTYPE = {"bf16": 1, "f16": 2, "f32": 3, "fp8": 4}
@@ -107,6 +107,12 @@ def _load():
                                      P, P, P, P]),
         "tl_block_fingerprints": (c.c_int, [P, P, c.c_size_t, P, P, P]),
         "tl_chain_lookup_par": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, c.c_uint64, P, P, P]),
+        "tl_file_open": (P, [c.c_char_p, c.c_uint64, c.c_int, c.c_int, c.POINTER(c.c_int)]),
+        "tl_file_close": (c.c_int, [P]),
+        "tl_file_records": (c.c_uint64, [P]),
+        "tl_file_read": (c.c_int, [P, P, c.c_size_t, P]),
+        "tl_file_write": (c.c_int, [P, P, c.c_size_t, P]),
+        "tl_file_drop_cache": (c.c_int, [P]),
         "tl_status_string": (c.c_char_p, [c.c_int]),
         "tl_verdict_string": (c.c_char_p, [c.c_int]),
         "tl_abi_version": (c.c_int, []),
@@ -128,7 +134,8 @@ EXPORTED = (
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
     "tl_dindex_bytes", "tl_dindex_create", "tl_dindex_destroy", "tl_dindex_workspace_bytes",
     "tl_dindex_put", "tl_dindex_get", "tl_dindex_stats", "tl_chain_lookup", "tl_chain_stage",
-    "tl_block_fingerprints", "tl_chain_lookup_par",
+    "tl_block_fingerprints", "tl_chain_lookup_par", "tl_file_open", "tl_file_close", "tl_file_records",
+    "tl_file_read", "tl_file_write", "tl_file_drop_cache",
     "tl_status_string", "tl_verdict_string", "tl_abi_version", "tl_test_sha256", "tl_timing",
     "tl_timing_read")
 KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4, "chain": 5,
@@ -428,6 +435,54 @@ def tl_chain_stage(ctx: Ctx, stream, n_chains: int, chains: tl_chains, d_hits, d
                                _addr(d_record_ptrs), _addr(d_record_lens), _addr(d_block_index),
                                _addr(d_tokens_out), _addr(d_tables_in), _addr(d_tables_out)),
            "tl_chain_stage")
+
+
+# ------------------------------------------------------------------ record files (disk tier)
+TL_FILE_WRITE, TL_FILE_CREATE = 1, 2
+
+
+class RecordFile:
+    """A tl_file: records of record_bytes each, back to back in one file."""
+
+    def __init__(self, path: str, record_bytes: int, write: bool = False, create: bool = False,
+                 n_threads: int = 8):
+        st = ctypes.c_int(0)
+        flags = (TL_FILE_WRITE if write or create else 0) | (TL_FILE_CREATE if create else 0)
+        self.record_bytes = record_bytes
+        self._h = _lib.tl_file_open(os.fsencode(path), record_bytes, flags, n_threads, ctypes.byref(st))
+        if not self._h:
+            raise TaliesinError(st.value, "tl_file_open")
+
+    def __len__(self):
+        return int(_lib.tl_file_records(self._h))
+
+    @staticmethod
+    def _ids(ids) -> np.ndarray:
+        return np.ascontiguousarray(np.asarray(ids, dtype=np.uint64))
+
+    def read(self, ids, dst):
+        """Records `ids` into host memory `dst` (a tensor or array of at least
+        len(ids) * record_bytes bytes)."""
+        a = self._ids(ids)
+        _check(_lib.tl_file_read(self._h, a.ctypes.data, a.size, _addr(dst)), "tl_file_read")
+
+    def write(self, ids, src):
+        a = self._ids(ids)
+        _check(_lib.tl_file_write(self._h, a.ctypes.data, a.size, _addr(src)), "tl_file_write")
+
+    def drop_cache(self):
+        _check(_lib.tl_file_drop_cache(self._h), "tl_file_drop_cache")
+
+    def close(self):
+        if self._h:
+            h, self._h = self._h, None
+            _check(_lib.tl_file_close(h), "tl_file_close")
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def sha256_selftest(data: bytes, impl: int) -> Optional[bytes]:

@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
+#include <unistd.h>
 
 #include <vector>
 
@@ -182,6 +183,36 @@ int main() {
   EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EDEVICE);
   EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, nullptr, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
   EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, nullptr, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
+  // record files: write in one order, read back in another on several threads
+  {
+    char path[] = "/tmp/tl_selftest_XXXXXX";
+    const int tmpfd = mkstemp(path);
+    EXPECT(tmpfd >= 0);
+    if (tmpfd >= 0) close(tmpfd);
+    const uint64_t frb = 1000;
+    std::vector<uint8_t> fsrc(frb * 37), fdst(frb * 60);
+    for (auto& x : fsrc) x = (uint8_t)rnd();
+    std::vector<uint64_t> wid(37), rid(60);
+    for (int i = 0; i < 37; ++i) wid[i] = (uint64_t)((i * 11) % 37);
+    std::vector<uint8_t> shuffled(frb * 37);
+    for (int i = 0; i < 37; ++i) memcpy(&shuffled[frb * i], &fsrc[frb * wid[i]], frb);
+    tl_file* wf = tl_file_open(path, frb, TL_FILE_WRITE | TL_FILE_CREATE, 6, &st);
+    EXPECT(wf && st == TL_OK);
+    EXPECT(tl_file_write(wf, wid.data(), 37, shuffled.data()) == TL_OK);
+    EXPECT(tl_file_drop_cache(wf) == TL_OK && tl_file_records(wf) == 37);
+    for (int i = 0; i < 60; ++i) rid[i] = rnd() % 37;
+    EXPECT(tl_file_read(wf, rid.data(), 60, fdst.data()) == TL_OK);
+    for (int i = 0; i < 60; ++i) EXPECT(!memcmp(&fdst[frb * i], &fsrc[frb * rid[i]], frb));
+    rid[7] = 37;
+    EXPECT(tl_file_read(wf, rid.data(), 60, fdst.data()) == TL_ERANGE);
+    EXPECT(tl_file_close(wf) == TL_OK);
+    tl_file* rf = tl_file_open(path, frb, 0, 1, &st);
+    EXPECT(rf && tl_file_write(rf, wid.data(), 1, fsrc.data()) == TL_EINVAL);
+    EXPECT(tl_file_close(rf) == TL_OK);
+    EXPECT(!tl_file_open(path, frb, 8, 1, &st) && st == TL_EINVAL);
+    EXPECT(!tl_file_open(path, 0, 0, 1, &st) && st == TL_EINVAL);
+    unlink(path);
+  }
   for (int s = 1; s >= -8; --s) EXPECT(tl_status_string(s) != nullptr);
   for (int v = 0; v < 0x20; ++v) EXPECT(tl_verdict_string(v) != nullptr);
   tl_ctx_destroy(c);

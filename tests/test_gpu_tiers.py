@@ -1,7 +1,8 @@
-"""GPU tests of the two paths around the HBM restore: saving layer by layer
-while prefill proceeds (tl_save_layers + tl_save_seal), and restoring from
-records that live in pinned host memory (read by the kernels over the host
-link). Both are checked byte for byte against the oracle."""
+"""GPU tests of the paths around the HBM restore: saving layer by layer
+while prefill proceeds (tl_save_layers + tl_save_seal), restoring from records
+that live in pinned host memory (read by the kernels over the host link), and
+restoring records streamed from a record file through two pinned buffers (the
+disk tier). All are checked byte for byte against the oracle."""
 import numpy as np
 import pytest
 import torch
@@ -126,3 +127,42 @@ def test_restore_from_pinned_host_records(name):
     hk, hv = host_layers(dst)
     for l in range(geom.n_layers):
         assert np.array_equal(hk[l], hk0[l]) and np.array_equal(hv[l], hv0[l])
+
+
+def test_restore_streamed_from_a_record_file(tmp_path):
+    from paper_2609_39358_amd import pipeline
+    geom = wl.Geometry(3, 4, 64, 16)
+    n = 45
+    c = Case(geom, n, 64, 64, seed=16)
+    c.make_src()
+    store, st = c.save()
+    recs_o, _ = c.oracle_save()
+    rb = c.lay.record_bytes
+    path = str(tmp_path / "records.bin")
+    f = T.RecordFile(path, rb, create=True, n_threads=4)
+    host = store.buf.cpu().numpy()
+    # records on disk in reverse order: block b is record n-1-b of the file
+    f.write(np.arange(n)[::-1], host)
+    recs = [bytearray(r) for r in recs_o]
+    po = c.lay.payload_offset
+    for b, off in ((4, po + 99), (30, 140)):  # damage on disk
+        rid = n - 1 - b
+        one = np.zeros((1, rb), np.uint8)
+        f.read([rid], one)
+        one[0, off] ^= 0x40
+        f.write([rid], one)
+        recs[b][off] ^= 0x40
+    f.drop_cache()
+    dst = random_fill(PagedCache(geom.n_layers, 64, c.stride, DEV), 17)
+    hk0, hv0 = host_layers(dst)
+    fr = pipeline.FileRestore(c.ctx, f, dst, batch=8)  # 45 blocks: five full batches and a ragged one
+    log("restore streamed from a record file:", n, "blocks in batches of 8")
+    v = fr.restore(np.arange(n)[::-1], c.d_keys, c.d_bidx, c.d_tokens, i32(c.t_dst)).cpu().numpy()
+    vo = ref.restore(c.lay, c.ns, [bytes(r) for r in recs], [k.tobytes() for k in c.keys], c.bidx, c.tokens,
+                     c.t_dst, hk0, hv0, n_pages=64)
+    assert [int(x) for x in v] == vo
+    assert vo[4] == ref.SEGMENT and vo[30] == ref.ROOT and vo.count(ref.ACCEPT) == n - 2
+    hk, hv = host_layers(dst)
+    for l in range(geom.n_layers):
+        assert np.array_equal(hk[l], hk0[l]) and np.array_equal(hv[l], hv0[l])
+    f.close()

@@ -212,3 +212,40 @@ def test_status_and_verdict_strings():
     assert T.verdict_name(0x77) == "UNKNOWN"
     for code, name in ref.VERDICT_NAMES.items():
         assert T.verdict_name(code) == name
+
+
+def test_record_file_round_trip_and_errors(tmp_path):
+    """The disk tier's file I/O on the CPU: records written in one order are
+    read back in another, on several threads; errors are statuses."""
+    rb = 4096 + 256
+    path = str(tmp_path / "records.bin")
+    rng = np.random.default_rng(9)
+    src = rng.integers(0, 256, (50, rb), dtype=np.uint8)
+    f = T.RecordFile(path, rb, create=True, n_threads=5)
+    order = rng.permutation(50)
+    f.write(order, src[order])  # record i = src[i], written in a shuffled order
+    f.drop_cache()
+    assert len(f) == 50 and os.path.getsize(path) == 50 * rb
+    ids = rng.integers(0, 50, 200)
+    dst = np.zeros((200, rb), np.uint8)
+    f.read(ids, dst)
+    assert np.array_equal(dst, src[ids])
+    with pytest.raises(T.TaliesinError) as e:
+        f.read([50], dst)
+    assert e.value.status == T.TL_ERANGE
+    f.close()
+    ro = T.RecordFile(path, rb, n_threads=1)
+    with pytest.raises(T.TaliesinError) as e:
+        ro.write([0], src[:1])
+    assert e.value.status == T.TL_EINVAL
+    one = np.zeros((1, rb), np.uint8)
+    ro.read([49], one)
+    assert np.array_equal(one[0], src[49])
+    ro.close()
+    for kw in ({"n_threads": 0}, {"n_threads": 257}):
+        with pytest.raises(T.TaliesinError) as e:
+            T.RecordFile(path, rb, **kw)
+        assert e.value.status == T.TL_EINVAL
+    with pytest.raises(T.TaliesinError) as e:
+        T.RecordFile(str(tmp_path / "missing.bin"), rb)
+    assert e.value.status == T.TL_EIO

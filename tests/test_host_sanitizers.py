@@ -19,7 +19,7 @@ def test_host_runtime_under_asan_and_ubsan(tmp_path):
            "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC,
            os.path.join(ROOT, "tests", "native", "host_selftest.cpp"),
-           os.path.join(CSRC, "ctx.cpp"), os.path.join(CSRC, "sha256.cpp"),
+           os.path.join(CSRC, "ctx.cpp"), os.path.join(CSRC, "sha256.cpp"), os.path.join(CSRC, "file_io.cpp"),
            "-pthread", "-o", str(exe)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-4000:]
