@@ -202,16 +202,19 @@ def namespace_digest(tenant: bytes, model_fp: bytes, lay: Layout) -> bytes:
     return hashlib.sha256(bytes(m)).digest()
 
 
-def block_keys(parent: bytes, data: bytes, block_bytes: int) -> List[bytes]:
+def block_keys(parent: bytes, data: bytes, block_bytes: int, tail: bool = False) -> List[bytes]:
     """Chained block fingerprints (Sec. 2.2: key = fingerprint of the exact input
     bytes; Sec. 5: reuse only whole blocks at matching positions, so a block's
     key must cover every byte before it):
         k_{-1} = parent,  k_i = SHA-256(k_{i-1} || data[i*B : (i+1)*B]).
-    Only full blocks get a key; a partial tail block is recomputed."""
+    Full blocks get a key; with tail=True so does a partial last block, whose
+    key hashes exactly its bytes (a document stored as whole blocks and one
+    partial block, Sec. 4.1: 11 blocks for 96,726 tokens)."""
     if len(parent) != 32 or block_bytes <= 0:
         raise ValueError("bad parent or block size")
     keys, k = [], bytes(parent)
-    for i in range(len(data) // block_bytes):
+    n = -(-len(data) // block_bytes) if tail else len(data) // block_bytes
+    for i in range(n):
         k = hashlib.sha256(k + bytes(data[i * block_bytes:(i + 1) * block_bytes])).digest()
         keys.append(k)
     return keys
@@ -225,13 +228,14 @@ def index_put(index: dict, keys: Sequence[bytes], handles: Sequence[int]) -> dic
     return index
 
 
-def chain_walk(parent: bytes, data: bytes, block_bytes: int, index: dict) -> Tuple[List[bytes], int, List[int]]:
+def chain_walk(parent: bytes, data: bytes, block_bytes: int, index: dict,
+               tail: bool = False) -> Tuple[List[bytes], int, List[int]]:
     """Reuse of one request against a store (Sec. 2.2: a later request that
     contains a stored block loads it; Sec. 5: only whole blocks at matching
     positions, so once a block has no stored state, no later block of the
     request can be reused either). Returns the request's block keys, the
     number of leading blocks whose key is in `index`, and their handles."""
-    keys = block_keys(parent, data, block_bytes)
+    keys = block_keys(parent, data, block_bytes, tail)
     hits = 0
     while hits < len(keys) and keys[hits] in index:
         hits += 1
@@ -277,7 +281,23 @@ def root_digest(meta: bytes) -> int:
 
 
 # ------------------------------------------------------------------ record
-def header_fields(lay: Layout, ns: bytes, key: bytes, block_index: int) -> bytes:
+def tail_field(lay: Layout, n_tokens: Optional[int]) -> int:
+    """Header field at offset 156: 0 for a full block, else the number of
+    tokens of a partial last block."""
+    if n_tokens is None or n_tokens == lay.block_tokens:
+        return 0
+    if not (1 <= n_tokens < lay.block_tokens):
+        raise ValueError("tokens per block out of range")
+    return n_tokens
+
+
+def pages_used(lay: Layout, n_tokens: Optional[int]) -> int:
+    """Pages of a block that hold its tokens."""
+    t = lay.block_tokens if n_tokens is None else n_tokens
+    return -(-t // lay.page_tokens)
+
+
+def header_fields(lay: Layout, ns: bytes, key: bytes, block_index: int, n_tokens: Optional[int] = None) -> bytes:
     """The 256-byte header with the root field still 0."""
     h = bytearray(HEADER_BYTES)
     h[0:8] = MAGIC
@@ -289,20 +309,22 @@ def header_fields(lay: Layout, ns: bytes, key: bytes, block_index: int) -> bytes
     h[72:104] = key
     h[104:136] = ns
     struct.pack_into("<II", h, 136, CHUNK_BYTES, lay.n_segments)
-    struct.pack_into("<I", h, 152, lay.pages_per_block)
+    struct.pack_into("<II", h, 152, lay.pages_per_block, tail_field(lay, n_tokens))
     return bytes(h)
 
 
 def make_meta(lay: Layout, ns: bytes, key: bytes, block_index: int, tokens, table: Sequence[int]) -> bytes:
+    """Metadata of a block of len(tokens) tokens (block tokens, or fewer for
+    a partial last block, whose token area is padded with zeros)."""
     toks = np.asarray(tokens, dtype="<u4")
-    assert toks.size == lay.block_tokens and len(table) == lay.n_segments
+    assert 1 <= toks.size <= lay.block_tokens and len(table) == lay.n_segments
     m = bytearray(lay.meta_bytes)
-    m[0:HEADER_BYTES] = header_fields(lay, ns, key, block_index)
+    m[0:HEADER_BYTES] = header_fields(lay, ns, key, block_index, toks.size)
     off = HEADER_BYTES
     for t in table:
         struct.pack_into("<Q", m, off, t)
         off += 8
-    m[off:off + 4 * lay.block_tokens] = toks.tobytes()
+    m[off:off + 4 * toks.size] = toks.tobytes()
     struct.pack_into("<Q", m, ROOT_OFFSET, root_digest(bytes(m)))
     return bytes(m)
 
@@ -322,14 +344,18 @@ def _page_ok(p: int, n_pages: int) -> bool:
     return 0 <= p < n_pages
 
 
-def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens, n_pages=None):
+def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens, n_pages=None,
+         n_tokens=None):
     """Gather every block's pages into a record.
 
     src_k[l], src_v[l]: uint8 arrays [pages, >= slab_bytes] (page rows).
     tables: [n_groups][n_blocks * pages_per_block] page ids; layer l uses
     tables[group(l)], page j of block b at index b * pages_per_block + j.
-    Returns (records, status): a block with any page id outside [0, n_pages)
-    gets an all-zero record and status BADARG, else status ACCEPT."""
+    n_tokens: tokens of each block (None: all full); a partial block stores
+    tokens[b][:n_tokens[b]], and its pages past the ones holding its tokens
+    may be -1, stored as zero slabs.
+    Returns (records, status): a block with any other page id outside
+    [0, n_pages) gets an all-zero record and status BADARG, else ACCEPT."""
     tables = np.asarray(tables)
     n = len(keys)
     ppb = lay.pages_per_block
@@ -337,7 +363,11 @@ def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens
     used = sorted({lay.group(l) for l in range(lay.n_layers)})
     records, status = [], []
     for b in range(n):
-        if not all(_page_ok(int(tables[g][b * ppb + j]), n_pages) for g in used for j in range(ppb)):
+        t = lay.block_tokens if n_tokens is None else int(n_tokens[b])
+        need = pages_used(lay, t)
+        ok = all(_page_ok(int(tables[g][b * ppb + j]), n_pages) or (j >= need and int(tables[g][b * ppb + j]) == -1)
+                 for g in used for j in range(ppb))
+        if not ok:
             records.append(bytes(lay.record_bytes))
             status.append(BADARG)
             continue
@@ -346,8 +376,9 @@ def save(lay: Layout, ns: bytes, src_k, src_v, tables, keys, block_index, tokens
             for kv, src in ((0, src_k), (1, src_v)):
                 for j in range(ppb):
                     page = table_entry(lay, tables, l, b, j)
-                    slabs.append(np.asarray(src[l][page, :lay.slab_bytes]).tobytes())
-        records.append(make_record(lay, ns, keys[b], int(block_index[b]), tokens[b], slabs))
+                    slabs.append(bytes(lay.slab_bytes) if page == -1 else
+                                 np.asarray(src[l][page, :lay.slab_bytes]).tobytes())
+        records.append(make_record(lay, ns, keys[b], int(block_index[b]), np.asarray(tokens[b])[:t], slabs))
         status.append(ACCEPT)
     return records, status
 
@@ -365,32 +396,35 @@ def read_slabs(lay: Layout, tables, b: int) -> List[Tuple[int, int, int, int]]:
     return out
 
 
-def check_meta(lay: Layout, ns: bytes, rec: bytes, key: bytes, block_index: int, tokens) -> int:
+def check_meta(lay: Layout, ns: bytes, rec: bytes, key: bytes, block_index: int, tokens,
+               n_tokens: Optional[int] = None) -> int:
     """Metadata checks in precedence order, on a record of exactly
-    record_bytes. Returns the first failing code, or ACCEPT."""
+    record_bytes, for a block expected to hold n_tokens tokens (None: a full
+    block). Returns the first failing code, or ACCEPT."""
     meta = rec[:lay.payload_offset]
     if struct.unpack_from("<Q", meta, ROOT_OFFSET)[0] != root_digest(meta):
         return ROOT
-    want = header_fields(lay, ns, bytes(32), 0)
+    t = lay.block_tokens if n_tokens is None else n_tokens
+    want = header_fields(lay, ns, bytes(32), 0, t)
     got = bytearray(meta[:HEADER_BYTES])
     got[64:72] = bytes(8)  # block index, checked as POSITION
     got[72:104] = bytes(32)  # key, checked as KEY
     got[ROOT_OFFSET:ROOT_OFFSET + 8] = bytes(8)
-    if bytes(got) != want or any(meta[lay.meta_end:]):
+    t0 = HEADER_BYTES + 8 * lay.n_segments
+    if bytes(got) != want or any(meta[t0 + 4 * t:]):  # header, then the zero padding after the tokens
         return HEADER
     if struct.unpack_from("<Q", meta, 64)[0] != block_index:
         return POSITION
     if meta[72:104] != key:
         return KEY
     if tokens is not None:
-        t0 = HEADER_BYTES + 8 * lay.n_segments
-        if meta[t0:t0 + 4 * lay.block_tokens] != np.asarray(tokens, dtype="<u4").tobytes():
+        if meta[t0:t0 + 4 * t] != np.asarray(tokens, dtype="<u4")[:t].tobytes():
             return TOKENS
     return ACCEPT
 
 
 def verify(lay: Layout, ns: bytes, rec: Optional[bytes], key: bytes, block_index: int,
-           tokens, slabs_read: Sequence[int], bad_arg: bool = False) -> int:
+           tokens, slabs_read: Sequence[int], bad_arg: bool = False, n_tokens: Optional[int] = None) -> int:
     """Verdict for one block (Sec. 2.2: checked on load; fail closed).
 
     rec is the readable record (None = no record; its length is the length the
@@ -403,7 +437,7 @@ def verify(lay: Layout, ns: bytes, rec: Optional[bytes], key: bytes, block_index
         return TRUNCATED
     if len(rec) > lay.record_bytes:
         return OVERLONG
-    code = check_meta(lay, ns, rec, key, block_index, tokens)
+    code = check_meta(lay, ns, rec, key, block_index, tokens, n_tokens)
     if code != ACCEPT:
         return code
     cps = lay.chunks_per_slab
@@ -419,11 +453,13 @@ def verify(lay: Layout, ns: bytes, rec: Optional[bytes], key: bytes, block_index
 
 
 def restore(lay: Layout, ns: bytes, records, keys, block_index, tokens, tables,
-            dst_k, dst_v, n_pages=None, misaligned=()):
+            dst_k, dst_v, n_pages=None, misaligned=(), n_tokens=None):
     """Verify every listed block and scatter accepted ones into the paged cache.
 
     records[b]: bytes or None; tokens: [n][block tokens] or None (no token
-    check); tables: [n_groups][n * pages_per_block] destination page ids
+    check); n_tokens: tokens of each block (None: all full; a partial last
+    block is compared on its first n_tokens[b] ids);
+    tables: [n_groups][n * pages_per_block] destination page ids
     (-1 = do not restore that page of that layer group). Accepted blocks: every read slab is copied to
     its page. Rejected blocks: every in-range page the block would have
     written is zero-filled. Pages of other blocks and -1 entries are untouched.
@@ -438,7 +474,8 @@ def restore(lay: Layout, ns: bytes, records, keys, block_index, tokens, tables,
         pages = [table_entry(lay, tables, l, b, j) for (_, l, _, j) in slabs]
         bad = b in misaligned or any(not _page_ok(p, n_pages) for p in pages)
         v = verify(lay, ns, records[b], keys[b], int(block_index[b]),
-                   None if tokens is None else tokens[b], [s for (s, *_) in slabs], bad)
+                   None if tokens is None else tokens[b], [s for (s, *_) in slabs], bad,
+                   None if n_tokens is None else int(n_tokens[b]))
         verdicts.append(v)
         for (s, l, kv, _), p in zip(slabs, pages):
             if not _page_ok(p, n_pages):

@@ -157,3 +157,30 @@ def test_first_duplicate_wins_caught(monkeypatch):
     monkeypatch.setattr(ref, "index_put", first_wins)
     with pytest.raises(AssertionError):
         reuse.test_index_put_last_duplicate_wins_and_overwrites()
+
+
+def test_tail_mutants_caught(monkeypatch):
+    from tests import test_oracle_tail as tail
+    # wrong: the tail field is not written (every tail looks like a full block)
+    real_field = ref.tail_field
+    monkeypatch.setattr(ref, "tail_field", lambda lay, n_tokens: 0)
+    with pytest.raises(AssertionError):
+        tail.test_tail_record_fields_and_padding()
+    monkeypatch.setattr(ref, "tail_field", real_field)
+    # wrong: the token area past a tail is not checked for zeros
+    real_check = ref.check_meta
+
+    def lax(lay, ns, rec, key, block_index, tokens, n_tokens=None):
+        t = lay.block_tokens if n_tokens is None else n_tokens
+        t0 = ref.HEADER_BYTES + 8 * lay.n_segments
+        r = bytearray(rec)
+        r[t0 + 4 * t:lay.meta_end] = bytes(lay.meta_end - t0 - 4 * t)
+        m = bytearray(r[:lay.payload_offset])
+        m[144:152] = ref.root_digest(bytes(m)).to_bytes(8, "little")
+        if real_check(lay, ns, rec, key, block_index, tokens, n_tokens) == ref.ROOT:
+            return ref.ROOT
+        return real_check(lay, ns, bytes(m) + bytes(r[lay.payload_offset:]), key, block_index, tokens, n_tokens)
+
+    monkeypatch.setattr(ref, "check_meta", lax)
+    with pytest.raises(AssertionError):
+        tail.test_tail_checks()
