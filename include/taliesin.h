@@ -142,6 +142,16 @@ typedef struct tl_blocks {
                                     entry must be in [0, n_pages). tl_load:
                                     -1 = do not restore that layer group for
                                     this block (its slabs are not read). */
+  const uint32_t* d_n_tokens;    /* [n] tokens of each block, or NULL: every
+                                    block holds tokens-per-block tokens. A
+                                    smaller count marks a document's partial
+                                    last block: its record stores that many
+                                    token ids (the rest of the token area is
+                                    zero) and the count (header offset 156);
+                                    tl_save accepts -1 for the pages that hold
+                                    none of its tokens and stores them as zero
+                                    slabs. A count outside [1, tokens per
+                                    block] is TL_BADARG. */
 } tl_blocks;
 
 typedef struct tl_ctx tl_ctx;
@@ -168,23 +178,26 @@ size_t tl_workspace_bytes(const tl_ctx* ctx, size_t n_blocks);
 /* ---- a1: chained block keys (host) -------------------------------------
  * k_{-1} = parent (NULL: the context's namespace digest),
  * k_i = SHA-256(k_{i-1} | bytes[i*B, (i+1)*B)), B = block_bytes (0: the
- * context's 4 * tokens per block, i.e. u32 little-endian token ids). Only full blocks
- * get a key; a partial tail is left for prefill. Sets *n_keys = n_full and
- * writes the n_full keys (32 bytes each) to keys_out; TL_ERANGE, with nothing
- * written, if cap < n_full.
+ * context's 4 * tokens per block, i.e. u32 little-endian token ids). Full
+ * blocks get a key; with TL_KEYS_TAIL in flags so does a partial last block,
+ * whose key hashes exactly the bytes it has (Sec. 4.1 stores 96,726 tokens
+ * as 11 blocks: the last one partial). Sets *n_keys and writes that many keys
+ * (32 bytes each) to keys_out; TL_ERANGE, with nothing written, if cap is
+ * smaller.
  * Sec. 2.2 (fingerprint of the exact input bytes, model and tenant), Sec. 5
  * (whole blocks at exact positions: every key covers all bytes before it). */
+#define TL_KEYS_TAIL 1
 int tl_block_keys(const tl_ctx* ctx, const uint8_t* parent, const void* bytes, size_t n_bytes,
-                  size_t block_bytes, uint8_t* keys_out, size_t cap, size_t* n_keys);
+                  size_t block_bytes, uint32_t flags, uint8_t* keys_out, size_t cap, size_t* n_keys);
 
 /* Same chain for n_docs independent documents, run on host threads
  * (one chain per thread at a time). doc_off[d], doc_len[d]: byte range of
  * document d in `bytes`; key_off[d]: first key slot of document d in keys_out
- * (caller sizes it for floor(doc_len/B) keys); n_keys_out[d] (optional)
- * receives the number of keys. parents: NULL or [n_docs][32]. */
+ * (caller sizes it for the key count of each document); n_keys_out[d]
+ * (optional) receives the number of keys. parents: NULL or [n_docs][32]. */
 int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* bytes,
                         const uint64_t* doc_off, const uint64_t* doc_len, size_t n_docs,
-                        size_t block_bytes, uint8_t* keys_out, const uint64_t* key_off,
+                        size_t block_bytes, uint32_t flags, uint8_t* keys_out, const uint64_t* key_off,
                         uint64_t* n_keys_out, int n_threads);
 
 /* ---- a6: save -----------------------------------------------------------

@@ -162,39 +162,48 @@ size_t tl_workspace_bytes(const tl_ctx* ctx, size_t n_blocks) {
 }
 
 // ---- a1: key chain ---------------------------------------------------------
-static void chain(const uint8_t* parent, const uint8_t* bytes, size_t n_full, size_t B, uint8_t* out) {
+// Keys of the first n_keys blocks of B bytes of a document of n_bytes
+// (the last one may be a partial block: it hashes only the bytes there are).
+static void chain(const uint8_t* parent, const uint8_t* bytes, size_t n_bytes, size_t n_keys, size_t B,
+                  uint8_t* out) {
   uint8_t k[32];
   memcpy(k, parent, 32);
-  for (size_t i = 0; i < n_full; ++i) {
-    tl::sha256(k, 32, bytes + i * B, B, k);
+  for (size_t i = 0; i < n_keys; ++i) {
+    const size_t len = std::min(B, n_bytes - i * B);
+    tl::sha256(k, 32, bytes + i * B, len, k);
     memcpy(out + 32 * i, k, 32);
   }
 }
 
+static size_t key_count(size_t n_bytes, size_t B, uint32_t flags) {
+  return (flags & TL_KEYS_TAIL) ? (n_bytes + B - 1) / B : n_bytes / B;
+}
+
 int tl_block_keys(const tl_ctx* ctx, const uint8_t* parent, const void* bytes, size_t n_bytes,
-                  size_t block_bytes, uint8_t* keys_out, size_t cap, size_t* n_keys) {
-  if (!ctx || !n_keys || (n_bytes && !bytes)) return TL_EINVAL;
+                  size_t block_bytes, uint32_t flags, uint8_t* keys_out, size_t cap, size_t* n_keys) {
+  if (!ctx || !n_keys || (n_bytes && !bytes) || (flags & ~uint32_t(TL_KEYS_TAIL))) return TL_EINVAL;
   const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->geo.block_tokens;
-  const size_t n_full = n_bytes / B;
-  *n_keys = n_full;
-  if (n_full > cap) return TL_ERANGE;
-  if (n_full && !keys_out) return TL_EINVAL;
-  chain(parent ? parent : ctx->ns, (const uint8_t*)bytes, n_full, B, keys_out);
+  const size_t nk = key_count(n_bytes, B, flags);
+  *n_keys = nk;
+  if (nk > cap) return TL_ERANGE;
+  if (nk && !keys_out) return TL_EINVAL;
+  chain(parent ? parent : ctx->ns, (const uint8_t*)bytes, n_bytes, nk, B, keys_out);
   return TL_OK;
 }
 
 int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* bytes,
                         const uint64_t* doc_off, const uint64_t* doc_len, size_t n_docs,
-                        size_t block_bytes, uint8_t* keys_out, const uint64_t* key_off,
+                        size_t block_bytes, uint32_t flags, uint8_t* keys_out, const uint64_t* key_off,
                         uint64_t* n_keys_out, int n_threads) {
   if (!ctx || (n_docs && (!bytes || !doc_off || !doc_len || !keys_out || !key_off))) return TL_EINVAL;
+  if (flags & ~uint32_t(TL_KEYS_TAIL)) return TL_EINVAL;
   const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->geo.block_tokens;
   std::atomic<size_t> next{0};
   auto work = [&]() {
     for (size_t d; (d = next.fetch_add(1)) < n_docs;) {
-      const size_t nf = doc_len[d] / B;
-      if (n_keys_out) n_keys_out[d] = nf;
-      chain(parents ? parents + 32 * d : ctx->ns, (const uint8_t*)bytes + doc_off[d], nf, B,
+      const size_t nk = key_count(doc_len[d], B, flags);
+      if (n_keys_out) n_keys_out[d] = nk;
+      chain(parents ? parents + 32 * d : ctx->ns, (const uint8_t*)bytes + doc_off[d], doc_len[d], nk, B,
             keys_out + 32 * key_off[d]);
     }
   };

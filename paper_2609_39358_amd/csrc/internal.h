@@ -19,6 +19,7 @@ constexpr uint32_t kIndexOffset = 64;    // block index (position)
 constexpr uint32_t kKeyOffset = 72;
 constexpr uint32_t kNsOffset = 104;
 constexpr uint32_t kPpbOffset = 152;     // pages per block
+constexpr uint32_t kTailOffset = 156;    // tokens of a partial last block (0: a full block)
 constexpr uint32_t kMaxPagesPerBlock = 1u << 16;
 static const char kMagic[9] = "TLSNKV01";
 static const char kNsTag[] = "taliesin-ns-v1";

@@ -224,6 +224,7 @@ struct SegArgs {
   uint32_t slab_major;   // 1: consecutive work items are consecutive blocks of one chunk
   uint32_t disabled;     // load checks switched off (sabotage build only; else 0)
   uint32_t* status;      // load: per-block status words
+  const uint32_t* n_tokens;  // [n] tokens per block, or null: every block full
 };
 
 struct MetaArgs {
@@ -239,6 +240,7 @@ struct MetaArgs {
   uint32_t* status;          // load: status words; save: unused
   uint8_t* out_status;       // save: per-block status bytes (optional)
   uint32_t disabled;         // load checks switched off (sabotage build only; else 0)
+  const uint32_t* n_tokens;  // [n] tokens per block, or null: every block full
   uint32_t tmpl[tl::kHeaderBytes / 4];
 };
 
@@ -378,8 +380,24 @@ __device__ __forceinline__ bool page_in_range(int32_t p, int64_t n_pages) {
 // True when every page id of block b, in every table a layer uses, lies in
 // [lo, n_pages). The wavefront checks the block's entries 64 at a time; all
 // lanes must be active.
+// Tokens of block b (the block size unless n_tokens gives a partial last
+// block); 0 when the given count is outside [1, block tokens].
+__device__ __forceinline__ uint32_t block_tok(const tl::Geo& g, const uint32_t* n_tokens, uint32_t b) {
+  if (!n_tokens) return g.block_tokens;
+  const uint32_t t = n_tokens[b];
+  return t >= 1 && t <= g.block_tokens ? t : 0;
+}
+
+// Pages of a block that hold its t tokens.
+__device__ __forceinline__ uint32_t pages_used(const tl::Geo& g, uint32_t t) {
+  return (t + g.page_tokens - 1) / g.page_tokens;
+}
+
+// Every page id of block b in [lo, n_pages); pages from `used` on (those of
+// a partial block that hold none of its tokens) may also be -1.
 __device__ __forceinline__ bool block_pages_ok(const tl::Geo& g, const int32_t* tables, uint32_t n,
-                                               uint32_t b, int64_t n_pages, int32_t lo, uint32_t lane) {
+                                               uint32_t b, int64_t n_pages, int32_t lo, uint32_t lane,
+                                               uint32_t used) {
   const uint64_t row = (uint64_t)n * g.ppb;
   bool bad = false;
   for (uint32_t grp = 0; grp < g.n_groups; ++grp) {
@@ -387,10 +405,27 @@ __device__ __forceinline__ bool block_pages_ok(const tl::Geo& g, const int32_t* 
     const int32_t* t = tables + grp * row + (uint64_t)b * g.ppb;
     for (uint32_t j = lane; j < g.ppb; j += 64) {
       const int32_t p = t[j];
-      bad |= p < lo || (int64_t)p >= n_pages;
+      bad |= p < (j < used ? lo : -1) || (int64_t)p >= n_pages;
     }
   }
   return !__any(bad);
+}
+
+// Writes `rows` zero rows to dst and returns this lane's column digest of
+// them: the chunk stored for a page that a partial block leaves out.
+__device__ uint64_t zero_hash(char* dst, uint32_t rows, uint32_t lane) {
+  gv4u* d = (gv4u*)dst + lane;
+  Column c;
+  c.init(lane);
+  const v4u z = zero4();
+  uint32_t r = 0;
+  for (; r + 2 <= rows; r += 2) {
+    st16(d + (uint64_t)r * 64, z);
+    st16(d + (uint64_t)(r + 1) * 64, z);
+    c.stripe(z, z);
+  }
+  if (r < rows) st16(d + (uint64_t)r * 64, z);
+  return c.finish(lane, rows, z);
 }
 
 __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
@@ -401,12 +436,14 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
     const uint64_t rec = a.rec[it.b];
     if (rec == 0 || (rec & 15)) continue;
     char* out = record_chunk(a, rec, it);
-    if (!block_pages_ok(a.g, a.tables, a.n, it.b, a.n_pages, 0, lane)) {
+    const uint32_t tk = block_tok(a.g, a.n_tokens, it.b);
+    if (tk == 0 || !block_pages_ok(a.g, a.tables, a.n, it.b, a.n_pages, 0, lane, pages_used(a.g, tk))) {
       zero_rows(out, it.rows, lane);  // k_save_meta zeroes the metadata
       continue;
     }
     const uint64_t leaf =
-        copy_hash<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(page_chunk(a, it), out, it.rows, lane);
+        it.page < 0 ? zero_hash(out, it.rows, lane)  // a page the partial block leaves out
+                    : copy_hash<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(page_chunk(a, it), out, it.rows, lane);
     const uint64_t digest = wave_sum64(leaf);
     if (lane == 0) *(uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t) = digest;
   }
@@ -454,12 +491,14 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
     return;
   }
   const uint32_t meta = (uint32_t)a.g.payload_offset;
-  if (!block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, 0, lane)) {
+  const uint32_t tk = block_tok(a.g, a.n_tokens, b);
+  if (tk == 0 || !block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, 0, lane, pages_used(a.g, tk))) {
     v4u* d = (v4u*)rec;
     for (uint32_t i = lane; i < meta / 16; i += 64) d[i] = zero4();
     if (lane == 0 && a.out_status) a.out_status[b] = TL_BADARG;
     return;
   }
+  const uint32_t tail = tk < a.g.block_tokens ? tk : 0;
   const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
   const uint32_t* tok = a.tokens + (uint64_t)a.g.block_tokens * b;
   const uint64_t bi = a.bidx[b];
@@ -473,11 +512,13 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
         if (o == tl::kIndexOffset) x = (uint32_t)bi;
         else if (o == tl::kIndexOffset + 4) x = (uint32_t)(bi >> 32);
         else if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) x = key32[(o - tl::kKeyOffset) / 4];
+        else if (o == tl::kTailOffset) x = tail;
         else x = a.tmpl[o / 4];  // root field is zero in the template
       } else if (o < a.g.tok_off) {
         x = *(const uint32_t*)(rec + o);  // chunk digest written by k_save_seg
       } else if (o < a.g.tok_end) {
-        x = tok[(o - a.g.tok_off) / 4];
+        const uint32_t wi = (o - a.g.tok_off) / 4;
+        x = wi < tk ? tok[wi] : 0;
       } else {
         x = 0;
       }
@@ -494,9 +535,9 @@ __global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
   }
   const uint64_t root = finish_root(acc, meta);
   if (lane == 0) {
-    // bytes 152..159 (pages per block, then zero) come from the expected header
+    // bytes 152..159: pages per block (from the expected header), then the tail field
     *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32),
-                                         a.tmpl[tl::kRootOffset / 4 + 2], a.tmpl[tl::kRootOffset / 4 + 3]};
+                                         a.tmpl[tl::kPpbOffset / 4], tail};
     if (a.out_status) a.out_status[b] = TL_ACCEPT;
   }
 }
@@ -523,11 +564,12 @@ __device__ __forceinline__ void load_meta_item(const MetaArgs& a, uint32_t b, ui
   const uint64_t rec = a.rec[b];
   const uint64_t len = a.len[b];
   // every lane takes part in the page-id check, so evaluate it up front
-  const bool pages_ok = block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, -1, lane);
+  const bool pages_ok = block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, -1, lane, a.g.ppb);
+  const uint32_t tk = block_tok(a.g, a.n_tokens, b);
   uint32_t code = 0;
   if (rec == 0) {
     code = TL_MISSING;
-  } else if ((rec & 15) || !pages_ok) {
+  } else if ((rec & 15) || !pages_ok || tk == 0) {
     code = TL_BADARG;
   } else if (len < a.g.record_bytes) {
     code = TL_TRUNCATED;
@@ -560,11 +602,14 @@ __device__ __forceinline__ void load_meta_item(const MetaArgs& a, uint32_t b, ui
         else if (o == tl::kIndexOffset + 4) pos_bad |= x != (uint32_t)(bi >> 32);
         else if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) key_bad |= x != key32[(o - tl::kKeyOffset) / 4];
         else if (o == tl::kRootOffset || o == tl::kRootOffset + 4) {}
+        else if (o == tl::kTailOffset) hdr_bad |= x != (tk < a.g.block_tokens ? tk : 0);
         else hdr_bad |= x != a.tmpl[o / 4];
       } else if (o < a.g.tok_off) {
         // chunk digests: checked by the chunk items, covered by the root
       } else if (o < a.g.tok_end) {
-        if (tok) tok_bad |= x != tok[(o - a.g.tok_off) / 4];
+        const uint32_t wi = (o - a.g.tok_off) / 4;
+        if (wi >= tk) hdr_bad |= x != 0;  // the padding after a partial block's tokens
+        else if (tok) tok_bad |= x != tok[wi];
       } else {
         hdr_bad |= x != 0;
       }
@@ -654,7 +699,8 @@ __global__ __launch_bounds__(256) void k_load_final(FinalArgs f) {
 }
 
 void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, const int32_t* tables,
-              const tl_cache* c, uint32_t* status, uint32_t layer_begin = 0, uint32_t layer_end = 0) {
+              const uint32_t* n_tokens, const tl_cache* c, uint32_t* status, uint32_t layer_begin = 0,
+              uint32_t layer_end = 0) {
   if (layer_end == 0) layer_end = ctx->geo.n_layers;
   a.g = ctx->geo;
   a.rec = rec;
@@ -672,6 +718,7 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.slab_major = 0;
   a.disabled = g_disabled_checks;
   a.status = status;
+  a.n_tokens = n_tokens;
 }
 
 void fill_meta(MetaArgs& m, const tl_ctx* ctx, size_t n, const uint64_t* rec, const uint64_t* len,
@@ -688,6 +735,7 @@ void fill_meta(MetaArgs& m, const tl_ctx* ctx, size_t n, const uint64_t* rec, co
   m.status = status;
   m.out_status = out_status;
   m.disabled = g_disabled_checks;
+  m.n_tokens = blk->d_n_tokens;
   __builtin_memcpy(m.tmpl, ctx->header_template, sizeof m.tmpl);
 }
 
@@ -731,7 +779,7 @@ int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache
                        uint32_t layer_end) {
   hipStream_t s = (hipStream_t)stream;
   SegArgs a;
-  fill_seg(a, ctx, n, d_rec, blk->d_tables, src, nullptr, layer_begin, layer_end);
+  fill_seg(a, ctx, n, d_rec, blk->d_tables, blk->d_n_tokens, src, nullptr, layer_begin, layer_end);
   a.slab_major = TL_SAVE_SLAB_MAJOR;
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
@@ -765,7 +813,7 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
   hipStream_t s = (hipStream_t)stream;
   LoadArgs la;
   fill_meta(la.m, ctx, n, d_rec, d_len, blk, dst->n_pages, d_ws, nullptr);
-  fill_seg(la.s, ctx, n, d_rec, blk->d_tables, dst, d_ws);
+  fill_seg(la.s, ctx, n, d_rec, blk->d_tables, blk->d_n_tokens, dst, d_ws);
   la.s.len = d_len;
   la.s.slab_major = TL_LOAD_SLAB_MAJOR;
   FinalArgs f;

@@ -55,7 +55,8 @@ class tl_cache(ctypes.Structure):
 
 class tl_blocks(ctypes.Structure):
     _fields_ = [("d_keys", ctypes.c_void_p), ("d_block_index", ctypes.c_void_p),
-                ("d_tokens", ctypes.c_void_p), ("d_tables", ctypes.c_void_p)]
+                ("d_tokens", ctypes.c_void_p), ("d_tables", ctypes.c_void_p),
+                ("d_n_tokens", ctypes.c_void_p)]
 
 
 class tl_chains(ctypes.Structure):
@@ -81,9 +82,9 @@ def _load():
         "tl_ctx_geometry": (c.c_int, [P, c.POINTER(tl_geometry)]),
         "tl_ns_digest": (c.c_int, [P, P]),
         "tl_workspace_bytes": (c.c_size_t, [P, c.c_size_t]),
-        "tl_block_keys": (c.c_int, [P, P, P, c.c_size_t, c.c_size_t, P, c.c_size_t,
+        "tl_block_keys": (c.c_int, [P, P, P, c.c_size_t, c.c_size_t, c.c_uint32, P, c.c_size_t,
                                     c.POINTER(c.c_size_t)]),
-        "tl_block_keys_batch": (c.c_int, [P, P, P, P, P, c.c_size_t, c.c_size_t, P, P, P, c.c_int]),
+        "tl_block_keys_batch": (c.c_int, [P, P, P, P, P, c.c_size_t, c.c_size_t, c.c_uint32, P, P, P, c.c_int]),
         "tl_save": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P, P]),
         "tl_save_layers": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P,
                                      c.c_uint32, c.c_uint32]),
@@ -142,6 +143,7 @@ KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_
            "stage": 6, "index": 7}
 TL_INDEX_STORED, TL_INDEX_FULL, TL_INDEX_TAG_CLASH = 0x01, 0x20, 0x21
 TL_CHAIN_ALL_KEYS = 1
+TL_KEYS_TAIL = 1
 MISS = 2**64 - 1
 
 
@@ -239,27 +241,29 @@ def tl_workspace_bytes(ctx: Ctx, n_blocks: int) -> int:
     return int(_lib.tl_workspace_bytes(ctx.handle, n_blocks))
 
 
-def tl_block_keys(ctx: Ctx, data, parent: Optional[bytes] = None, block_bytes: int = 0) -> np.ndarray:
-    """Chained keys of every full block of `data`, as uint8 [n, 32]."""
+def tl_block_keys(ctx: Ctx, data, parent: Optional[bytes] = None, block_bytes: int = 0,
+                  tail: bool = False) -> np.ndarray:
+    """Chained keys of every full block of `data` (and of a partial last
+    block with tail=True), as uint8 [n, 32]."""
     buf = _host_buf(data)
     B = block_bytes or ctx.block_bytes
-    n_full = len(buf) // B
-    out = np.empty((n_full, KEY_BYTES), dtype=np.uint8)
+    n = -(-len(buf) // B) if tail else len(buf) // B
+    out = np.empty((n, KEY_BYTES), dtype=np.uint8)
     nk = ctypes.c_size_t(0)
     par = None if parent is None else bytes(parent)
-    _check(_lib.tl_block_keys(ctx.handle, par, buf, len(buf), block_bytes, out.ctypes.data, n_full,
-                              ctypes.byref(nk)), "tl_block_keys")
+    _check(_lib.tl_block_keys(ctx.handle, par, buf, len(buf), block_bytes, TL_KEYS_TAIL if tail else 0,
+                              out.ctypes.data, n, ctypes.byref(nk)), "tl_block_keys")
     return out
 
 
 def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int = 0,
-                        n_threads: int = 0):
+                        n_threads: int = 0, tail: bool = False):
     """Keys for several documents in parallel; returns a list of [n_i, 32] arrays."""
     bufs = [_host_buf(d) for d in docs]
     B = block_bytes or ctx.block_bytes
     lens = np.array([len(b) for b in bufs], dtype=np.uint64)
     offs = np.concatenate([[0], np.cumsum(lens)[:-1]]).astype(np.uint64) if bufs else np.zeros(0, np.uint64)
-    nk = lens // np.uint64(B)
+    nk = (lens + np.uint64(B - 1)) // np.uint64(B) if tail else lens // np.uint64(B)
     koff = np.concatenate([[0], np.cumsum(nk)[:-1]]).astype(np.uint64) if bufs else np.zeros(0, np.uint64)
     allb = b"".join(bufs)
     keys = np.empty((int(nk.sum()), KEY_BYTES), dtype=np.uint8)
@@ -269,7 +273,8 @@ def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int
         par = np.ascontiguousarray(np.asarray(parents, dtype=np.uint8).reshape(len(bufs), 32))
     _check(_lib.tl_block_keys_batch(ctx.handle, None if par is None else par.ctypes.data, allb or None,
                                     offs.ctypes.data, lens.ctypes.data, len(bufs), block_bytes,
-                                    keys.ctypes.data, koff.ctypes.data, nout.ctypes.data, n_threads),
+                                    TL_KEYS_TAIL if tail else 0, keys.ctypes.data, koff.ctypes.data,
+                                    nout.ctypes.data, n_threads),
            "tl_block_keys_batch")
     return [keys[int(o):int(o) + int(k)] for o, k in zip(koff, nk)]
 
@@ -281,9 +286,10 @@ def make_cache(d_layer_k, d_layer_v, page_stride: int, n_pages: int) -> tl_cache
     return c
 
 
-def make_blocks(d_keys, d_block_index, d_tokens, d_tables) -> tl_blocks:
-    b = tl_blocks(_addr(d_keys), _addr(d_block_index), _addr(d_tokens), _addr(d_tables))
-    b._keep = (d_keys, d_block_index, d_tokens, d_tables)
+def make_blocks(d_keys, d_block_index, d_tokens, d_tables, d_n_tokens=None) -> tl_blocks:
+    """d_n_tokens: device u32 [n] tokens per block (partial last blocks), or None."""
+    b = tl_blocks(_addr(d_keys), _addr(d_block_index), _addr(d_tokens), _addr(d_tables), _addr(d_n_tokens))
+    b._keep = (d_keys, d_block_index, d_tokens, d_tables, d_n_tokens)
     return b
 
 

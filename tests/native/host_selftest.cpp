@@ -96,16 +96,21 @@ int main() {
   // key chain: single document, capacity error, tail, explicit parent, threads
   std::vector<uint32_t> toks(16 * 40 + 7);
   for (auto& t : toks) t = rnd() % 32000;
-  std::vector<uint8_t> keys(32 * 40), keys2(32 * 40);
+  std::vector<uint8_t> keys(32 * 40), keys2(32 * 41);
   size_t nk = 0;
-  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, keys.data(), 40, &nk) == TL_OK && nk == 40);
-  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, keys2.data(), 39, &nk) == TL_ERANGE);
-  EXPECT(tl_block_keys(c, nullptr, nullptr, 0, 0, nullptr, 0, &nk) == TL_OK && nk == 0);
-  EXPECT(tl_block_keys(c, nullptr, nullptr, 8, 0, nullptr, 0, &nk) == TL_EINVAL);
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, 0, keys.data(), 40, &nk) == TL_OK && nk == 40);
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, 0, keys2.data(), 39, &nk) == TL_ERANGE);
+  EXPECT(tl_block_keys(c, nullptr, nullptr, 0, 0, 0, nullptr, 0, &nk) == TL_OK && nk == 0);
+  EXPECT(tl_block_keys(c, nullptr, nullptr, 8, 0, 0, nullptr, 0, &nk) == TL_EINVAL);
   std::vector<uint64_t> off = {0, 64 * 10, 64 * 25}, len = {64 * 10, 64 * 15 + 3, 64 * 15 + 28}, koff = {0, 10, 25}, nko(3);
-  EXPECT(tl_block_keys_batch(c, nullptr, toks.data(), off.data(), len.data(), 3, 0, keys2.data(), koff.data(), nko.data(), 3) == TL_OK);
+  EXPECT(tl_block_keys_batch(c, nullptr, toks.data(), off.data(), len.data(), 3, 0, 0, keys2.data(), koff.data(), nko.data(), 3) == TL_OK);
   EXPECT(nko[0] == 10 && nko[1] == 15 && nko[2] == 15);
   EXPECT(!memcmp(keys.data(), keys2.data(), 32 * 10));  // the first document is the prefix of the first chain
+  // a partial last block gets a key only when asked; it extends the full chain
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, TL_KEYS_TAIL, keys2.data(), 41, &nk) == TL_OK &&
+         nk == 41 && !memcmp(keys.data(), keys2.data(), 32 * 40));
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), 16 * 40 * 4, 0, TL_KEYS_TAIL, keys2.data(), 41, &nk) == TL_OK && nk == 40);
+  EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, 2, keys2.data(), 41, &nk) == TL_EINVAL);
   // index: fill to capacity, overwrite, miss, full
   tl_index* idx = tl_index_create(500);
   std::vector<uint8_t> ik(32 * 600);

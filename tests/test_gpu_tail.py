@@ -1,0 +1,139 @@
+"""Partial last blocks on the GPU against the oracle: records saved with a
+token count below the block size (tail field, zero-padded token area, pages
+the tail does not use stored as zero slabs when their table entry is -1),
+restored with their count, and refused when loaded with another count."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+from paper_2609_39358_amd import taliesin as T
+from paper_2609_39358_amd.device import PagedCache, RecordStore
+from tests.gpu_case import DEV, Case, host_layers, i32, i64, log, random_fill
+
+pytestmark = pytest.mark.gpu
+
+GEOMS = {
+    "one_page": wl.Geometry(2, 4, 64, 16),
+    "three_pages": wl.Geometry(2, 2, 64, 4, pages_per_block=3),
+}
+
+
+def geom_of(name):
+    if name == "groups":
+        g = wl.hybrid_geometry(n_layers=4, n_kv_heads=2, head_dim=64, page_tokens=8, window=8, period=2)
+        return wl.Geometry(g.n_layers, g.n_kv_heads, g.head_dim, g.page_tokens, g.dtype, g.layer_window,
+                           g.layer_group, pages_per_block=2)
+    return GEOMS[name]
+
+
+def counts(bt, n, seed):
+    """Block sizes: mostly full, every fifth block a tail of 1..bt-1 tokens."""
+    rng = np.random.default_rng(seed)
+    return np.array([bt if b % 5 else int(rng.integers(1, bt)) for b in range(n)], np.uint32)
+
+
+def tail_tables(c, table, n_tok):
+    """Copy of [G][n*ppb] with -1 on the pages a tail block does not use."""
+    t = np.array(table, np.int32, copy=True)
+    ppb, P = c.geom.pages_per_block, c.geom.page_tokens
+    for b, k in enumerate(n_tok):
+        used = -(-int(k) // P)
+        t[:, b * ppb + used:(b + 1) * ppb] = -1
+    return t
+
+
+@pytest.mark.parametrize("name", ["one_page", "three_pages", "groups"])
+def test_tail_blocks_save_and_load(name):
+    geom = geom_of(name)
+    n = 20
+    c = Case(geom, n, 64, 64, seed=30)
+    c.make_src()
+    bt = c.lay.block_tokens
+    n_tok = counts(bt, n, 31)
+    assert (n_tok < bt).sum() >= 3
+    d_ntok = i32(n_tok.view(np.int32))
+    t_src = tail_tables(c, c.t_src, n_tok)
+    t_dst = tail_tables(c, c.t_dst, n_tok)
+    # save
+    store = RecordStore(n, c.lay.record_bytes, DEV)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    d_ts = i32(t_src)
+    log(name, "save", n, "blocks,", int((n_tok < bt).sum()), "tails")
+    T.tl_save(c.ctx, torch.cuda.current_stream(), n, c.src.tl(),
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, d_ts, d_ntok), store.ptrs, st)
+    torch.cuda.synchronize()
+    hk, hv = host_layers(c.src)
+    recs, st_o = ref.save(c.lay, c.ns, hk, hv, t_src, [k.tobytes() for k in c.keys], c.bidx, c.tokens,
+                          n_pages=64, n_tokens=n_tok)
+    assert [int(x) for x in st.cpu()] == st_o == [ref.ACCEPT] * n
+    for b in range(n):
+        assert store.buf[b].cpu().numpy().tobytes() == recs[b], b
+    # load with the right counts, one damaged tail
+    tb = int(np.nonzero(n_tok < bt)[0][1])
+    store.buf[tb, c.lay.payload_offset + 5] ^= 0x01
+    recs[tb] = bytearray(recs[tb])
+    recs[tb][c.lay.payload_offset + 5] ^= 0x01
+    recs[tb] = bytes(recs[tb])
+    dst = random_fill(PagedCache(geom.n_layers, 64, c.stride, DEV), 32)
+    hk0, hv0 = host_layers(dst)
+    ws_b = T.tl_workspace_bytes(c.ctx, n)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    verd = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    d_td = i32(t_dst)
+    T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, d_td, d_ntok), dst.tl(), verd, ws, ws_b)
+    torch.cuda.synchronize()
+    vo = ref.restore(c.lay, c.ns, recs, [k.tobytes() for k in c.keys], c.bidx, c.tokens, t_dst, hk0, hv0,
+                     n_pages=64, n_tokens=n_tok)
+    assert [int(x) for x in verd.cpu()] == vo
+    assert vo[tb] == ref.SEGMENT and vo.count(ref.ACCEPT) == n - 1
+    got_k, got_v = host_layers(dst)
+    for l in range(geom.n_layers):
+        assert np.array_equal(got_k[l], hk0[l]) and np.array_equal(got_v[l], hv0[l])
+    # the same records loaded as full blocks, and with counts off by one, or invalid
+    for label, alt in (("full", np.full(n, bt, np.uint32)), ("plus_one", np.minimum(n_tok + 1, bt)),
+                       ("minus_one", np.maximum(n_tok - 1, 1))):
+        T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
+                  T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, d_td, i32(alt.view(np.int32))), dst.tl(), verd, ws,
+                  ws_b)
+        torch.cuda.synchronize()
+        v = [int(x) for x in verd.cpu()]
+        hk1, hv1 = host_layers(dst)
+        vo = ref.restore(c.lay, c.ns, recs, [k.tobytes() for k in c.keys], c.bidx, c.tokens, t_dst, hk1, hv1,
+                         n_pages=64, n_tokens=alt)
+        assert v == vo, label
+        for b in range(n):
+            if alt[b] != n_tok[b]:
+                assert v[b] == ref.HEADER, (label, b)
+    bad = n_tok.copy()
+    bad[3], bad[7] = 0, bt + 1
+    T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, d_td, i32(bad.view(np.int32))), dst.tl(), verd, ws, ws_b)
+    torch.cuda.synchronize()
+    v = verd.cpu().numpy()
+    assert v[3] == ref.BADARG and v[7] == ref.BADARG
+
+
+def test_tail_save_refuses_missing_pages_that_hold_tokens():
+    geom = geom_of("three_pages")
+    n = 6
+    c = Case(geom, n, 32, 32, seed=33)
+    c.make_src()
+    n_tok = np.array([12, 5, 12, 4, 12, 9], np.uint32)
+    t_src = tail_tables(c, c.t_src, n_tok)
+    t_src[0, 1 * 3 + 1] = -1  # block 1 (5 tokens) needs pages 0 and 1
+    store = RecordStore(n, c.lay.record_bytes, DEV)
+    store.buf.fill_(0x11)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    T.tl_save(c.ctx, torch.cuda.current_stream(), n, c.src.tl(),
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_src), i32(n_tok.view(np.int32))), store.ptrs, st)
+    torch.cuda.synchronize()
+    hk, hv = host_layers(c.src)
+    recs, st_o = ref.save(c.lay, c.ns, hk, hv, t_src, [k.tobytes() for k in c.keys], c.bidx, c.tokens,
+                          n_pages=32, n_tokens=n_tok)
+    assert [int(x) for x in st.cpu()] == st_o
+    assert st_o[1] == ref.BADARG and st_o.count(ref.ACCEPT) == n - 1
+    for b in range(n):
+        assert store.buf[b].cpu().numpy().tobytes() == recs[b], b

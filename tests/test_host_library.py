@@ -122,8 +122,11 @@ def test_block_keys_capacity_error():
     n = ctypes.c_size_t(0)
     buf = bytes(64 * 3)
     out = (ctypes.c_uint8 * 64)()
-    st = T.lib().tl_block_keys(c.handle, None, buf, len(buf), 0, out, 2, ctypes.byref(n))
+    st = T.lib().tl_block_keys(c.handle, None, buf, len(buf), 0, 0, out, 2, ctypes.byref(n))
     assert st == T.TL_ERANGE and n.value == 3
+    st = T.lib().tl_block_keys(c.handle, None, buf + bytes(5), len(buf) + 5, 0, T.TL_KEYS_TAIL, out, 3,
+                               ctypes.byref(n))
+    assert st == T.TL_ERANGE and n.value == 4
 
 
 def test_batch_keys_match_single_chains():
@@ -137,6 +140,19 @@ def test_batch_keys_match_single_chains():
     got = T.tl_block_keys_batch(c, docs, parents=pars, n_threads=3)
     for d, k, p in zip(docs, got, pars):
         assert np.array_equal(k, T.tl_block_keys(c, d, parent=p.tobytes()))
+
+
+def test_tail_keys_match_oracle():
+    """Partial last blocks: the library's keys equal the oracle's, single and batched."""
+    cfg = wl.CONFIGS[3]
+    c = _ctx(cfg)
+    ns = T.tl_ns_digest(c)
+    docs = [wl.tokens(n, 6, i) for i, n in enumerate([0, 1, 15, 16, 17, 1000, 4099])]
+    got = T.tl_block_keys_batch(c, docs, n_threads=3, tail=True)
+    for d, k in zip(docs, got):
+        want = ref.block_keys(ns, d.tobytes(), 64, tail=True)
+        assert [x.tobytes() for x in k] == want
+        assert np.array_equal(T.tl_block_keys(c, d, tail=True), k)
 
 
 def test_index_put_get():
