@@ -323,7 +323,8 @@ int tl_dindex_stats(const tl_dindex* idx, void* stream, uint64_t* d_out);
  * slot slot_off[c] + k. Offsets are clamped to n_tokens / n_slots, so an
  * inconsistent offset array yields fewer blocks, never an access outside the
  * arrays: chain c has n_c = min(floor(tokens / tokens per block), slots)
- * blocks. To pass the per-slot arrays to tl_load whole, the slot ranges
+ * blocks, plus its partial last block under TL_CHAIN_TAIL when a slot is
+ * left for it. To pass the per-slot arrays to tl_load whole, the slot ranges
  * should tile [0, n_slots). */
 typedef struct tl_chains {
   const uint32_t* d_tokens;      /* token ids of every chain, back to back */
@@ -338,6 +339,10 @@ typedef struct tl_chains {
 } tl_chains;
 
 #define TL_CHAIN_ALL_KEYS 1 /* flag: keep computing keys past the first miss */
+#define TL_CHAIN_TAIL 2     /* flag: a chain's partial last block (its last
+                               tokens, fewer than a block, if it has any and
+                               a slot is left for it) is keyed as its last
+                               block, as TL_KEYS_TAIL does on the host */
 
 /* Keys and lookup, one lane per chain (fewer than 2^24 chains). Without an
  * index: every block's key is written (slots [0, n_c) of each chain) and
@@ -354,14 +359,17 @@ int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_c
 
 /* Block fingerprints for a token index: d_out[b] = SHA-256(namespace digest
  * | u64 little-endian d_block_index[b] | the block's token ids) for n blocks
- * (device d_tokens [n][tokens per block], d_block_index [n], d_out [n][32]).
+ * (device d_tokens [n][tokens per block], d_block_index [n], d_out [n][32];
+ * d_n_tokens [n] or NULL: the tokens of a partial last block, which alone
+ * are hashed; a count outside [1, tokens per block] counts as full).
  * A token index is a tl_dindex from these fingerprints to the handles of the
  * stored blocks (the same handles as in the key index). */
 int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
-                          const uint64_t* d_block_index, uint8_t* d_out);
+                          const uint64_t* d_block_index, const uint32_t* d_n_tokens, uint8_t* d_out);
 
-/* Same results as tl_chain_lookup with flags 0 (d_hits, d_handles for slots
- * [0, n_c), d_keys for slots [0, min(hits + 1, n_c))), computed for all
+/* Same results as tl_chain_lookup with the same flags (0 or TL_CHAIN_TAIL:
+ * d_hits, d_handles for slots [0, n_c), d_keys for slots
+ * [0, min(hits + 1, n_c))), computed for all
  * blocks of a chain at once instead of one after another: the token index
  * `tok_idx` proposes for each block the chain key of a stored block with the
  * same tokens at the same position (d_handle_keys [n_handles][32]: the key
@@ -374,7 +382,8 @@ int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint3
  * chain; fewer than 2^24 chains. */
 int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
                         const tl_dindex* idx, const tl_dindex* tok_idx, const uint8_t* d_handle_keys,
-                        uint64_t n_handles, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits);
+                        uint64_t n_handles, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,
+                        uint32_t* d_hits);
 
 /* tl_load's per-block inputs from a lookup, for every slot of every chain's
  * range (n_slots blocks): slot k of chain c is a hit when k < d_hits[c] and
@@ -385,14 +394,18 @@ int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const 
  * n_c); d_tables_out (device [n_groups][n_slots * pages_per_block] or NULL)
  * = the page ids of d_tables_in (same shape; NULL: page j of slot q is
  * q * pages_per_block + j in every group) for hits and -1 for every other
- * slot, so that tl_load neither reads nor writes pages for it. The two may
- * be the same array. d_keys from tl_chain_lookup serve as tl_blocks.d_keys
+ * slot, so that tl_load neither reads nor writes pages for it; a restored
+ * partial block gets -1 on the pages that hold none of its tokens. The two
+ * may be the same array. flags: the lookup's TL_CHAIN_TAIL. d_n_tokens_out
+ * (device [n_slots] or NULL) = each slot's token count, for
+ * tl_blocks.d_n_tokens. d_keys from tl_chain_lookup serve as tl_blocks.d_keys
  * unchanged. */
 int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
-                   const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_handle_ptrs,
-                   const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,
-                   uint64_t* d_record_lens, uint64_t* d_block_index, uint32_t* d_tokens_out,
-                   const int32_t* d_tables_in, int32_t* d_tables_out);
+                   uint32_t flags, const uint32_t* d_hits, const uint64_t* d_handles,
+                   const uint64_t* d_handle_ptrs, const uint64_t* d_handle_lens, uint64_t n_handles,
+                   uint64_t* d_record_ptrs, uint64_t* d_record_lens, uint64_t* d_block_index,
+                   uint32_t* d_tokens_out, uint32_t* d_n_tokens_out, const int32_t* d_tables_in,
+                   int32_t* d_tables_out);
 
 /* ---- record files: the disk tier ------------------------------------------
  * Records of one context kept back to back in one file (record id i at byte

@@ -117,7 +117,7 @@ __device__ __forceinline__ void sha_tokens(uint32_t (&out)[8], const uint32_t (&
 struct MsgLen {
   uint32_t nb, hi, lo;
 };
-inline MsgLen msg_len(uint32_t pw, uint32_t bt) {
+__host__ __device__ inline MsgLen msg_len(uint32_t pw, uint32_t bt) {
   const uint64_t bytes = 4ull * pw + 4ull * bt;
   return MsgLen{(uint32_t)((bytes + 8) / 64 + 1), (uint32_t)((bytes * 8) >> 32), (uint32_t)(bytes * 8)};
 }
@@ -282,19 +282,22 @@ struct ChainIn {
   const uint64_t* first_block;
   uint32_t n_chains;
   uint32_t bt;     // tokens per block
-  MsgLen key;      // chain key message
-  MsgLen fp;       // fingerprint message
+  uint32_t tail;   // 1: a chain's partial last block is keyed too
+  MsgLen key;      // chain key message of a full block
+  MsgLen fp;       // fingerprint message of a full block
   uint32_t ns[8];  // namespace digest as big-endian words
 };
 
 struct Range {
-  uint64_t t0, s0, n;  // first token, first slot, blocks
+  uint64_t t0, s0, n;  // first token, first slot, blocks (full ones, then the tail if keyed)
   uint64_t slots;      // slots in the chain's range
+  uint64_t full;       // full blocks among the n
+  uint32_t tail_tok;   // tokens of the keyed partial last block, 0 if none
 };
 
 __device__ __forceinline__ Range chain_range(const uint64_t* tok_off, const uint64_t* slot_off,
                                              uint64_t n_tokens, uint64_t n_slots, uint32_t bt,
-                                             uint32_t c) {
+                                             uint32_t tail, uint32_t c) {
   Range r;
   const uint64_t a = tok_off[c], b = tok_off[c + 1];
   r.t0 = a < n_tokens ? a : n_tokens;
@@ -303,13 +306,21 @@ __device__ __forceinline__ Range chain_range(const uint64_t* tok_off, const uint
   r.s0 = p < n_slots ? p : n_slots;
   const uint64_t s1 = q < r.s0 ? r.s0 : (q < n_slots ? q : n_slots);
   r.slots = s1 - r.s0;
-  const uint64_t nk = (t1 - r.t0) / bt;
-  r.n = nk < r.slots ? nk : r.slots;
+  const uint64_t nf = (t1 - r.t0) / bt;
+  const uint32_t rem = (uint32_t)(t1 - r.t0 - nf * bt);
+  r.full = nf < r.slots ? nf : r.slots;
+  r.tail_tok = tail && rem && nf < r.slots ? rem : 0;
+  r.n = r.full + (r.tail_tok ? 1 : 0);
   return r;
 }
 
 __device__ __forceinline__ Range chain_range(const ChainIn& in, uint32_t c) {
-  return chain_range(in.tok_off, in.slot_off, in.n_tokens, in.n_slots, in.bt, c);
+  return chain_range(in.tok_off, in.slot_off, in.n_tokens, in.n_slots, in.bt, in.tail, c);
+}
+
+// Tokens of block k of a chain.
+__device__ __forceinline__ uint32_t block_len(const Range& r, uint64_t k, uint32_t bt) {
+  return k < r.full ? bt : r.tail_tok;
 }
 
 __device__ __forceinline__ void parent_words(uint32_t (&h)[8], const ChainIn& in, uint32_t c) {
@@ -324,8 +335,9 @@ __device__ __forceinline__ void parent_words(uint32_t (&h)[8], const ChainIn& in
 }
 
 __device__ __forceinline__ void chain_key(uint32_t (&out)[8], const ChainIn& in, const uint32_t (&prev)[8],
-                                          const uint32_t* tok) {
-  sha_tokens<8>(out, prev, tok, in.bt, in.key.nb, in.key.hi, in.key.lo);
+                                          const uint32_t* tok, uint32_t len) {
+  const MsgLen m = len == in.bt ? in.key : msg_len(8, len);
+  sha_tokens<8>(out, prev, tok, len, m.nb, m.hi, m.lo);
 }
 
 __device__ __forceinline__ void store_key(uint8_t* keys, uint64_t slot, const uint32_t (&h)[8]) {
@@ -360,7 +372,7 @@ __device__ uint64_t seq_walk(const ChainIn& in, const Dx& x, bool all_keys, cons
   for (uint64_t k = k0; k <= r.n; ++k) {
     uint32_t nk[8];
     const bool compute = k < r.n && (!missed || all_keys);
-    if (compute) chain_key(nk, in, cur, in.tokens + r.t0 + k * in.bt);
+    if (compute) chain_key(nk, in, cur, in.tokens + r.t0 + k * in.bt, block_len(r, k, in.bt));
     if (pending) {
       const uint64_t hv = resolve(x, kw, sv, maxp);
       if (hv == kMiss) {
@@ -416,20 +428,22 @@ __global__ __launch_bounds__(64) void k_chain(ChainArgs a) {
 // ids), the key of the token index that proposes, for a block of a request,
 // the chain key of a stored block with the same tokens at the same position.
 __device__ __forceinline__ void fingerprint(uint32_t (&out)[8], const ChainIn& in, uint64_t pos,
-                                            const uint32_t* tok) {
+                                            const uint32_t* tok, uint32_t len) {
   uint32_t pre[10];
 #pragma unroll
   for (int i = 0; i < 8; ++i) pre[i] = in.ns[i];
   pre[8] = __builtin_bswap32((uint32_t)pos);
   pre[9] = __builtin_bswap32((uint32_t)(pos >> 32));
-  sha_tokens<10>(out, pre, tok, in.bt, in.fp.nb, in.fp.hi, in.fp.lo);
+  const MsgLen m = len == in.bt ? in.fp : msg_len(10, len);
+  sha_tokens<10>(out, pre, tok, len, m.nb, m.hi, m.lo);
 }
 
 struct FpArgs {
   ChainIn in;
-  const uint32_t* tokens;  // [n][bt]
-  const uint64_t* pos;     // [n]
-  uint8_t* out;            // [n][32]
+  const uint32_t* tokens;    // [n][bt]
+  const uint64_t* pos;       // [n]
+  const uint32_t* n_tokens;  // [n] or null (all full); a count outside [1, bt] counts as bt
+  uint8_t* out;              // [n][32]
   uint32_t n;
 };
 
@@ -437,7 +451,9 @@ __global__ __launch_bounds__(256) void k_fingerprint(FpArgs a) {
   const uint32_t step = gridDim.x * 256;
   for (uint32_t b = blockIdx.x * 256 + threadIdx.x; b < a.n; b += step) {
     uint32_t f[8];
-    fingerprint(f, a.in, a.pos[b], a.tokens + (uint64_t)b * a.in.bt);
+    uint32_t len = a.n_tokens ? a.n_tokens[b] : a.in.bt;
+    if (len < 1 || len > a.in.bt) len = a.in.bt;
+    fingerprint(f, a.in, a.pos[b], a.tokens + (uint64_t)b * a.in.bt, len);
     store_key(a.out, b, f);
   }
 }
@@ -488,11 +504,12 @@ __global__ __launch_bounds__(kParThreads) void k_chain_par(ParArgs a) {
       const uint64_t k = t0 + tid;
       const bool live = k < r.n;
       const uint32_t* tok = a.in.tokens + r.t0 + k * a.in.bt;
+      const uint32_t len = block_len(r, k, a.in.bt);
       if (tid == 0) first = 0xffffffffu;
       uint32_t hc = 0;
       if (live) {
         uint32_t f[8];
-        fingerprint(f, a.in, pos0 + k, tok);
+        fingerprint(f, a.in, pos0 + k, tok, len);
         uint64_t fw[4];
         key_words(fw, f);
         const uint64_t h = probe_from(a.t, fw, tmaxp, 0);
@@ -509,7 +526,7 @@ __global__ __launch_bounds__(kParThreads) void k_chain_par(ParArgs a) {
         uint32_t prev[8], ck[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) prev[i] = cand[tid][i];
-        chain_key(ck, a.in, prev, tok);
+        chain_key(ck, a.in, prev, tok, len);
         store_key(a.keys, r.s0 + k, ck);
         uint64_t kw[4];
         key_words(kw, ck);
@@ -547,7 +564,7 @@ __global__ __launch_bounds__(kParThreads) void k_chain_par(ParArgs a) {
         uint32_t prev[8], cur[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) prev[i] = cand[l][i];
-        chain_key(cur, a.in, prev, a.in.tokens + r.t0 + stop * a.in.bt);
+        chain_key(cur, a.in, prev, a.in.tokens + r.t0 + stop * a.in.bt, block_len(r, stop, a.in.bt));
         seq_hits = stop + 1 + seq_walk(a.in, a.x, false, r, stop + 1, cur, a.keys, a.handles);
       }
       __syncthreads();
@@ -570,7 +587,10 @@ struct StageArgs {
   uint32_t n_chains;
   uint32_t bt;
   uint32_t ppb;
+  uint32_t page_tokens;
   uint32_t n_groups;
+  uint32_t tail;               // chains key their partial last block
+  uint32_t* n_tokens_out;      // [n_slots] tokens per slot, or null
   const uint32_t* hits;
   const uint64_t* handles;
   const uint64_t* hptr;
@@ -595,7 +615,7 @@ __device__ __forceinline__ bool stage_hit(const StageArgs& a, uint64_t slot, uin
 __global__ __launch_bounds__(64) void k_chain_stage(StageArgs a) {
   const uint32_t lane = threadIdx.x;
   for (uint32_t c = blockIdx.x; c < a.n_chains; c += gridDim.x) {
-    const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, c);
+    const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, a.tail, c);
     const uint64_t hits_raw = a.hits[c];
     const uint64_t hits = hits_raw < r.n ? hits_raw : r.n;
     const uint64_t first = a.first_block ? a.first_block[c] : 0;
@@ -606,19 +626,22 @@ __global__ __launch_bounds__(64) void k_chain_stage(StageArgs a) {
       a.rec_ptrs[q] = hit ? a.hptr[h] : 0;
       a.rec_lens[q] = hit ? a.hlen[h] : 0;
       a.bidx[q] = first + k;
+      if (a.n_tokens_out) a.n_tokens_out[q] = k == r.full && r.tail_tok ? r.tail_tok : a.bt;
     }
     if (a.tokens_out) {
-      const uint64_t n_tok = r.slots * a.bt, have = r.n * a.bt;
+      const uint64_t n_tok = r.slots * a.bt, have = r.full * a.bt + r.tail_tok;
       uint32_t* dst = a.tokens_out + r.s0 * a.bt;
       const uint32_t* src = a.tokens + r.t0;
       for (uint64_t e = lane; e < n_tok; e += 64) dst[e] = e < have ? src[e] : 0;
     }
     if (a.tables_out) {
       const uint64_t per = r.slots * a.ppb, row = a.n_slots * a.ppb;
+      // a restored partial block restores only the pages holding its tokens
+      const uint64_t tail_pages = (r.tail_tok + a.page_tokens - 1) / a.page_tokens;
       for (uint64_t e = lane; e < per; e += 64) {
-        const uint64_t k = e / a.ppb, at = r.s0 * a.ppb + e;
+        const uint64_t k = e / a.ppb, j = e - k * a.ppb, at = r.s0 * a.ppb + e;
         uint64_t h = 0;
-        const bool hit = stage_hit(a, r.s0 + k, k, hits, &h);
+        const bool hit = stage_hit(a, r.s0 + k, k, hits, &h) && !(r.tail_tok && k == r.full && j >= tail_pages);
         for (uint32_t g = 0; g < a.n_groups; ++g) {
           const uint64_t i = (uint64_t)g * row + at;
           a.tables_out[i] = !hit ? -1 : (a.tables_in ? a.tables_in[i] : (int32_t)at);
@@ -715,7 +738,7 @@ int launch_dindex_stats(const void* mem, void* stream, uint64_t* d_out) {
 }
 
 namespace {
-ChainIn chain_in(const tl_ctx* ctx, size_t n_chains, const tl_chains* ch) {
+ChainIn chain_in(const tl_ctx* ctx, size_t n_chains, const tl_chains* ch, uint32_t flags) {
   ChainIn in;
   in.tokens = ch ? ch->d_tokens : nullptr;
   in.n_tokens = ch ? ch->n_tokens : 0;
@@ -726,6 +749,7 @@ ChainIn chain_in(const tl_ctx* ctx, size_t n_chains, const tl_chains* ch) {
   in.first_block = ch ? ch->d_first_block : nullptr;
   in.n_chains = (uint32_t)n_chains;
   in.bt = ctx->geo.block_tokens;
+  in.tail = (flags & TL_CHAIN_TAIL) ? 1 : 0;
   in.key = msg_len(8, in.bt);
   in.fp = msg_len(10, in.bt);
   for (int i = 0; i < 8; ++i)
@@ -740,7 +764,7 @@ int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
                  uint64_t* d_handles, uint32_t* d_hits) {
   hipStream_t s = (hipStream_t)stream;
   ChainArgs a;
-  a.in = chain_in(ctx, n_chains, ch);
+  a.in = chain_in(ctx, n_chains, ch, flags);
   // one chain per wavefront while chains fit the SIMDs, else share
   const uint64_t simds = 4ull * (uint64_t)sm_count();
   uint64_t lanes = (n_chains + simds - 1) / simds;
@@ -763,10 +787,10 @@ int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
 int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
                      const void* index_mem, uint64_t capacity, const void* tok_mem,
                      uint64_t tok_capacity, const uint8_t* d_handle_keys, uint64_t n_handles,
-                     uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits) {
+                     uint32_t flags, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits) {
   hipStream_t s = (hipStream_t)stream;
   ParArgs a;
-  a.in = chain_in(ctx, n_chains, ch);
+  a.in = chain_in(ctx, n_chains, ch, flags);
   a.x.mem = (uint64_t*)index_mem;
   a.x.mask = capacity - 1;
   a.t.mem = (uint64_t*)tok_mem;
@@ -787,12 +811,13 @@ int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_
 }
 
 int launch_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
-                        const uint64_t* d_pos, uint8_t* d_out) {
+                        const uint64_t* d_pos, const uint32_t* d_n_tokens, uint8_t* d_out) {
   hipStream_t s = (hipStream_t)stream;
   FpArgs a;
-  a.in = chain_in(ctx, 0, nullptr);
+  a.in = chain_in(ctx, 0, nullptr, 0);
   a.tokens = d_tokens;
   a.pos = d_pos;
+  a.n_tokens = d_n_tokens;
   a.out = d_out;
   a.n = (uint32_t)n;
   (void)hipGetLastError();
@@ -803,11 +828,11 @@ int launch_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_
   return launched();
 }
 
-int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
+int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch, uint32_t flags,
                  const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_hptr,
                  const uint64_t* d_hlen, uint64_t n_handles, uint64_t* d_ptrs, uint64_t* d_lens,
-                 uint64_t* d_bidx, uint32_t* d_tokens_out, const int32_t* d_tables_in,
-                 int32_t* d_tables_out) {
+                 uint64_t* d_bidx, uint32_t* d_tokens_out, uint32_t* d_n_tokens_out,
+                 const int32_t* d_tables_in, int32_t* d_tables_out) {
   hipStream_t s = (hipStream_t)stream;
   StageArgs a;
   a.tokens = ch->d_tokens;
@@ -819,7 +844,10 @@ int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
   a.n_chains = (uint32_t)n_chains;
   a.bt = ctx->geo.block_tokens;
   a.ppb = ctx->geo.ppb;
+  a.page_tokens = ctx->geo.page_tokens;
   a.n_groups = ctx->geo.n_groups;
+  a.tail = (flags & TL_CHAIN_TAIL) ? 1 : 0;
+  a.n_tokens_out = d_n_tokens_out;
   a.hits = d_hits;
   a.handles = d_handles;
   a.hptr = d_hptr;

@@ -439,7 +439,7 @@ int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_c
   if (n_chains == 0) return TL_OK;
   int r = check_chains(n_chains, chains);
   if (r) return r;
-  if (flags & ~uint32_t(TL_CHAIN_ALL_KEYS)) return TL_EINVAL;
+  if (flags & ~uint32_t(TL_CHAIN_ALL_KEYS | TL_CHAIN_TAIL)) return TL_EINVAL;
   if (!d_hits || ((uintptr_t)d_hits & 3)) return TL_EINVAL;
   if (chains->n_slots && (!d_keys || ((uintptr_t)d_keys & 3))) return TL_EINVAL;
   if (idx && chains->n_slots && (!d_handles || ((uintptr_t)d_handles & 7))) return TL_EINVAL;
@@ -448,19 +448,21 @@ int tl_chain_lookup(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_c
 }
 
 int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
-                          const uint64_t* d_block_index, uint8_t* d_out) {
+                          const uint64_t* d_block_index, const uint32_t* d_n_tokens, uint8_t* d_out) {
   if (!ctx) return TL_EINVAL;
   if (n == 0) return TL_OK;
   if (n >= (size_t(1) << 31)) return TL_ERANGE;
   if (!d_tokens || !d_block_index || !d_out) return TL_EINVAL;
-  if (((uintptr_t)d_tokens | (uintptr_t)d_out) & 3 || ((uintptr_t)d_block_index & 7)) return TL_EINVAL;
-  return tl::launch_fingerprints(ctx, stream, n, d_tokens, d_block_index, d_out);
+  if (((uintptr_t)d_tokens | (uintptr_t)d_out | (uintptr_t)d_n_tokens) & 3 || ((uintptr_t)d_block_index & 7))
+    return TL_EINVAL;
+  return tl::launch_fingerprints(ctx, stream, n, d_tokens, d_block_index, d_n_tokens, d_out);
 }
 
 int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
                         const tl_dindex* idx, const tl_dindex* tok_idx, const uint8_t* d_handle_keys,
-                        uint64_t n_handles, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits) {
-  if (!ctx) return TL_EINVAL;
+                        uint64_t n_handles, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,
+                        uint32_t* d_hits) {
+  if (!ctx || (flags & ~uint32_t(TL_CHAIN_TAIL))) return TL_EINVAL;
   if (n_chains == 0) return TL_OK;
   int r = check_chains(n_chains, chains);
   if (r) return r;
@@ -469,15 +471,16 @@ int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const 
   if (chains->n_slots && (!d_keys || !d_handles || ((uintptr_t)d_keys & 3) || ((uintptr_t)d_handles & 7)))
     return TL_EINVAL;
   return tl::launch_chain_par(ctx, stream, n_chains, chains, idx->mem, idx->capacity, tok_idx->mem,
-                              tok_idx->capacity, d_handle_keys, n_handles, d_keys, d_handles, d_hits);
+                              tok_idx->capacity, d_handle_keys, n_handles, flags, d_keys, d_handles, d_hits);
 }
 
 int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
-                   const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_handle_ptrs,
-                   const uint64_t* d_handle_lens, uint64_t n_handles, uint64_t* d_record_ptrs,
-                   uint64_t* d_record_lens, uint64_t* d_block_index, uint32_t* d_tokens_out,
-                   const int32_t* d_tables_in, int32_t* d_tables_out) {
-  if (!ctx) return TL_EINVAL;
+                   uint32_t flags, const uint32_t* d_hits, const uint64_t* d_handles,
+                   const uint64_t* d_handle_ptrs, const uint64_t* d_handle_lens, uint64_t n_handles,
+                   uint64_t* d_record_ptrs, uint64_t* d_record_lens, uint64_t* d_block_index,
+                   uint32_t* d_tokens_out, uint32_t* d_n_tokens_out, const int32_t* d_tables_in,
+                   int32_t* d_tables_out) {
+  if (!ctx || (flags & ~uint32_t(TL_CHAIN_TAIL))) return TL_EINVAL;
   if (n_chains == 0) return TL_OK;
   int r = check_chains(n_chains, chains);
   if (r) return r;
@@ -489,12 +492,13 @@ int tl_chain_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_ch
     if (((uintptr_t)d_handles | (uintptr_t)d_record_ptrs | (uintptr_t)d_record_lens |
          (uintptr_t)d_block_index) & 7)
       return TL_EINVAL;
-    if (((uintptr_t)d_tokens_out | (uintptr_t)d_tables_in | (uintptr_t)d_tables_out) & 3)
+    if (((uintptr_t)d_tokens_out | (uintptr_t)d_n_tokens_out | (uintptr_t)d_tables_in |
+         (uintptr_t)d_tables_out) & 3)
       return TL_EINVAL;
   }
-  return tl::launch_stage(ctx, stream, n_chains, chains, d_hits, d_handles, d_handle_ptrs,
+  return tl::launch_stage(ctx, stream, n_chains, chains, flags, d_hits, d_handles, d_handle_ptrs,
                           d_handle_lens, n_handles, d_record_ptrs, d_record_lens, d_block_index,
-                          d_tokens_out, d_tables_in, d_tables_out);
+                          d_tokens_out, d_n_tokens_out, d_tables_in, d_tables_out);
 }
 
 // ---- misc -------------------------------------------------------------------

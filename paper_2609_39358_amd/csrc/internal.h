@@ -97,14 +97,14 @@ int launch_chain(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
 int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
                      const void* index_mem, uint64_t capacity, const void* tok_mem,
                      uint64_t tok_capacity, const uint8_t* d_handle_keys, uint64_t n_handles,
-                     uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits);
+                     uint32_t flags, uint8_t* d_keys, uint64_t* d_handles, uint32_t* d_hits);
 int launch_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint32_t* d_tokens,
-                        const uint64_t* d_pos, uint8_t* d_out);
-int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch,
+                        const uint64_t* d_pos, const uint32_t* d_n_tokens, uint8_t* d_out);
+int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* ch, uint32_t flags,
                  const uint32_t* d_hits, const uint64_t* d_handles, const uint64_t* d_hptr,
                  const uint64_t* d_hlen, uint64_t n_handles, uint64_t* d_ptrs, uint64_t* d_lens,
-                 uint64_t* d_bidx, uint32_t* d_tokens_out, const int32_t* d_tables_in,
-                 int32_t* d_tables_out);
+                 uint64_t* d_bidx, uint32_t* d_tokens_out, uint32_t* d_n_tokens_out,
+                 const int32_t* d_tables_in, int32_t* d_tables_out);
 
 // Brackets one kernel launch with a pair of HIP events on `stream` while
 // timing is enabled (tl_timing); kernels.hip.

@@ -128,36 +128,39 @@ class DeviceStore:
         return self.records.lens
 
     def save_blocks(self, src: PagedCache, d_tables: torch.Tensor, d_keys: torch.Tensor, d_tokens: torch.Tensor,
-                    d_positions: torch.Tensor, d_slots: torch.Tensor, stream=None) -> torch.Tensor:
+                    d_positions: torch.Tensor, d_slots: torch.Tensor, stream=None,
+                    d_n_tokens: torch.Tensor = None) -> torch.Tensor:
         """Save n blocks of a paged cache (after their prefill) into record
         slots d_slots and index them (Sec. 2.2: state is written once, after the
         runtime computes it). Tables [n_groups][n * pages_per_block] name each
-        block's pages in src. Returns the device save status [n]."""
+        block's pages in src; d_n_tokens (u32 [n] or None) marks partial last
+        blocks. Returns the device save status [n]."""
         stream = stream or torch.cuda.current_stream()
         n = d_keys.shape[0]
         status = torch.zeros(max(n, 1), dtype=torch.uint8, device=self.device)
         if n == 0:
             return status[:0]
         ptrs = self.records.ptrs.index_select(0, d_slots)
-        T.tl_save(self.ctx, stream, n, src.tl(), T.make_blocks(d_keys, d_positions, d_tokens, d_tables), ptrs,
-                  status)
+        T.tl_save(self.ctx, stream, n, src.tl(), T.make_blocks(d_keys, d_positions, d_tokens, d_tables, d_n_tokens),
+                  ptrs, status)
         if not bool((status[:n] == T.ACCEPT).all()):
             raise RuntimeError("save refused some blocks (bad page ids)")
         self.records.lens.index_fill_(0, d_slots, self.ctx.record_bytes)
-        self.add(d_keys, d_tokens, d_positions, d_slots, stream)
+        self.add(d_keys, d_tokens, d_positions, d_slots, stream, d_n_tokens)
         return status[:n]
 
     def add(self, d_keys: torch.Tensor, d_tokens: torch.Tensor, d_positions: torch.Tensor,
-            d_slots: torch.Tensor, stream=None):
+            d_slots: torch.Tensor, stream=None, d_n_tokens: torch.Tensor = None):
         """Index n saved blocks: keys [n][32] u8, tokens [n][block tokens] i32,
-        positions [n] i64, slots [n] i64 (all device)."""
+        positions [n] i64, slots [n] i64, token counts [n] u32 or None (all
+        device)."""
         stream = stream or torch.cuda.current_stream()
         n = d_keys.shape[0]
         if n == 0:
             return
         self.slot_keys.index_copy_(0, d_slots, d_keys)
         fps = torch.empty((n, 32), dtype=torch.uint8, device=self.device)
-        T.tl_block_fingerprints(self.ctx, stream, n, d_tokens, d_positions, fps)
+        T.tl_block_fingerprints(self.ctx, stream, n, d_tokens, d_positions, fps, d_n_tokens)
         wsb = T.tl_dindex_workspace_bytes(n)
         ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
         st = torch.empty(n, dtype=torch.uint8, device=self.device)
@@ -182,17 +185,20 @@ class DeviceRestorePipeline:
     prompts. One verified parallel key walk, one staging kernel and one
     tl_load, all on `stream` with no host synchronisation."""
 
-    def __init__(self, store: DeviceStore, pool: PagedCache, stream=None):
+    def __init__(self, store: DeviceStore, pool: PagedCache, stream=None, tail: bool = False):
+        """tail: a request's partial last block is keyed and restored too."""
         self.store, self.pool = store, pool
         self.ctx = store.ctx
         self.stream = stream or torch.cuda.current_stream()
         self.bt = self.ctx.block_bytes // 4
+        self.flags = T.TL_CHAIN_TAIL if tail else 0
 
     def restore(self, d_tokens: torch.Tensor, lengths: Sequence[int], d_first_block=None) -> DeviceBatch:
         dev, s, ctx, bt = self.pool.k[0].device, self.stream, self.ctx, self.bt
         lengths = [int(x) for x in lengths]
         tok_off = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
-        slot_off = np.concatenate([[0], np.cumsum([L // bt for L in lengths])]).astype(np.int64)
+        per = [-(-L // bt) if self.flags else L // bt for L in lengths]
+        slot_off = np.concatenate([[0], np.cumsum(per)]).astype(np.int64)
         n, S = len(lengths), int(slot_off[-1])
         if S * ctx.pages_per_block > self.pool.n_pages:
             raise ValueError("batch needs %d pages, pool has %d" % (S * ctx.pages_per_block, self.pool.n_pages))
@@ -209,17 +215,19 @@ class DeviceRestorePipeline:
         handles = torch.empty(Sx, dtype=torch.int64, device=dev)
         ptrs, lens, bidx = (torch.empty(Sx, dtype=torch.int64, device=dev) for _ in range(3))
         toks = torch.empty((Sx, bt), dtype=torch.int32, device=dev)
+        ntok = torch.empty(Sx, dtype=torch.int32, device=dev)
         tab = torch.empty((ctx.n_groups, Sx * ctx.pages_per_block), dtype=torch.int32, device=dev)
         st = self.store
         T.tl_chain_lookup_par(ctx, s, n, chains, st.key_index, st.token_index, st.slot_keys, st.capacity, keys,
-                              handles, hits)
+                              handles, hits, self.flags)
         T.tl_chain_stage(ctx, s, n, chains, hits, handles, st.records.ptrs, st.records.lens, st.capacity, ptrs,
-                         lens, bidx, toks, None, tab)
+                         lens, bidx, toks, None, tab, self.flags, ntok)
         if S:
             ws_b = T.tl_workspace_bytes(ctx, S)
             ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
-            T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab), self.pool.tl(), verd, ws, ws_b)
-            out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, tab, ws)
+            T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab, ntok), self.pool.tl(), verd, ws,
+                      ws_b)
+            out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, ntok, tab, ws)
         return out
 
 

@@ -104,10 +104,11 @@ def _load():
         "tl_dindex_get": (c.c_int, [P, P, c.c_size_t, P, P]),
         "tl_dindex_stats": (c.c_int, [P, P, P]),
         "tl_chain_lookup": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, c.c_uint32, P, P, P]),
-        "tl_chain_stage": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, P, c.c_uint64, P, P,
-                                     P, P, P, P]),
-        "tl_block_fingerprints": (c.c_int, [P, P, c.c_size_t, P, P, P]),
-        "tl_chain_lookup_par": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, c.c_uint64, P, P, P]),
+        "tl_chain_stage": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), c.c_uint32, P, P, P, P, c.c_uint64,
+                                     P, P, P, P, P, P, P]),
+        "tl_block_fingerprints": (c.c_int, [P, P, c.c_size_t, P, P, P, P]),
+        "tl_chain_lookup_par": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_chains), P, P, P, c.c_uint64, c.c_uint32,
+                                          P, P, P]),
         "tl_file_open": (P, [c.c_char_p, c.c_uint64, c.c_int, c.c_int, c.POINTER(c.c_int)]),
         "tl_file_close": (c.c_int, [P]),
         "tl_file_records": (c.c_uint64, [P]),
@@ -142,7 +143,7 @@ EXPORTED = (
 KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_final": 4, "chain": 5,
            "stage": 6, "index": 7}
 TL_INDEX_STORED, TL_INDEX_FULL, TL_INDEX_TAG_CLASH = 0x01, 0x20, 0x21
-TL_CHAIN_ALL_KEYS = 1
+TL_CHAIN_ALL_KEYS, TL_CHAIN_TAIL = 1, 2
 TL_KEYS_TAIL = 1
 MISS = 2**64 - 1
 
@@ -421,26 +422,27 @@ def tl_chain_lookup(ctx: Ctx, stream, n_chains: int, chains: tl_chains, index: O
                                 _addr(d_handles), _addr(d_hits)), "tl_chain_lookup")
 
 
-def tl_block_fingerprints(ctx: Ctx, stream, n: int, d_tokens, d_block_index, d_out):
+def tl_block_fingerprints(ctx: Ctx, stream, n: int, d_tokens, d_block_index, d_out, d_n_tokens=None):
     _check(_lib.tl_block_fingerprints(ctx.handle, _stream(stream), n, _addr(d_tokens), _addr(d_block_index),
-                                      _addr(d_out)), "tl_block_fingerprints")
+                                      _addr(d_n_tokens), _addr(d_out)), "tl_block_fingerprints")
 
 
 def tl_chain_lookup_par(ctx: Ctx, stream, n_chains: int, chains: tl_chains, index: DeviceIndex,
-                        token_index: DeviceIndex, d_handle_keys, n_handles: int, d_keys, d_handles, d_hits):
+                        token_index: DeviceIndex, d_handle_keys, n_handles: int, d_keys, d_handles, d_hits,
+                        flags: int = 0):
     _check(_lib.tl_chain_lookup_par(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains), index.handle,
-                                    token_index.handle, _addr(d_handle_keys), n_handles, _addr(d_keys),
+                                    token_index.handle, _addr(d_handle_keys), n_handles, flags, _addr(d_keys),
                                     _addr(d_handles), _addr(d_hits)), "tl_chain_lookup_par")
 
 
 def tl_chain_stage(ctx: Ctx, stream, n_chains: int, chains: tl_chains, d_hits, d_handles, d_handle_ptrs,
                    d_handle_lens, n_handles: int, d_record_ptrs, d_record_lens, d_block_index,
-                   d_tokens_out=None, d_tables_in=None, d_tables_out=None):
-    _check(_lib.tl_chain_stage(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains), _addr(d_hits),
+                   d_tokens_out=None, d_tables_in=None, d_tables_out=None, flags: int = 0, d_n_tokens_out=None):
+    _check(_lib.tl_chain_stage(ctx.handle, _stream(stream), n_chains, ctypes.byref(chains), flags, _addr(d_hits),
                                _addr(d_handles), _addr(d_handle_ptrs), _addr(d_handle_lens), n_handles,
                                _addr(d_record_ptrs), _addr(d_record_lens), _addr(d_block_index),
-                               _addr(d_tokens_out), _addr(d_tables_in), _addr(d_tables_out)),
-           "tl_chain_stage")
+                               _addr(d_tokens_out), _addr(d_n_tokens_out), _addr(d_tables_in),
+                               _addr(d_tables_out)), "tl_chain_stage")
 
 
 # ------------------------------------------------------------------ record files (disk tier)

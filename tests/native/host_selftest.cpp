@@ -27,12 +27,15 @@ int launch_dindex_stats(const void*, void*, uint64_t*) { return TL_EDEVICE; }
 int launch_chain(const tl_ctx*, void*, size_t, const tl_chains*, const void*, uint64_t, uint32_t, uint8_t*,
                  uint64_t*, uint32_t*) { return TL_EDEVICE; }
 int launch_chain_par(const tl_ctx*, void*, size_t, const tl_chains*, const void*, uint64_t, const void*,
-                     uint64_t, const uint8_t*, uint64_t, uint8_t*, uint64_t*, uint32_t*) { return TL_EDEVICE; }
-int launch_fingerprints(const tl_ctx*, void*, size_t, const uint32_t*, const uint64_t*, uint8_t*) {
+                     uint64_t, const uint8_t*, uint64_t, uint32_t, uint8_t*, uint64_t*, uint32_t*) {
   return TL_EDEVICE;
 }
-int launch_stage(const tl_ctx*, void*, size_t, const tl_chains*, const uint32_t*, const uint64_t*,
-                 const uint64_t*, const uint64_t*, uint64_t, uint64_t*, uint64_t*, uint64_t*, uint32_t*,
+int launch_fingerprints(const tl_ctx*, void*, size_t, const uint32_t*, const uint64_t*, const uint32_t*,
+                        uint8_t*) {
+  return TL_EDEVICE;
+}
+int launch_stage(const tl_ctx*, void*, size_t, const tl_chains*, uint32_t, const uint32_t*, const uint64_t*,
+                 const uint64_t*, const uint64_t*, uint64_t, uint64_t*, uint64_t*, uint64_t*, uint32_t*, uint32_t*,
                  const int32_t*, int32_t*) { return TL_EDEVICE; }
 }  // namespace tl
 
@@ -171,23 +174,27 @@ int main() {
   EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, 0, ck, nullptr, hits) == TL_EDEVICE);
   EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, &fake, 0, ck, nullptr, hits) == TL_EINVAL);  // handles needed
   EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, &fake, 0, ck, dh, hits) == TL_EDEVICE);
-  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, 2, ck, nullptr, hits) == TL_EINVAL);  // unknown flag
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, 4, ck, nullptr, hits) == TL_EINVAL);  // unknown flag
+  EXPECT(tl_chain_lookup(c, nullptr, 2, &chn, nullptr, TL_CHAIN_TAIL | TL_CHAIN_ALL_KEYS, ck, nullptr, hits) == TL_EDEVICE);
   EXPECT(tl_chain_lookup(c, nullptr, (size_t)1 << 24, &chn, nullptr, 0, ck, nullptr, hits) == TL_ERANGE);
   EXPECT(tl_chain_lookup(c, nullptr, 0, nullptr, nullptr, 0, nullptr, nullptr, nullptr) == TL_OK);
   tl_chains no_off = chn;
   no_off.d_slot_off = nullptr;
   EXPECT(tl_chain_lookup(c, nullptr, 2, &no_off, nullptr, 0, ck, nullptr, hits) == TL_EINVAL);
-  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, ck, dh, hits) == TL_EDEVICE);
-  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, nullptr, ck, 2, ck, dh, hits) == TL_EINVAL);
-  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, nullptr, 2, ck, dh, hits) == TL_EINVAL);
-  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, ck, nullptr, hits) == TL_EINVAL);
-  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, dh, ck) == TL_EDEVICE);
-  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, nullptr, ck) == TL_EINVAL);
-  EXPECT(tl_block_fingerprints(c, nullptr, 0, nullptr, nullptr, nullptr) == TL_OK);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, 0, ck, dh, hits) == TL_EDEVICE);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, TL_CHAIN_TAIL, ck, dh, hits) == TL_EDEVICE);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, TL_CHAIN_ALL_KEYS, ck, dh, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, nullptr, ck, 2, 0, ck, dh, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, nullptr, 2, 0, ck, dh, hits) == TL_EINVAL);
+  EXPECT(tl_chain_lookup_par(c, nullptr, 2, &chn, &fake, &fake, ck, 2, 0, ck, nullptr, hits) == TL_EINVAL);
+  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, dh, nullptr, ck) == TL_EDEVICE);
+  EXPECT(tl_block_fingerprints(c, nullptr, 1, tk, nullptr, nullptr, ck) == TL_EINVAL);
+  EXPECT(tl_block_fingerprints(c, nullptr, 0, nullptr, nullptr, nullptr, nullptr) == TL_OK);
   uint64_t sp[2], sl[2], sb[2];
-  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EDEVICE);
-  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, dh, nullptr, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
-  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, hits, nullptr, sp, sl, 2, sp, sl, sb, nullptr, nullptr, tb) == TL_EINVAL);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, 0, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, nullptr, tb) == TL_EDEVICE);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, 0, hits, dh, nullptr, sl, 2, sp, sl, sb, nullptr, nullptr, nullptr, tb) == TL_EINVAL);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, 0, hits, nullptr, sp, sl, 2, sp, sl, sb, nullptr, nullptr, nullptr, tb) == TL_EINVAL);
+  EXPECT(tl_chain_stage(c, nullptr, 2, &chn, 4, hits, dh, sp, sl, 2, sp, sl, sb, nullptr, nullptr, nullptr, tb) == TL_EINVAL);
   // record files: write in one order, read back in another on several threads
   {
     char path[] = "/tmp/tl_selftest_XXXXXX";

@@ -757,3 +757,173 @@ def test_reuse_loop_on_the_device():
         for ta, tb in ((pool_a.k[l], pool_b.k[l]), (pool_a.v[l], pool_b.v[l])):
             assert torch.equal(tb[:25], ta[:25])  # the restored state is the saved state
             assert (tb[25:] == 0x42).all()  # the rest is left to prefill
+
+
+# ---------------------------------------------------------------- partial last blocks
+def _tail_slots(lengths, bt):
+    return [-(-L // bt) for L in lengths]
+
+
+@pytest.mark.parametrize("page_tokens,ppb", [(5, 1), (13, 1), (16, 1), (16, 3)])
+def test_chain_tail_keys_equal_the_oracle(page_tokens, ppb):
+    ctx, ns, bt = ctx_bt(page_tokens, ppb)
+    lengths = lengths_for(bt, 100, 40 + bt)
+    ch = Chains(ctx, lengths, 41 + bt, bt, slot_counts=_tail_slots(lengths, bt))
+    keys, _, hits = ch.lookup(ctx, None, T.TL_CHAIN_TAIL)
+    for c in range(ch.n):
+        want = ref.block_keys(ns, ch.data(c), 4 * bt, tail=True)
+        assert hits[c] == len(want), c
+        s0 = int(ch.slot_off[c])
+        assert [keys[s0 + k].tobytes() for k in range(len(want))] == want, (c, bt)
+
+
+class TailStore:
+    """Key and token indexes over stored documents whose last block may be
+    partial (handle = record id)."""
+
+    def __init__(self, ctx, ns, bt, docs, cap=8192):
+        self.keys, toks, pos, ntok = [], [], [], []
+        for d in docs:
+            ks = ref.block_keys(ns, d.tobytes(), 4 * bt, tail=True)
+            for i, k in enumerate(ks):
+                blk = d[i * bt:(i + 1) * bt]
+                self.keys.append(k)
+                toks.append(np.concatenate([blk, np.zeros(bt - blk.size, np.uint32)]))
+                pos.append(i)
+                ntok.append(blk.size)
+        n = len(self.keys)
+        self.idx, self.tidx = new_index(cap), new_index(cap)
+        assert (dput(self.idx, self.keys, range(n)) == T.TL_INDEX_STORED).all()
+        d_toks = i32(np.stack(toks).view(np.int32))
+        fps = torch.empty((n, 32), dtype=torch.uint8, device=DEV)
+        T.tl_block_fingerprints(ctx, torch.cuda.current_stream(), n, d_toks, i64(np.array(pos, np.uint64)), fps,
+                                i32(np.array(ntok, np.int32)))
+        torch.cuda.synchronize()
+        assert (dput(self.tidx, [fps[b].cpu().numpy().tobytes() for b in range(n)], range(n)) ==
+                T.TL_INDEX_STORED).all()
+        self.index = ref.index_put({}, self.keys, range(n))
+        self.d_hkeys = torch.from_numpy(np.frombuffer(b"".join(self.keys), np.uint8).reshape(n, 32).copy()).to(DEV)
+        self.n = n
+
+
+def test_walks_with_tails_equal_the_oracle_walk():
+    ctx, ns, bt = ctx_bt(16)
+    docs = [wl.tokens(n_tok, 120 + i) for i, n_tok in enumerate([40 * 16 + 5, 300 * 16 + 15, 70 * 16, 1 * 16 + 1])]
+    ts = TailStore(ctx, ns, bt, docs)
+    rng = np.random.default_rng(121)
+    reqs = []
+    for d in docs:
+        reqs.append(d.copy())                                    # the stored document: every block, tail too
+        reqs.append(np.concatenate([d, wl.tokens(7, 122)]))       # a longer tail: reuse ends before it
+        cut = int(rng.integers(1, d.size))
+        reqs.append(d[:cut])                                      # ends inside a stored block
+    reqs += [wl.tokens(int(rng.integers(0, 100)), 123 + i) for i in range(5)]
+    lengths = [r.size for r in reqs]
+    ch = Chains(ctx, lengths, 0, bt, slot_counts=_tail_slots(lengths, bt))
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    two = type("Two", (), {"idx": ts.idx, "tidx": ts.tidx, "d_hkeys": ts.d_hkeys, "n": ts.n})()
+    S = max(ch.n_slots, 1)
+    for variant in ("sequential", "parallel"):
+        keys = torch.full((S, 32), SENT, dtype=torch.uint8, device=DEV)
+        handles = torch.full((S,), 0x7777, dtype=torch.int64, device=DEV)
+        hits = torch.full((ch.n,), -1, dtype=torch.int32, device=DEV)
+        if variant == "sequential":
+            T.tl_chain_lookup(ctx, torch.cuda.current_stream(), ch.n, ch.tl, ts.idx, T.TL_CHAIN_TAIL, keys, handles,
+                              hits)
+        else:
+            T.tl_chain_lookup_par(ctx, torch.cuda.current_stream(), ch.n, ch.tl, ts.idx, ts.tidx, ts.d_hkeys, ts.n,
+                                  keys, handles, hits, T.TL_CHAIN_TAIL)
+        torch.cuda.synchronize()
+        k_np, h_np, hits_np = keys.cpu().numpy(), handles.cpu().numpy().view(np.uint64), hits.cpu().numpy()
+        for c in range(ch.n):
+            want_keys, want_hits, want_h = ref.chain_walk(ns, ch.data(c), 4 * bt, ts.index, tail=True)
+            s0, nk = int(ch.slot_off[c]), len(want_keys)
+            assert hits_np[c] == want_hits, (variant, c)
+            assert list(h_np[s0:s0 + want_hits]) == want_h
+            assert (h_np[s0 + want_hits:s0 + nk] == np.uint64(T.MISS)).all()
+            kept = min(want_hits + 1, nk)
+            assert [k_np[s0 + k].tobytes() for k in range(kept)] == want_keys[:kept], (variant, c)
+        log(variant, "walk with tails: hits", [int(x) for x in hits_np[:12]])
+    # the stored documents are found whole, tails included
+    assert [int(x) for x in hits_np[0:12:3]] == [41, 301, 70, 2]
+
+
+def test_stage_with_tails():
+    ctx, ns, bt = ctx_bt(4, ppb=3, n_layers=2, groups=[0, 1])  # 12-token blocks of three 4-token pages
+    docs = [wl.tokens(n_tok, 130 + i) for i, n_tok in enumerate([5 * 12 + 5, 3 * 12 + 1, 4 * 12])]
+    ts = TailStore(ctx, ns, bt, docs)
+    reqs = [d.copy() for d in docs]
+    lengths = [r.size for r in reqs]
+    ch = Chains(ctx, lengths, 0, bt, slot_counts=_tail_slots(lengths, bt))
+    ch.tokens[:] = np.concatenate(reqs)
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    S = ch.n_slots
+    keys = torch.empty((S, 32), dtype=torch.uint8, device=DEV)
+    handles = torch.empty(S, dtype=torch.int64, device=DEV)
+    hits = torch.empty(ch.n, dtype=torch.int32, device=DEV)
+    T.tl_chain_lookup_par(ctx, torch.cuda.current_stream(), ch.n, ch.tl, ts.idx, ts.tidx, ts.d_hkeys, ts.n, keys,
+                          handles, hits, T.TL_CHAIN_TAIL)
+    hptr = i64(np.arange(ts.n, dtype=np.uint64) * 4096 + 0x200000)
+    hlen = i64(np.full(ts.n, 77, np.uint64))
+    ptrs, lens, bidx = (torch.empty(S, dtype=torch.int64, device=DEV) for _ in range(3))
+    toks = torch.full((S, bt), -5, dtype=torch.int32, device=DEV)
+    ntok = torch.full((S,), -5, dtype=torch.int32, device=DEV)
+    tab = torch.full((2, S * 3), -9, dtype=torch.int32, device=DEV)
+    T.tl_chain_stage(ctx, torch.cuda.current_stream(), ch.n, ch.tl, hits, handles, hptr, hlen, ts.n, ptrs, lens, bidx,
+                     toks, None, tab, T.TL_CHAIN_TAIL, ntok)
+    torch.cuda.synchronize()
+    assert hits.cpu().tolist() == [6, 4, 4]
+    ntok, toks, tab = ntok.cpu().numpy(), toks.cpu().numpy().view(np.uint32), tab.cpu().numpy()
+    want_n = [12] * 5 + [5] + [12] * 3 + [1] + [12] * 4
+    assert ntok.tolist() == want_n
+    for q, t in enumerate(want_n):
+        c = 0 if q < 6 else (1 if q < 10 else 2)
+        k = q - (0, 6, 10)[c]
+        d = reqs[c]
+        assert np.array_equal(toks[q][:t], d[k * bt:k * bt + t]) and not toks[q][t:].any()
+        used = -(-t // 4)
+        for g in range(2):
+            for j in range(3):
+                assert tab[g, q * 3 + j] == (q * 3 + j if j < used else -1), (q, g, j)
+
+
+def test_reuse_loop_with_a_tail():
+    """A request's partial last block is saved with its count and restored
+    by a later identical request; a request whose last block continues past
+    the stored tail does not reuse it."""
+    from paper_2609_39358_amd import pipeline
+    from tests.gpu_case import ctx_of, fill_cache, layout_of
+    geom = wl.Geometry(2, 4, 64, 16)
+    ctx, lay = ctx_of(geom), layout_of(geom)
+    ns, bt = ref.namespace_digest(TEN, FP, lay), 16
+    store = pipeline.DeviceStore(ctx, 64, DEV)
+    a = wl.tokens(40 * bt + 5, 310)
+    pool_a = fill_cache(PagedCache(geom.n_layers, 64, lay.slab_bytes, DEV), geom, 311)
+    keys = ref.block_keys(ns, a.tobytes(), 4 * bt, tail=True)
+    assert len(keys) == 41
+    toks = np.zeros((41, bt), np.uint32)
+    for k in range(41):
+        blk = a[k * bt:(k + 1) * bt]
+        toks[k, :blk.size] = blk
+    n_tok = np.array([bt] * 40 + [5], np.int32)
+    st = store.save_blocks(pool_a, i32(np.arange(41)[None, :]),
+                           torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(41, 32).copy()).to(DEV),
+                           i32(toks.view(np.int32)), i64(np.arange(41)), torch.arange(41, dtype=torch.int64, device=DEV),
+                           d_n_tokens=i32(n_tok))
+    assert (st.cpu().numpy() == ref.ACCEPT).all()
+    for req, want_hits in ((a.copy(), 41), (np.concatenate([a, wl.tokens(20, 312)]), 40), (a[:40 * bt + 3], 40)):
+        pool_b = PagedCache(geom.n_layers, 64, lay.slab_bytes, DEV)
+        for t in pool_b.k + pool_b.v:
+            t.fill_(0x42)
+        res = pipeline.DeviceRestorePipeline(store, pool_b, tail=True).restore(i32(req.view(np.int32)), [req.size])
+        torch.cuda.synchronize()
+        index = ref.index_put({}, keys, range(41))
+        assert res.hits.cpu().tolist() == [ref.chain_walk(ns, req.tobytes(), 4 * bt, index, tail=True)[1]] == \
+            [want_hits]
+        v = res.verdicts.cpu().numpy()
+        assert (v[:want_hits] == ref.ACCEPT).all() and (v[want_hits:] == ref.MISSING).all()
+        for l in range(geom.n_layers):
+            for ta, tb in ((pool_a.k[l], pool_b.k[l]), (pool_a.v[l], pool_b.v[l])):
+                assert torch.equal(tb[:want_hits], ta[:want_hits])
+                assert (tb[want_hits:] == 0x42).all()
