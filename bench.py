@@ -362,20 +362,32 @@ def main():
             "hbm_frac": step_bytes / (save_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
     log("save: %.3f ms/step, %.0f GB/s" % (save_ms, save["GBps"]))
 
-    # ---- the same corpus at the paper's block granularity (Sec. 4.1: 11 blocks):
-    # 550 pages (8,800 tokens) per record, saved from the same source cache
+    # ---- the same corpus at the paper's block granularity (Sec. 4.1: 11 blocks
+    # for the corpus, the last one partial): 550 pages (8,800 tokens) per
+    # record, and a last block of the remaining 200 tokens on 13 pages (its
+    # other pages left out), saved from the same source cache
     pb = None
     if not args.no_paper_blocks:
         ppb = 550
         ctx_pb = T.tl_ctx_create(b"bench-tenant", b"gemma-31b-class-fp", g.n_layers, g.n_kv_heads,
                                  g.head_dim, g.dtype, P, pages_per_block=ppb)
-        n_pb = cfg.n_tokens // (P * ppb)
-        keys_pb = T.tl_block_keys(ctx_pb, tokens)
+        bt_pb = P * ppb
+        n_pb = -(-cfg.n_tokens // bt_pb)
+        tail_pb = cfg.n_tokens - (n_pb - 1) * bt_pb
+        used_pb = -(-tail_pb // P)
+        keys_pb = T.tl_block_keys(ctx_pb, tokens, tail=True)
         store_pb = RecordStore(n_pb, ctx_pb.record_bytes, dev)
-        tok_pb = torch.from_numpy(tokens[:n_pb * ppb * P].view(np.int32).reshape(n_pb, -1).copy()).to(dev)
-        t_src_pb = torch.from_numpy(wl.page_table(n_pb * ppb, cfg.src_pages, cfg.seed, 5)[None, :]).to(dev)
+        rows_pb = np.zeros((n_pb, bt_pb), np.uint32)
+        rows_pb.reshape(-1)[:cfg.n_tokens] = tokens
+        tok_pb = torch.from_numpy(rows_pb.view(np.int32)).to(dev)
+        ntok_pb = torch.tensor([bt_pb] * (n_pb - 1) + [tail_pb], dtype=torch.int32, device=dev)
+        n_ent = (n_pb - 1) * ppb + used_pb  # pages that hold tokens: one more than the source cache has
+        ent = np.resize(wl.page_table(cfg.src_pages, cfg.src_pages, cfg.seed, 5), n_ent)  # one page read twice
+        t_src_np = np.full(n_pb * ppb, -1, np.int32)
+        t_src_np[:n_ent] = ent
+        t_src_pb = torch.from_numpy(t_src_np[None, :]).to(dev)
         blk_pb = T.make_blocks(torch.from_numpy(keys_pb).to(dev), torch.arange(n_pb, dtype=torch.int64, device=dev),
-                               tok_pb, t_src_pb)
+                               tok_pb, t_src_pb, ntok_pb)
         st_pb = torch.zeros(n_pb, dtype=torch.uint8, device=dev)
         T.tl_save(ctx_pb, stream, n_pb, src.tl(), blk_pb, store_pb.ptrs, st_pb)
         torch.cuda.synchronize()
@@ -389,7 +401,7 @@ def main():
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
 
-    dst = PagedCache(g.n_layers, cfg.dst_pages, ctx.slab_bytes, dev)
+    dst = PagedCache(g.n_layers, cfg.dst_pages + 1, ctx.slab_bytes, dev)  # + the paper-granularity tail's page
     ws_bytes = T.tl_workspace_bytes(ctx, n)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     verd = torch.zeros(n, dtype=torch.uint8, device=dev)
@@ -453,8 +465,10 @@ def main():
 
     # ---- restore of the paper-granularity records (same destination cache)
     if not args.no_paper_blocks:
-        t_dst_pb = torch.from_numpy(wl.page_table(n_pb * ppb, cfg.dst_pages, cfg.seed, 6)[None, :]).to(dev)
-        lblk_pb = T.make_blocks(blk_pb._keep[0], blk_pb._keep[1], tok_pb, t_dst_pb)
+        t_dst_np = np.full(n_pb * ppb, -1, np.int32)
+        t_dst_np[:n_ent] = wl.page_table(n_ent, cfg.dst_pages + 1, cfg.seed, 6)
+        t_dst_pb = torch.from_numpy(t_dst_np[None, :]).to(dev)
+        lblk_pb = T.make_blocks(blk_pb._keep[0], blk_pb._keep[1], tok_pb, t_dst_pb, ntok_pb)
         ws_pb = torch.empty(T.tl_workspace_bytes(ctx_pb, n_pb), dtype=torch.uint8, device=dev)
         v_pb = torch.zeros(n_pb, dtype=torch.uint8, device=dev)
         T.tl_timing(True)
@@ -472,12 +486,17 @@ def main():
         ms_pb = (time.perf_counter() - t0) * 1e3 / 5
         kern_pb = {k: T.tl_timing_read(k)[0] / 5 for k in ("load_init", "load_main", "load_final")}
         T.tl_timing(False)
-        bytes_pb = n_pb * (ctx_pb.record_bytes + ctx_pb.n_slabs * ctx_pb.slab_bytes)
+        # every record of a full block is read and its pages written; the
+        # partial block's metadata and the slabs of its 13 pages
+        slabs_tail = 2 * g.n_layers * used_pb
+        bytes_pb = (n_pb - 1) * (ctx_pb.record_bytes + ctx_pb.n_slabs * ctx_pb.slab_bytes) + \
+            ctx_pb.payload_offset + 2 * slabs_tail * ctx_pb.slab_bytes
         pb = {"blocks": n_pb, "pages_per_block": ppb, "record_bytes": ctx_pb.record_bytes,
-              "tokens_restored": n_pb * ppb * P, "ms": ms_pb, "GBps": bytes_pb / (ms_pb * 1e-3) / 1e9,
+              "last_block_tokens": tail_pb, "last_block_pages": used_pb,
+              "tokens_restored": cfg.n_tokens, "ms": ms_pb, "GBps": bytes_pb / (ms_pb * 1e-3) / 1e9,
               "hbm_frac": bytes_pb / (ms_pb * 1e-3) / 1e9 / HBM_PEAK_GBPS, "kernel_ms": kern_pb}
-        log("paper-granularity restore: %d x %.2f GB records, %.3f ms, %.0f GB/s, kernels %s"
-            % (n_pb, ctx_pb.record_bytes / 1e9, ms_pb, pb["GBps"], kern_pb))
+        log("paper-granularity restore: %d x %.2f GB records (the last %d tokens on %d pages), %.3f ms, %.0f GB/s, "
+            "kernels %s" % (n_pb, ctx_pb.record_bytes / 1e9, tail_pb, used_pb, ms_pb, pb["GBps"], kern_pb))
         del store_pb
 
     # ---- host steps a1 (keys) and a2 (lookup) on their own

@@ -213,3 +213,79 @@ def test_paper_sized_blocks_full_scale():
         for l in (0, geom.n_layers - 1):
             p = torch.from_numpy(c.t_dst[0][b * 550:(b + 1) * 550].astype(np.int64)).to(DEV)
             assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
+
+
+def test_paper_sized_blocks_with_the_partial_last_block():
+    """The whole 97,000-token corpus at the paper's granularity: 11 blocks of
+    8,800 tokens and a last block of the remaining 200 tokens (13 of its 550
+    pages; the other 537 are left out of the save and not restored), each a
+    4.3 GB record. The tail record is checked field by field against the
+    oracle; every block by verdicts and the permutation copy of its pages."""
+    base = wl.CONFIGS[2].geom
+    geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
+    bt, ppb = geom.block_tokens, 550
+    toks = wl.tokens(97000, 2)
+    n = -(-97000 // bt)
+    assert n == 12 and 97000 - 11 * bt == 200
+    c = Case(geom, n, n * ppb, n * ppb, seed=2)
+    lay = c.lay
+    keys = T.tl_block_keys(c.ctx, toks, tail=True)
+    assert [k.tobytes() for k in keys] == ref.block_keys(c.ns, toks.tobytes(), lay.block_bytes, tail=True)
+    rows = np.zeros((n, bt), np.uint32)
+    rows.reshape(-1)[:97000] = toks
+    n_tok = np.array([bt] * 11 + [200], np.uint32)
+    used = -(-200 // geom.page_tokens)
+    assert used == 13
+    t_src = c.t_src.copy()
+    t_dst = c.t_dst.copy()
+    t_src[:, 11 * ppb + used:] = -1
+    t_dst[:, 11 * ppb + used:] = -1
+    c.keys, c.tokens = keys, rows
+    c.d_keys, c.d_tokens = torch.from_numpy(keys).to(DEV), i32(rows.view(np.int32))
+    d_ntok = i32(n_tok.view(np.int32))
+    c.make_src()
+    store = RecordStore(n, lay.record_bytes, DEV)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    log("paper-sized blocks with the tail: 11 + 1 records of %.2f GB" % (lay.record_bytes / 1e9))
+    T.tl_save(c.ctx, torch.cuda.current_stream(), n, c.src.tl(),
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_src), d_ntok), store.ptrs, st)
+    torch.cuda.synchronize()
+    assert (st.cpu().numpy() == ref.ACCEPT).all()
+    po, S = lay.payload_offset, lay.slab_bytes
+    meta = store.buf[11, :po].cpu().numpy().tobytes()
+    want = ref.header_fields(lay, c.ns, keys[11].tobytes(), 11, 200)
+    assert meta[:144] == want[:144] and meta[152:256] == want[152:256]
+    assert int.from_bytes(meta[144:152], "little") == ref.root_digest(meta)
+    t0 = 256 + 8 * lay.n_segments
+    assert meta[t0:t0 + 800] == toks[11 * bt:].tobytes() and not any(meta[t0 + 800:])
+    r = np.random.default_rng(5)
+    for s in r.choice(lay.n_slabs, 40, replace=False):
+        l, kv, j = (s // ppb) >> 1, (s // ppb) & 1, s % ppb
+        body = store.buf[11, po + s * S: po + (s + 1) * S].cpu().numpy().tobytes()
+        if j < used:
+            page = int(t_src[0][11 * ppb + j])
+            assert body == (c.src.k if kv == 0 else c.src.v)[l][page].cpu().numpy().tobytes()
+        else:
+            assert not any(body)
+        stored = int.from_bytes(meta[256 + 8 * s: 264 + 8 * s], "little")
+        assert stored == ref.chunk_digest(body), s
+    dst = PagedCache(geom.n_layers, n * ppb, c.stride, DEV)
+    for t in dst.k + dst.v:
+        t.fill_(0x11)
+    ws_b = T.tl_workspace_bytes(c.ctx, n)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    verd = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_dst), d_ntok), dst.tl(), verd, ws, ws_b)
+    torch.cuda.synchronize()
+    assert (verd.cpu().numpy() == ref.ACCEPT).all()
+    ent = np.concatenate([np.arange(b * ppb, (b + 1) * ppb) for b in range(11)] + [np.arange(11 * ppb, 11 * ppb + used)])
+    check_pages_equal(c, dst, t_dst, blocks=ent)
+    # the pages the tail leaves out keep their bytes
+    p = torch.from_numpy(c.t_dst[0][11 * ppb + used:12 * ppb].astype(np.int64)).to(DEV)
+    assert (dst.k[0][p] == 0x11).all().item() and (dst.v[-1][p] == 0x11).all().item()
+    # loaded as a full block, the tail record is refused
+    T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_dst)), dst.tl(), verd, ws, ws_b)
+    torch.cuda.synchronize()
+    assert verd.cpu().numpy()[11] == ref.HEADER and (verd.cpu().numpy()[:11] == ref.ACCEPT).all()
