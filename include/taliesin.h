@@ -23,8 +23,8 @@
  * Conventions for every call:
  *   - Pointers named d_* are device (HBM) addresses; all others are host.
  *   - The caller owns every buffer (caches, records, tables, verdicts,
- *     workspace). tl_save / tl_load allocate no device memory and perform no
- *     host<->device copies; they only enqueue kernels on `stream`
+ *     indexes, workspace). No call allocates device memory or copies between
+ *     host and device; the device calls only enqueue kernels on `stream`
  *     (a hipStream_t; NULL = the null stream) and return. Outputs are valid
  *     after that stream is synchronised.
  *   - Return value: TL_OK (0) or a negative TL_E* status. On a negative status
@@ -201,14 +201,16 @@ int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* b
                         uint64_t* n_keys_out, int n_threads);
 
 /* ---- a6: save -----------------------------------------------------------
- * Gathers block b's 2*L slabs (layer l uses page d_tables[group(l)][b] of
- * src) into the record at d_record_ptrs[b] (record_bytes long, 16-byte
- * aligned, caller-allocated): metadata (header, chunk digest table, token
- * ids, zero padding, root) followed by the slabs verbatim. d_status[b]
- * (optional, device [n]): TL_ACCEPT when written; TL_MISSING for a 0
- * pointer and TL_BADARG for a misaligned pointer (nothing written); TL_BADARG
- * for a page id outside [0, n_pages) (the whole record is written as zeros, so
- * any later load fails). Sec. 2.2 (save after prefill), Fig. 1. */
+ * Gathers block b's 2*L*pages_per_block slabs (page j of the block in layer
+ * l is page d_tables[group(l)][b*pages_per_block + j] of src) into the
+ * record at d_record_ptrs[b] (record_bytes long, 16-byte aligned,
+ * caller-allocated): metadata (header, chunk digest table, token ids, zero
+ * padding, root) followed by the slabs verbatim. d_status[b] (optional,
+ * device [n]): TL_ACCEPT when written; TL_MISSING for a 0 pointer and
+ * TL_BADARG for a misaligned pointer (nothing written); TL_BADARG for a page
+ * id outside [0, n_pages) (other than -1 on a page that a partial block
+ * leaves out) or an invalid token count (the whole record is written as
+ * zeros, so any later load fails). Sec. 2.2 (save after prefill), Fig. 1. */
 int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
             const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status);
 
@@ -239,10 +241,11 @@ int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pag
  * speed while using no device memory beyond the destination pages (the
  * paper's blocks streamed in and discarded after use, Sec. 4.3 "Long windows
  * at flat GPU memory"). Checks, in order: pointer,
- * length, root (metadata checksum), header fields and namespace, position
- * (d_block_index[b]), key (d_keys[b]), token ids (if d_tokens), and the tree
- * XXH64 of every payload chunk it reads. It copies each read slab to page
- * d_tables[group(l)][b] of dst in the same pass and writes d_verdicts[b]
+ * length, root (metadata checksum), header fields, namespace and token count
+ * (d_n_tokens), position (d_block_index[b]), key (d_keys[b]), token ids (if
+ * d_tokens), and the tree XXH64 of every payload chunk it reads. It copies
+ * each read slab to its page d_tables[group(l)][b*pages_per_block + j] of dst
+ * in the same pass and writes d_verdicts[b]
  * (device [n], TL_ACCEPT or the first failing code). Every page a rejected
  * block would have written is zero-filled; pages of -1 entries are untouched.
  * Distinct blocks must not name the same destination page.
@@ -258,7 +261,7 @@ int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_
 /* ---- a2: key -> record index (host) --------------------------------------
  * Open addressing over 32-byte keys, 64-bit handles. Readers may run
  * concurrently; writers need external exclusion. */
-tl_index* tl_index_create(size_t capacity);
+tl_index* tl_index_create(size_t capacity); /* NULL if capacity is 0 or memory is short */
 void tl_index_destroy(tl_index* idx);
 /* insert or overwrite; TL_EFULL beyond capacity */
 int tl_index_put(tl_index* idx, const uint8_t key[TL_KEY_BYTES], uint64_t handle);
@@ -291,8 +294,11 @@ typedef struct tl_dindex tl_dindex;
                                    highest-indexed duplicate's handle wins */
 #define TL_INDEX_FULL 0x20      /* no free slot within reach: not inserted */
 #define TL_INDEX_TAG_CLASH 0x21 /* a different key with the same first eight
-                                   bytes (bit 0 aside) holds the slot: not
-                                   inserted (about 2^-63 per pair of keys) */
+                                   bytes (bit 0 aside) holds a slot on this
+                                   key's probe path: not inserted (about
+                                   2^-63 per pair of keys); lookups compare
+                                   whole keys, so neither is ever taken for
+                                   the other */
 
 /* 256 + 64 * capacity, or 0 unless capacity is a power of two in [2, 2^31]. */
 size_t tl_dindex_bytes(size_t capacity);
