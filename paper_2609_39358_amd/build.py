@@ -54,11 +54,31 @@ def build(verbose: bool = False, extra_hip_flags=(), out: str = OUT, build_dir: 
     return out
 
 
+C_ABI_TEST = os.path.join(PKG, "c_abi_roundtrip")  # test program that uses the C ABI alone
+
+
+def build_c_abi_test(verbose: bool = False) -> str:
+    """A C program (tests/native/c_abi_roundtrip.c) linked against the
+    release library and the HIP runtime only: the GPU tests run it to check
+    the boundary without the Python binding."""
+    cc = os.environ.get("CC") or shutil.which("gcc") or "gcc"
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    tmp = C_ABI_TEST + ".tmp"
+    _run([cc, "-O1", "-std=c11", "-Wall", "-D__HIP_PLATFORM_AMD__", "-I", INCLUDE, "-I", os.path.join(rocm, "include"),
+          os.path.join(ROOT, "tests", "native", "c_abi_roundtrip.c"), "-o", tmp, "-L", PKG, "-ltaliesin",
+          "-L", os.path.join(rocm, "lib"), "-lamdhip64", "-Wl,-rpath,$ORIGIN", "-Wl,-rpath," + os.path.join(rocm, "lib")],
+         verbose)
+    os.replace(tmp, C_ABI_TEST)
+    return C_ABI_TEST
+
+
 def build_all(verbose: bool = False):
-    """The release library and the sabotage build used by the sabotage tests."""
+    """The release library, the sabotage build used by the sabotage tests and
+    the C-ABI test program."""
     out = build(verbose)
     build(verbose, extra_hip_flags=("-DTL_SABOTAGE",), out=SABOTAGE_OUT,
           build_dir=os.path.join(BUILD_DIR, "sabotage"))
+    build_c_abi_test(verbose)
     return out
 
 
