@@ -51,6 +51,112 @@ def stored_traffic():
     return t.get("traffic_bytes_per_launch")
 
 
+def layerwise_save_leg(T, ctx, n, src, blocks, store, d_status, step_bytes, whole_ms, args):
+    """Layer-wise save of the paper corpus (Sec. 2.2: state is saved once the
+    runtime has computed it; one call per layer lets the copy of layer l run
+    while later layers are still being prefilled).
+    (1) 60 one-layer tl_save_layers calls and a tl_save_seal on one stream,
+        against one tl_save of the same blocks.
+    (2) The same calls overlapped with a stand-in for prefill: one bf16 GEMM
+        (torch.mm, [tokens x width] @ [width x width]) per layer on a second
+        stream; the save of layer l waits for layer l's GEMM. The stand-in
+        only occupies the GPU; it does not write the pages. Reports the
+        stand-in alone, the stand-in with the overlapped save, and how much
+        save time remains exposed, for both save kernels (flags 0 and
+        TL_SAVE_SHARED)."""
+    import torch
+
+    L = src.n_layers
+    main = torch.cuda.current_stream()
+    roots = store.buf[:, 144:152].clone()  # the roots of the whole-save records
+
+    def per_layer(s):
+        for l in range(L):
+            T.tl_save_layers(ctx, s, n, src.tl(), blocks, store.ptrs, l, l + 1)
+        T.tl_save_seal(ctx, s, n, src.n_pages, blocks, store.ptrs, d_status)
+
+    per_layer(main)
+    torch.cuda.synchronize()
+    assert (d_status == T.ACCEPT).all().item() and torch.equal(store.buf[:, 144:152], roots), \
+        "layer-wise save differs from the whole save"
+    reps = 3
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        per_layer(main)
+    torch.cuda.synchronize()
+    lw_ms = (time.perf_counter() - t0) * 1e3 / reps
+
+    comp, saver = torch.cuda.Stream(), torch.cuda.Stream()
+    done = [torch.cuda.Event() for _ in range(L)]
+
+    def save_alone(shared):
+        saver.wait_stream(main)
+        for l in range(L):
+            T.tl_save_layers(ctx, saver, n, src.tl(), blocks, store.ptrs, l, l + 1, shared)
+        T.tl_save_seal(ctx, saver, n, src.n_pages, blocks, store.ptrs, d_status)
+
+    def timed(f):
+        f()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            f()
+            torch.cuda.synchronize()
+            t.append((time.perf_counter() - t0) * 1e3)
+        return sorted(t)[reps // 2]
+
+    alone = {}
+    for shared in (False, True):
+        alone[shared] = timed(lambda: save_alone(shared))
+        assert (d_status == T.ACCEPT).all().item() and torch.equal(store.buf[:, 144:152], roots)
+    runs = []
+    for gm in args.layerwise_tokens:  # [gm x gk] @ [gk x gk]: gm tokens through a gk x gk weight
+        gk = args.layerwise_width
+        ga = torch.randn((gm, gk), device=main.device, dtype=torch.bfloat16)
+        gb = torch.randn((gk, gk), device=main.device, dtype=torch.bfloat16)
+        gc = torch.empty((gm, gk), device=main.device, dtype=torch.bfloat16)
+        flop = 2 * gm * gk * gk
+
+        def prefill_only():
+            comp.wait_stream(main)
+            with torch.cuda.stream(comp):
+                for _ in range(L):
+                    torch.mm(ga, gb, out=gc)
+
+        def overlapped(shared):
+            comp.wait_stream(main)
+            saver.wait_stream(main)
+            for l in range(L):
+                with torch.cuda.stream(comp):
+                    torch.mm(ga, gb, out=gc)
+                    done[l].record(comp)
+                saver.wait_event(done[l])
+                T.tl_save_layers(ctx, saver, n, src.tl(), blocks, store.ptrs, l, l + 1, shared)
+            T.tl_save_seal(ctx, saver, n, src.n_pages, blocks, store.ptrs, d_status)
+
+        p_ms = timed(prefill_only)
+        modes = {}
+        for shared in (False, True):
+            o_ms = timed(lambda: overlapped(shared))
+            assert (d_status == T.ACCEPT).all().item() and torch.equal(store.buf[:, 144:152], roots)
+            exposed = max(o_ms - p_ms, 0.0)
+            name = "shared" if shared else "default"
+            modes[name] = {"prefill_with_overlapped_save_ms": o_ms, "save_exposed_ms": exposed,
+                           "save_hidden_frac": 1.0 - exposed / alone[shared]}
+            log("layer-wise save (%s kernel) beside %d-token GEMMs: stand-in prefill %.2f ms, with the "
+                "overlapped save %.2f ms: %.2f ms of %.2f exposed" % (name, gm, p_ms, o_ms, exposed, alone[shared]))
+        runs.append({"stand_in": "one [%d x %d] @ [%d x %d] bf16 GEMM per layer (torch.mm), %.2f TFLOP per layer"
+                                 % (gm, gk, gk, gk, flop / 1e12),
+                     "prefill_stand_in_ms": p_ms, "stand_in_TFLOPs": flop * L / (p_ms * 1e-3) / 1e12,
+                     "overlapped": modes})
+        del ga, gb, gc
+    out = {"layers": L, "blocks": n, "whole_save_ms": whole_ms, "per_layer_calls_ms": lw_ms,
+           "per_layer_GBps": step_bytes / (lw_ms * 1e-3) / 1e9,
+           "per_layer_alone_ms": {"default": alone[False], "shared": alone[True]}, "beside_prefill": runs}
+    return out
+
+
 def multi_request_leg(T, PagedCache, wl, dev):
     """256 requests (lognormal lengths, median 4,096 tokens) sharing 50-95 % of
     their blocks with one of 8 base documents whose 16,384 records (5 %
@@ -287,6 +393,9 @@ def main():
     ap.add_argument("--no-other-configs", action="store_true")
     ap.add_argument("--host-tier-blocks", type=int, default=1024)
     ap.add_argument("--no-disk-tier", action="store_true")
+    ap.add_argument("--no-layerwise", action="store_true")
+    ap.add_argument("--layerwise-tokens", type=int, nargs="+", default=[8192, 65536])
+    ap.add_argument("--layerwise-width", type=int, default=8192)
     ap.add_argument("--disk-tier-blocks", type=int, default=512)
     args = ap.parse_args()
     if args.gpus != 1:
@@ -361,6 +470,9 @@ def main():
             "save_seg_ms": ss_ms / max(ss_n, 1), "save_meta_ms": sm_ms / max(sm_n, 1),
             "hbm_frac": step_bytes / (save_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
     log("save: %.3f ms/step, %.0f GB/s" % (save_ms, save["GBps"]))
+    layerwise = None
+    if not args.no_layerwise:
+        layerwise = layerwise_save_leg(T, ctx, n, src, save_blocks, store, d_status, step_bytes, save_ms, args)
 
     # ---- the same corpus at the paper's block granularity (Sec. 4.1: 11 blocks
     # for the corpus, the last one partial): 550 pages (8,800 tokens) per
@@ -703,6 +815,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "save": save,
+        "layerwise_save": layerwise,
         "host_ms": host,
         "host_tier": host_tier,
         "disk_tier": disk,

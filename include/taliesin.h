@@ -223,11 +223,18 @@ int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* sr
  * and root, and d_status as tl_save does; n_pages is the source cache's page
  * count, used to report TL_BADARG. A record is valid only after its seal, and
  * only if every layer range was saved before the seal (stream order). tl_save
- * is exactly tl_save_layers(0, n_layers) followed by tl_save_seal. TL_EINVAL
- * if layer_begin >= layer_end or layer_end > n_layers. */
+ * is exactly tl_save_layers(0, n_layers, 0) followed by tl_save_seal.
+ * flags: 0, or TL_SAVE_SHARED for a save that runs while kernels of other
+ * streams (the prefill of later layers) keep the device busy: it then uses a
+ * kernel with a smaller footprint (two wavefronts per SIMD), which keeps
+ * pace with such a prefill where the default kernel falls behind it and
+ * finishes after it. Without other work on the device it is about as fast
+ * as flags 0. The bytes written do not depend on flags. TL_EINVAL if
+ * layer_begin >= layer_end, layer_end > n_layers or flags has other bits. */
+#define TL_SAVE_SHARED 1
 int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
                    const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
-                   uint32_t layer_end);
+                   uint32_t layer_end, uint32_t flags);
 int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pages,
                  const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint8_t* d_status);
 

@@ -324,16 +324,16 @@ int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* sr
 
 int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
                    const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
-                   uint32_t layer_end) {
+                   uint32_t layer_end, uint32_t flags) {
   if (!ctx) return TL_EINVAL;
-  if (layer_begin >= layer_end || layer_end > ctx->L) return TL_EINVAL;
+  if (layer_begin >= layer_end || layer_end > ctx->L || (flags & ~TL_SAVE_SHARED)) return TL_EINVAL;
   if (n_blocks == 0) return TL_OK;
   int r = check_cache(ctx, src);
   if (r) return r;
   if ((r = check_blocks(ctx, n_blocks, blocks, false))) return r;
   if (!d_record_ptrs || ((uintptr_t)d_record_ptrs & 7)) return TL_EINVAL;
   return tl::launch_save_layers(ctx, stream, n_blocks, src, blocks, d_record_ptrs, layer_begin,
-                                layer_end);
+                                layer_end, flags);
 }
 
 int tl_save_seal(const tl_ctx* ctx, void* stream, size_t n_blocks, int64_t n_pages,

@@ -78,7 +78,7 @@ int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                 const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status);
 int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                        const tl_blocks* blk, const uint64_t* d_rec, uint32_t layer_begin,
-                       uint32_t layer_end);
+                       uint32_t layer_end, uint32_t flags);
 int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
                      const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status);
 int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,

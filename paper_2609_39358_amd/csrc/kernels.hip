@@ -71,6 +71,9 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 #ifndef TL_SAVE_PREFETCH
 #define TL_SAVE_PREFETCH 0
 #endif
+#ifndef TL_SHARED_SAVE_BATCH_ROWS
+#define TL_SHARED_SAVE_BATCH_ROWS 32  // shared save: rows per batch (no prefetch)
+#endif
 #ifndef TL_NT_LOAD
 #define TL_NT_LOAD 1        // non-temporal (streaming) loads of the source
 #endif
@@ -428,7 +431,10 @@ __device__ uint64_t zero_hash(char* dst, uint32_t rows, uint32_t lane) {
   return c.finish(lane, rows, z);
 }
 
-__global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
+// The chunk loop of the save, for both save kernels: one wavefront per
+// (block, chunk) work item, striding over the grid.
+template <int B, int PF>
+__device__ __forceinline__ void save_chunks(const SegArgs& a) {
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t step = gridDim.x * kSegWaves;
   for (uint32_t w = blockIdx.x * kSegWaves + uniform(threadIdx.x >> 6); w < a.total; w += step) {
@@ -443,10 +449,27 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
     }
     const uint64_t leaf =
         it.page < 0 ? zero_hash(out, it.rows, lane)  // a page the partial block leaves out
-                    : copy_hash<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(page_chunk(a, it), out, it.rows, lane);
+                    : copy_hash<B, PF>(page_chunk(a, it), out, it.rows, lane);
     const uint64_t digest = wave_sum64(leaf);
     if (lane == 0) *(uint64_t*)(rec + tl::kHeaderBytes + 8ull * it.t) = digest;
   }
+}
+
+// The whole device to itself: a whole 64 KiB chunk in flight per wavefront,
+// one wavefront per SIMD (about 300 registers per lane).
+__global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
+  save_chunks<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(a);
+}
+
+// Beside other kernels: half the chunk per batch and at most 256 registers
+// per lane (two wavefronts per SIMD, two workgroups per compute unit). Alone
+// it saves as fast as k_save_seg; while another stream keeps the device busy
+// (a prefill of persistent bf16 GEMMs, one 512-register wavefront per SIMD on
+// every compute unit), its per-layer saves finish within the GEMMs they
+// overlap where k_save_seg's fall behind them.
+__global__ __launch_bounds__(64 * kSegWaves) __attribute__((amdgpu_waves_per_eu(2))) void
+k_save_seg_shared(SegArgs a) {
+  save_chunks<TL_SHARED_SAVE_BATCH_ROWS, 0>(a);
 }
 
 // Root checksum over one metadata tile already staged in LDS: lane k (k < 4)
@@ -776,14 +799,17 @@ namespace tl {
 
 int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                        const tl_blocks* blk, const uint64_t* d_rec, uint32_t layer_begin,
-                       uint32_t layer_end) {
+                       uint32_t layer_end, uint32_t flags) {
   hipStream_t s = (hipStream_t)stream;
   SegArgs a;
   fill_seg(a, ctx, n, d_rec, blk->d_tables, blk->d_n_tokens, src, nullptr, layer_begin, layer_end);
   a.slab_major = TL_SAVE_SLAB_MAJOR;
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
-    hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
+    if (flags & TL_SAVE_SHARED)
+      hipLaunchKernelGGL(k_save_seg_shared, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
+    else
+      hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
   });
   return launched();
 }
@@ -802,7 +828,7 @@ int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
 
 int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                 const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
-  int r = launch_save_layers(ctx, stream, n, src, blk, d_rec, 0, ctx->geo.n_layers);
+  int r = launch_save_layers(ctx, stream, n, src, blk, d_rec, 0, ctx->geo.n_layers, 0);
   if (r) return r;
   return launch_save_seal(ctx, stream, n, src->n_pages, blk, d_rec, d_status);
 }

@@ -87,7 +87,7 @@ def _load():
         "tl_block_keys_batch": (c.c_int, [P, P, P, P, P, c.c_size_t, c.c_size_t, c.c_uint32, P, P, P, c.c_int]),
         "tl_save": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P, P]),
         "tl_save_layers": (c.c_int, [P, P, c.c_size_t, c.POINTER(tl_cache), c.POINTER(tl_blocks), P,
-                                     c.c_uint32, c.c_uint32]),
+                                     c.c_uint32, c.c_uint32, c.c_uint32]),
         "tl_save_seal": (c.c_int, [P, P, c.c_size_t, c.c_int64, c.POINTER(tl_blocks), P, P]),
         "tl_load": (c.c_int, [P, P, c.c_size_t, P, P, c.POINTER(tl_blocks), c.POINTER(tl_cache),
                               P, P, c.c_size_t]),
@@ -145,6 +145,7 @@ KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_
 TL_INDEX_STORED, TL_INDEX_FULL, TL_INDEX_TAG_CLASH = 0x01, 0x20, 0x21
 TL_CHAIN_ALL_KEYS, TL_CHAIN_TAIL = 1, 2
 TL_KEYS_TAIL = 1
+TL_SAVE_SHARED = 1
 MISS = 2**64 - 1
 
 
@@ -301,9 +302,10 @@ def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d
 
 
 def tl_save_layers(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
-                   layer_begin: int, layer_end: int):
+                   layer_begin: int, layer_end: int, shared: bool = False):
     _check(_lib.tl_save_layers(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src),
-                               ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end),
+                               ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end,
+                               TL_SAVE_SHARED if shared else 0),
            "tl_save_layers")
 
 

@@ -14,7 +14,7 @@ namespace tl {
 int launch_save(const tl_ctx*, void*, size_t, const tl_cache*, const tl_blocks*, const uint64_t*,
                 uint8_t*) { return TL_EDEVICE; }
 int launch_save_layers(const tl_ctx*, void*, size_t, const tl_cache*, const tl_blocks*, const uint64_t*,
-                       uint32_t, uint32_t) { return TL_EDEVICE; }
+                       uint32_t, uint32_t, uint32_t) { return TL_EDEVICE; }
 int launch_save_seal(const tl_ctx*, void*, size_t, int64_t, const tl_blocks*, const uint64_t*,
                      uint8_t*) { return TL_EDEVICE; }
 int launch_load(const tl_ctx*, void*, size_t, const uint64_t*, const uint64_t*, const tl_blocks*,
@@ -144,7 +144,8 @@ int main() {
   tl_blocks no_tok = blk;
   no_tok.d_tokens = nullptr;
   EXPECT(tl_save(c, nullptr, 1, &cache, &no_tok, rp, nullptr) == TL_EINVAL);
-  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 1, 1) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 1, 1, 0) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 0, 1, 2) == TL_EINVAL);
   EXPECT(tl_save_seal(c, nullptr, 1, -5, &blk, rp, nullptr) == TL_EINVAL);
   tl_cache narrow = cache;
   narrow.page_stride = 4096;

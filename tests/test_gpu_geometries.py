@@ -53,3 +53,32 @@ def test_edge_geometry_round_trip(name):
         assert vo[1] == ref.SEGMENT
     if n > 2:
         assert vo[2] == ref.ROOT
+
+
+@pytest.mark.parametrize("name", list(GEOMS))
+def test_edge_geometry_shared_save(name):
+    """The save kernel for running beside other work (TL_SAVE_SHARED) writes
+    the oracle's records on every edge geometry, in one layer range and in
+    one-layer parts."""
+    from paper_2609_39358_amd import taliesin as T
+    from paper_2609_39358_amd.device import RecordStore
+    from tests.gpu_case import i32
+    geom, n = GEOMS[name]
+    c = Case(geom, n, n + 2, n + 3, seed=19)
+    c.make_src()
+    recs_o, st_o = c.oracle_save()
+    blk = c.blocks(i32(c.t_src))
+    s = torch.cuda.current_stream()
+    L = geom.n_layers
+    for parts in ([(0, L)], [(l, l + 1) for l in range(L)][::-1]):
+        store = RecordStore(n, c.lay.record_bytes, DEV)
+        store.buf.fill_(0xA5)
+        for a, b in parts:
+            T.tl_save_layers(c.ctx, s, n, c.src.tl(), blk, store.ptrs, a, b, shared=True)
+        st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+        T.tl_save_seal(c.ctx, s, n, c.src_pages, blk, store.ptrs, st)
+        torch.cuda.synchronize()
+        assert [int(x) for x in st.cpu()] == st_o
+        got = store.buf.cpu().numpy()
+        for b in range(n):
+            assert got[b].tobytes() == recs_o[b], (len(parts), b)

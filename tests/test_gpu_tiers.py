@@ -33,8 +33,8 @@ def test_save_by_layer_ranges_equals_whole_save(geom):
     ranges = list(zip(cuts[:-1], cuts[1:]))[::-1]  # any order before the seal
     blk = c.blocks(i32(c.t_src))
     s = torch.cuda.current_stream()
-    for a, b in ranges:
-        T.tl_save_layers(c.ctx, s, n, c.src.tl(), blk, parts.ptrs, a, b)
+    for i, (a, b) in enumerate(ranges):  # both save kernels; the bytes must not depend on the choice
+        T.tl_save_layers(c.ctx, s, n, c.src.tl(), blk, parts.ptrs, a, b, shared=i % 2 == 1)
     st2 = torch.zeros(n, dtype=torch.uint8, device=DEV)
     T.tl_save_seal(c.ctx, s, n, c.src_pages, blk, parts.ptrs, st2)
     torch.cuda.synchronize()
@@ -69,7 +69,7 @@ def test_save_layers_overlapped_with_prefill():
                 t.copy_(torch.randint(0, 256, t.shape, generator=g, device=DEV, dtype=torch.uint8))
             done[l].record(prefill)
         saver.wait_event(done[l])
-        T.tl_save_layers(c.ctx, saver, n, c.src.tl(), blk, store.ptrs, l, l + 1)
+        T.tl_save_layers(c.ctx, saver, n, c.src.tl(), blk, store.ptrs, l, l + 1, shared=True)
     st = torch.zeros(n, dtype=torch.uint8, device=DEV)
     T.tl_save_seal(c.ctx, saver, n, c.src_pages, blk, store.ptrs, st)
     torch.cuda.synchronize()
