@@ -194,7 +194,10 @@ int tl_block_keys(const tl_ctx* ctx, const uint8_t* parent, const void* bytes, s
  * (one chain per thread at a time). doc_off[d], doc_len[d]: byte range of
  * document d in `bytes`; key_off[d]: first key slot of document d in keys_out
  * (caller sizes it for the key count of each document); n_keys_out[d]
- * (optional) receives the number of keys. parents: NULL or [n_docs][32]. */
+ * (optional) receives the number of keys. parents: NULL or [n_docs][32].
+ * bytes, keys_out and key_off may be NULL when every doc_len is 0 (no keys).
+ * TL_EINVAL for a NULL doc_off or doc_len with n_docs > 0, a NULL bytes,
+ * keys_out or key_off with some non-empty document, or unknown flags. */
 int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* bytes,
                         const uint64_t* doc_off, const uint64_t* doc_len, size_t n_docs,
                         size_t block_bytes, uint32_t flags, uint8_t* keys_out, const uint64_t* key_off,

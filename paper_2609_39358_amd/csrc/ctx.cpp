@@ -195,14 +195,18 @@ int tl_block_keys_batch(const tl_ctx* ctx, const uint8_t* parents, const void* b
                         const uint64_t* doc_off, const uint64_t* doc_len, size_t n_docs,
                         size_t block_bytes, uint32_t flags, uint8_t* keys_out, const uint64_t* key_off,
                         uint64_t* n_keys_out, int n_threads) {
-  if (!ctx || (n_docs && (!bytes || !doc_off || !doc_len || !keys_out || !key_off))) return TL_EINVAL;
+  if (!ctx || (n_docs && (!doc_off || !doc_len))) return TL_EINVAL;
   if (flags & ~uint32_t(TL_KEYS_TAIL)) return TL_EINVAL;
+  bool any_bytes = false;  // with no bytes at all there are no keys: the buffers may be absent
+  for (size_t d = 0; d < n_docs; ++d) any_bytes |= doc_len[d] != 0;
+  if (any_bytes && (!bytes || !keys_out || !key_off)) return TL_EINVAL;
   const size_t B = block_bytes ? block_bytes : 4 * (size_t)ctx->geo.block_tokens;
   std::atomic<size_t> next{0};
   auto work = [&]() {
     for (size_t d; (d = next.fetch_add(1)) < n_docs;) {
       const size_t nk = key_count(doc_len[d], B, flags);
       if (n_keys_out) n_keys_out[d] = nk;
+      if (!doc_len[d]) continue;  // no bytes, no keys (its buffers may be absent)
       chain(parents ? parents + 32 * d : ctx->ns, (const uint8_t*)bytes + doc_off[d], doc_len[d], nk, B,
             keys_out + 32 * key_off[d]);
     }

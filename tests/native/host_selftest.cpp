@@ -108,6 +108,12 @@ int main() {
   std::vector<uint64_t> off = {0, 64 * 10, 64 * 25}, len = {64 * 10, 64 * 15 + 3, 64 * 15 + 28}, koff = {0, 10, 25}, nko(3);
   EXPECT(tl_block_keys_batch(c, nullptr, toks.data(), off.data(), len.data(), 3, 0, 0, keys2.data(), koff.data(), nko.data(), 3) == TL_OK);
   EXPECT(nko[0] == 10 && nko[1] == 15 && nko[2] == 15);
+  // documents that are all empty need no buffers; a non-empty one does
+  std::vector<uint64_t> zero3 = {0, 0, 0};
+  EXPECT(tl_block_keys_batch(c, nullptr, nullptr, zero3.data(), zero3.data(), 3, 0, TL_KEYS_TAIL, nullptr, nullptr, nko.data(), 2) == TL_OK);
+  EXPECT(nko[0] == 0 && nko[1] == 0 && nko[2] == 0);
+  EXPECT(tl_block_keys_batch(c, nullptr, nullptr, off.data(), len.data(), 3, 0, 0, keys2.data(), koff.data(), nullptr, 2) == TL_EINVAL);
+  EXPECT(tl_block_keys_batch(c, nullptr, toks.data(), nullptr, len.data(), 3, 0, 0, keys2.data(), koff.data(), nullptr, 2) == TL_EINVAL);
   EXPECT(!memcmp(keys.data(), keys2.data(), 32 * 10));  // the first document is the prefix of the first chain
   // a partial last block gets a key only when asked; it extends the full chain
   EXPECT(tl_block_keys(c, nullptr, toks.data(), toks.size() * 4, 0, TL_KEYS_TAIL, keys2.data(), 41, &nk) == TL_OK &&
