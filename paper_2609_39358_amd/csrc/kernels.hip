@@ -80,11 +80,16 @@ constexpr uint64_t kP5 = 0x27D4EB2F165667C5ull;
 #ifndef TL_NT_STORE
 #define TL_NT_STORE 1       // non-temporal (streaming) stores of the copy
 #endif
-#ifndef TL_SAVE_SLAB_MAJOR
-#define TL_SAVE_SLAB_MAJOR 0  // save work order: 0 = block-major, 1 = slab-major
+// Work orders (which work item a wavefront takes next): 0 block-major (a
+// block's chunks in record order, then the next block), 1 slab-major (one
+// chunk of every block, then the next chunk), 2 block-major with a block's
+// pages outermost (page j of every layer and K|V, then page j + 1; the same
+// as 0 for one-page blocks).
+#ifndef TL_SAVE_ORDER
+#define TL_SAVE_ORDER 0  // the records are written front to back
 #endif
-#ifndef TL_LOAD_SLAB_MAJOR
-#define TL_LOAD_SLAB_MAJOR 0  // load work order: 0 = block-major, 1 = slab-major
+#ifndef TL_LOAD_ORDER
+#define TL_LOAD_ORDER 2  // consecutive wavefronts write the same page of different layers
 #endif
 #ifndef TL_GRID_WGS_PER_CU
 #define TL_GRID_WGS_PER_CU 0  // >0: cap the save chunk grid at this many workgroups per CU
@@ -224,7 +229,7 @@ struct SegArgs {
   uint32_t t_begin;      // first chunk index of the range handled (save by layers)
   uint32_t n_sub;        // chunks per block in that range
   uint32_t total;        // n * n_sub work items
-  uint32_t slab_major;   // 1: consecutive work items are consecutive blocks of one chunk
+  uint32_t order;        // work order (0, 1 or 2, as TL_SAVE_ORDER / TL_LOAD_ORDER)
   uint32_t disabled;     // load checks switched off (sabotage build only; else 0)
   uint32_t* status;      // load: per-block status words
   const uint32_t* n_tokens;  // [n] tokens per block, or null: every block full
@@ -256,13 +261,24 @@ struct Item {
 
 __device__ __forceinline__ Item decode(const SegArgs& a, uint32_t w) {
   Item it;
-  if (a.slab_major) {
+  if (a.order == 1) {
     const uint32_t q = w / a.n;
     it.b = w - q * a.n;
     it.t = a.t_begin + q;
   } else {
     it.b = w / a.n_sub;
-    it.t = a.t_begin + (w - it.b * a.n_sub);
+    const uint32_t r = w - it.b * a.n_sub;
+    if (a.order == 2 && a.g.ppb > 1) {
+      // pages outermost within a block: page j of every (layer, K|V) of the
+      // range, then page j + 1
+      const uint32_t per_page = a.n_sub / a.g.ppb;
+      const uint32_t j = r / per_page;
+      const uint32_t q = r - j * per_page;
+      const uint32_t side = a.t_begin / (a.g.ppb * a.g.cps) + q / a.g.cps;
+      it.t = (side * a.g.ppb + j) * a.g.cps + (q - (q / a.g.cps) * a.g.cps);
+    } else {
+      it.t = a.t_begin + r;
+    }
   }
   it.s = it.t / a.g.cps;
   it.k = it.t - it.s * a.g.cps;
@@ -738,7 +754,7 @@ void fill_seg(SegArgs& a, const tl_ctx* ctx, size_t n, const uint64_t* rec, cons
   a.t_begin = 2 * layer_begin * ctx->geo.ppb * ctx->geo.cps;
   a.n_sub = 2 * (layer_end - layer_begin) * ctx->geo.ppb * ctx->geo.cps;
   a.total = (uint32_t)(n * a.n_sub);
-  a.slab_major = 0;
+  a.order = 0;
   a.disabled = g_disabled_checks;
   a.status = status;
   a.n_tokens = n_tokens;
@@ -803,7 +819,7 @@ int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache
   hipStream_t s = (hipStream_t)stream;
   SegArgs a;
   fill_seg(a, ctx, n, d_rec, blk->d_tables, blk->d_n_tokens, src, nullptr, layer_begin, layer_end);
-  a.slab_major = TL_SAVE_SLAB_MAJOR;
+  a.order = TL_SAVE_ORDER;
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
     if (flags & TL_SAVE_SHARED)
@@ -841,10 +857,10 @@ int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec
   fill_meta(la.m, ctx, n, d_rec, d_len, blk, dst->n_pages, d_ws, nullptr);
   fill_seg(la.s, ctx, n, d_rec, blk->d_tables, blk->d_n_tokens, dst, d_ws);
   la.s.len = d_len;
-  la.s.slab_major = TL_LOAD_SLAB_MAJOR;
+  la.s.order = TL_LOAD_ORDER;
   FinalArgs f;
   f.s = la.s;
-  f.s.slab_major = 0;
+  f.s.order = 0;
   f.verdicts = d_verdicts;
   f.groups = (ctx->geo.n_seg + kFinalGroup - 1) / kFinalGroup;
   f.total_groups = (uint32_t)(n * f.groups);
