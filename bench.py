@@ -504,6 +504,16 @@ def main():
         T.tl_save(ctx_pb, stream, n_pb, src.tl(), blk_pb, store_pb.ptrs, st_pb)
         torch.cuda.synchronize()
         assert (st_pb == T.ACCEPT).all().item()
+        T.tl_timing(True)
+        for k in T.KERNELS:
+            T.tl_timing_read(k)
+        t0 = time.perf_counter()
+        for _ in range(3):
+            T.tl_save(ctx_pb, stream, n_pb, src.tl(), blk_pb, store_pb.ptrs, st_pb)
+        torch.cuda.synchronize()
+        save_pb_ms = (time.perf_counter() - t0) * 1e3 / 3
+        save_pb_kern = {k: T.tl_timing_read(k)[0] / 3 for k in ("save_seg", "save_meta")}
+        assert (st_pb == T.ACCEPT).all().item()
 
     # ---- the store's index: key -> record slot
     idx = T.tl_index_create(n)
@@ -607,6 +617,13 @@ def main():
               "last_block_tokens": tail_pb, "last_block_pages": used_pb,
               "tokens_restored": cfg.n_tokens, "ms": ms_pb, "GBps": bytes_pb / (ms_pb * 1e-3) / 1e9,
               "hbm_frac": bytes_pb / (ms_pb * 1e-3) / 1e9 / HBM_PEAK_GBPS, "kernel_ms": kern_pb}
+        # the save (timed before the source cache was freed): every page that
+        # holds tokens read, every record written whole (zero slabs included)
+        save_bytes_pb = ((n_pb - 1) * ctx_pb.n_slabs + 2 * g.n_layers * used_pb) * ctx_pb.slab_bytes + \
+            n_pb * ctx_pb.record_bytes
+        pb.update({"save_ms": save_pb_ms, "save_GBps": save_bytes_pb / (save_pb_ms * 1e-3) / 1e9,
+                   "save_kernel_ms": save_pb_kern})
+        log("paper-granularity save: %.3f ms, %.0f GB/s, kernels %s" % (save_pb_ms, pb["save_GBps"], save_pb_kern))
         log("paper-granularity restore: %d x %.2f GB records (the last %d tokens on %d pages), %.3f ms, %.0f GB/s, "
             "kernels %s" % (n_pb, ctx_pb.record_bytes / 1e9, tail_pb, used_pb, ms_pb, pb["GBps"], kern_pb))
         del store_pb

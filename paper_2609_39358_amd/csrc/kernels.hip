@@ -502,6 +502,17 @@ __device__ __forceinline__ void hash_tile(const uint64_t* tile64, uint32_t n_byt
   }
 }
 
+// The same over a tile whose words were already multiplied by P2 (the
+// product does not depend on the accumulator, so the threads that stage the
+// tile compute it); the root's word is zero, and so is its product.
+__device__ __forceinline__ void hash_tile_premul(const uint64_t* tile64, uint32_t n_bytes, uint32_t lane,
+                                                 uint64_t& acc) {
+  if (lane < 4) {
+    const uint32_t stripes = n_bytes / 32;
+    for (uint32_t st = 0; st < stripes; ++st) acc = rotl64(acc + tile64[st * 4 + lane], 31) * kP1;
+  }
+}
+
 __device__ __forceinline__ uint64_t finish_root(uint64_t acc, uint64_t len) {
   const uint64_t v1 = readlane64(acc, 0), v2 = readlane64(acc, 1), v3 = readlane64(acc, 2),
                  v4 = readlane64(acc, 3);
@@ -519,65 +530,101 @@ __device__ __forceinline__ uint64_t root_init(uint32_t lane) {
   return lane == 0 ? kP1 + kP2 : lane == 1 ? kP2 : lane == 2 ? 0 : (uint64_t)0 - kP1;
 }
 
-__global__ __launch_bounds__(64) void k_save_meta(MetaArgs a) {
-  __shared__ uint64_t tile64[kMetaTile / 8];
-  uint32_t* tile32 = (uint32_t*)tile64;
-  const uint32_t lane = threadIdx.x;
+// One word of block b's metadata at byte offset o: header fields from the
+// context's template and the block's arguments, chunk digests (already in
+// the record, written by k_save_seg), token ids, zero padding.
+struct MetaWords {
+  const uint32_t* key32;
+  const uint32_t* tok;
+  uint64_t bi;
+  uint32_t tk, tail;
+};
+
+__device__ __forceinline__ uint32_t meta_word(const MetaArgs& a, const MetaWords& m, uint64_t rec, uint32_t o) {
+  if (o < tl::kHeaderBytes) {
+    if (o == tl::kIndexOffset) return (uint32_t)m.bi;
+    if (o == tl::kIndexOffset + 4) return (uint32_t)(m.bi >> 32);
+    if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) return m.key32[(o - tl::kKeyOffset) / 4];
+    if (o == tl::kTailOffset) return m.tail;
+    return a.tmpl[o / 4];  // root field is zero in the template
+  }
+  if (o < a.g.tok_off) return *(const uint32_t*)(rec + o);
+  if (o < a.g.tok_end) {
+    const uint32_t wi = (o - a.g.tok_off) / 4;
+    return wi < m.tk ? m.tok[wi] : 0;
+  }
+  return 0;
+}
+
+// Metadata of one block per workgroup of kMetaThreads threads: each thread
+// assembles one 16-byte granule of a 4 KiB tile (the chunk digests, most of
+// the metadata of a multi-page block, with one 16-byte load), writes it to
+// the record unless it holds only digests, and puts its two words times P2
+// in LDS; lanes 0-3 of the first wavefront run the rest of the XXH64 rounds
+// over the previous tile meanwhile (two LDS buffers). The 16 bytes holding
+// the root are written last.
+constexpr uint32_t kMetaThreads = kMetaTile / 16;
+
+__global__ __launch_bounds__(kMetaThreads) void k_save_meta(MetaArgs a) {
+  __shared__ uint64_t tile[2][kMetaTile / 8];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t lane = tid & 63;
   const uint32_t b = blockIdx.x;
   const uint64_t rec = a.rec[b];
   if (rec == 0 || (rec & 15)) {
-    if (lane == 0 && a.out_status) a.out_status[b] = rec == 0 ? TL_MISSING : TL_BADARG;
+    if (tid == 0 && a.out_status) a.out_status[b] = rec == 0 ? TL_MISSING : TL_BADARG;
     return;
   }
   const uint32_t meta = (uint32_t)a.g.payload_offset;
   const uint32_t tk = block_tok(a.g, a.n_tokens, b);
+  // every wavefront checks the table (the same answer), so the whole
+  // workgroup takes the same branch
   if (tk == 0 || !block_pages_ok(a.g, a.tables, a.n, b, a.n_pages, 0, lane, pages_used(a.g, tk))) {
     v4u* d = (v4u*)rec;
-    for (uint32_t i = lane; i < meta / 16; i += 64) d[i] = zero4();
-    if (lane == 0 && a.out_status) a.out_status[b] = TL_BADARG;
+    for (uint32_t i = tid; i < meta / 16; i += kMetaThreads) d[i] = zero4();
+    if (tid == 0 && a.out_status) a.out_status[b] = TL_BADARG;
     return;
   }
-  const uint32_t tail = tk < a.g.block_tokens ? tk : 0;
-  const uint32_t* key32 = (const uint32_t*)(a.keys + 32ull * b);
-  const uint32_t* tok = a.tokens + (uint64_t)a.g.block_tokens * b;
-  const uint64_t bi = a.bidx[b];
+  MetaWords m;
+  m.tail = tk < a.g.block_tokens ? tk : 0;
+  m.key32 = (const uint32_t*)(a.keys + 32ull * b);
+  m.tok = a.tokens + (uint64_t)a.g.block_tokens * b;
+  m.bi = a.bidx[b];
+  m.tk = tk;
+  auto stage = [&](uint32_t off, uint64_t* buf) {
+    const uint32_t o = off + 16 * tid;
+    if (o >= meta) return;
+    v4u x;
+    if (o >= tl::kHeaderBytes && o + 16 <= a.g.tok_off) {
+      x = *(const v4u*)(rec + o);  // chunk digests: already in place
+    } else {
+      x = v4u{meta_word(a, m, rec, o), meta_word(a, m, rec, o + 4), meta_word(a, m, rec, o + 8),
+              meta_word(a, m, rec, o + 12)};
+      if (o != tl::kRootOffset) *(v4u*)(rec + o) = x;
+    }
+    // the root field is zero in x (the template holds zeros there)
+    buf[2 * tid] = ((uint64_t)x.y << 32 | x.x) * kP2;
+    buf[2 * tid + 1] = ((uint64_t)x.w << 32 | x.z) * kP2;
+  };
   uint64_t acc = root_init(lane);
-  for (uint32_t off = 0; off < meta; off += kMetaTile) {
-    const uint32_t nb = meta - off < kMetaTile ? meta - off : kMetaTile;
-    for (uint32_t wd = lane; wd < nb / 4; wd += 64) {
-      const uint32_t o = off + 4 * wd;
-      uint32_t x;
-      if (o < tl::kHeaderBytes) {
-        if (o == tl::kIndexOffset) x = (uint32_t)bi;
-        else if (o == tl::kIndexOffset + 4) x = (uint32_t)(bi >> 32);
-        else if (o >= tl::kKeyOffset && o < tl::kKeyOffset + 32) x = key32[(o - tl::kKeyOffset) / 4];
-        else if (o == tl::kTailOffset) x = tail;
-        else x = a.tmpl[o / 4];  // root field is zero in the template
-      } else if (o < a.g.tok_off) {
-        x = *(const uint32_t*)(rec + o);  // chunk digest written by k_save_seg
-      } else if (o < a.g.tok_end) {
-        const uint32_t wi = (o - a.g.tok_off) / 4;
-        x = wi < tk ? tok[wi] : 0;
-      } else {
-        x = 0;
-      }
-      tile32[wd] = x;
+  stage(0, tile[0]);
+  __syncthreads();
+  for (uint32_t off = 0, t = 0; off < meta; off += kMetaTile, ++t) {
+    if (off + kMetaTile < meta) stage(off + kMetaTile, tile[(t + 1) & 1]);
+    if (tid < 64) {
+      const uint32_t nb = meta - off < kMetaTile ? meta - off : kMetaTile;
+      hash_tile_premul(tile[t & 1], nb, lane, acc);
     }
     __syncthreads();
-    hash_tile(tile64, nb, off, lane, acc);
-    // write the tile back; the 16 bytes holding the root are written last
-    const v4u* t4 = (const v4u*)tile64;
-    v4u* d = (v4u*)(rec + off);
-    for (uint32_t i = lane; i < nb / 16; i += 64)
-      if (off + 16 * i != tl::kRootOffset) d[i] = t4[i];
-    __syncthreads();
   }
-  const uint64_t root = finish_root(acc, meta);
-  if (lane == 0) {
-    // bytes 152..159: pages per block (from the expected header), then the tail field
-    *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32),
-                                         a.tmpl[tl::kPpbOffset / 4], tail};
-    if (a.out_status) a.out_status[b] = TL_ACCEPT;
+  if (tid < 64) {
+    const uint64_t root = finish_root(acc, meta);
+    if (tid == 0) {
+      // bytes 152..159: pages per block (from the expected header), then the tail field
+      *(v4u*)(rec + tl::kRootOffset) = v4u{(uint32_t)root, (uint32_t)(root >> 32),
+                                           a.tmpl[tl::kPpbOffset / 4], m.tail};
+      if (a.out_status) a.out_status[b] = TL_ACCEPT;
+    }
   }
 }
 
@@ -837,7 +884,7 @@ int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
   fill_meta(m, ctx, n, d_rec, nullptr, blk, n_pages, nullptr, d_status);
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_META, s, [&] {
-    hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(64), 0, s, m);
+    hipLaunchKernelGGL(k_save_meta, dim3((uint32_t)n), dim3(kMetaThreads), 0, s, m);
   });
   return launched();
 }
