@@ -308,14 +308,13 @@ def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
 
     out = {}
     stream = torch.cuda.current_stream()
-    for ci in (0, 1, 4):
-        cfg = wl.CONFIGS[ci]
+    for cfg in (wl.TINY, wl.MID, wl.HYBRID):
         g = cfg.geom
         P = g.page_tokens
         n = cfg.n_tokens // P
         tokens = wl.tokens(cfg.n_tokens, cfg.seed)
-        ctx = T.tl_ctx_create(b"bench-tenant", b"model-%d" % ci, g.n_layers, g.n_kv_heads, g.head_dim, g.dtype,
-                              P, list(g.layer_window) or None, list(g.layer_group) or None)
+        ctx = T.tl_ctx_create(b"bench-tenant", b"model-" + cfg.name.encode(), g.n_layers, g.n_kv_heads,
+                              g.head_dim, g.dtype, P, list(g.layer_window) or None, list(g.layer_group) or None)
         rb, slab = ctx.record_bytes, ctx.slab_bytes
         src = PagedCache(g.n_layers, cfg.src_pages, slab, dev)
         for l in range(g.n_layers):
@@ -368,7 +367,7 @@ def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
             "load_ms": load_ms, "load_GBps": load_bytes / (load_ms * 1e-3) / 1e9,
             "load_main_ms": main_ms / max(cnt, 1), "save_ms": save_ms,
             "save_GBps": save_bytes / (save_ms * 1e-3) / 1e9}
-        if ci == 4:
+        if cfg is wl.HYBRID:
             out[cfg.name]["hbm_frac"] = out[cfg.name]["load_GBps"] / HBM_PEAK_GBPS
         log("%s: save %.3f ms (%.0f GB/s), load %.3f ms for %.2f GB (%.0f GB/s)"
             % (cfg.name, save_ms, out[cfg.name]["save_GBps"], load_ms, load_bytes / 1e9, out[cfg.name]["load_GBps"]))
@@ -399,7 +398,7 @@ def main():
     ap.add_argument("--disk-tier-blocks", type=int, default=512)
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one MI355X: this build has no multi-GPU path "
+        print("bench.py measures one MI355X: this library has no multi-GPU path "
               "(--gpus %d is not supported; run with --gpus 1)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     if int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -423,7 +422,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = "cuda"
-    cfg = wl.CONFIGS[2]
+    cfg = wl.PAPER_CORPUS
     g = cfg.geom
     P = g.page_tokens
     tokens = wl.tokens(cfg.n_tokens, cfg.seed)

@@ -51,7 +51,7 @@ def check_pages_equal(c: Case, dst: PagedCache, tables, blocks=None):
 
 
 def test_paper_corpus_full_scale():
-    cfg = wl.CONFIGS[2]
+    cfg = wl.PAPER_CORPUS
     n = cfg.n_tokens // cfg.geom.page_tokens
     c = Case(cfg.geom, n, cfg.src_pages, cfg.dst_pages, cfg.seed)
     log("paper corpus: %d blocks, %.1f GB of records" % (n, n * c.lay.record_bytes / 1e9))
@@ -110,7 +110,7 @@ def test_paper_corpus_full_scale():
 
 
 def test_hybrid_full_scale():
-    cfg = wl.CONFIGS[4]
+    cfg = wl.HYBRID
     g = cfg.geom
     n = cfg.n_tokens // g.page_tokens
     c = Case(g, n, cfg.src_pages, cfg.dst_pages, cfg.seed)
@@ -164,7 +164,7 @@ def test_paper_sized_blocks_full_scale():
     per block. Every block is checked by verdicts and the permutation-copy
     property; the oracle recomputes the metadata of every record and the
     digests of 256 sampled chunks from the record bytes."""
-    base = wl.CONFIGS[2].geom
+    base = wl.PAPER_CORPUS.geom
     geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
     n = 97000 // geom.block_tokens
     assert n == 11
@@ -221,7 +221,7 @@ def test_paper_sized_blocks_with_the_partial_last_block():
     pages; the other 537 are left out of the save and not restored), each a
     4.3 GB record. The tail record is checked field by field against the
     oracle; every block by verdicts and the permutation copy of its pages."""
-    base = wl.CONFIGS[2].geom
+    base = wl.PAPER_CORPUS.geom
     geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
     bt, ppb = geom.block_tokens, 550
     toks = wl.tokens(97000, 2)

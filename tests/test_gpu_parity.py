@@ -53,7 +53,7 @@ def check_restore(c: Case, recs, ptrs, lens, tables, dst, hk0, hv0, tokens=True,
 
 
 def test_tiny_workload_parity():
-    cfg = wl.CONFIGS[0]
+    cfg = wl.TINY
     c = Case(cfg.geom, 64, cfg.src_pages, cfg.dst_pages, cfg.seed)
     c.make_src()
     store, st = c.save()
@@ -214,7 +214,7 @@ def test_empty_calls_are_noops():
 
 
 def test_mid_workload_parity():
-    cfg = wl.CONFIGS[1]
+    cfg = wl.MID
     c = Case(cfg.geom, cfg.n_tokens // cfg.geom.page_tokens, cfg.src_pages, cfg.dst_pages, cfg.seed)
     c.make_src()
     store, st = c.save()

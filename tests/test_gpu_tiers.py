@@ -16,7 +16,7 @@ from tests.gpu_case import DEV, Case, host_layers, i32, i64, log, random_fill
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("geom", [wl.CONFIGS[0].geom,
+@pytest.mark.parametrize("geom", [wl.TINY.geom,
                                   wl.hybrid_geometry(n_layers=6, n_kv_heads=2, head_dim=64,
                                                      page_tokens=16, window=32),
                                   wl.Geometry(3, 16, 128, 32),
@@ -94,7 +94,7 @@ def test_save_layers_argument_errors():
 
 @pytest.mark.parametrize("name", ["tiny", "two_chunks"])
 def test_restore_from_pinned_host_records(name):
-    geom = wl.CONFIGS[0].geom if name == "tiny" else wl.Geometry(2, 16, 128, 32)
+    geom = wl.TINY.geom if name == "tiny" else wl.Geometry(2, 16, 128, 32)
     n = 40
     c = Case(geom, n, 64, 64, seed=15)
     c.make_src()

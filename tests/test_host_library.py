@@ -70,9 +70,9 @@ def _ctx(cfg, tenant=TEN, fp=FP):
                            list(g.layer_window) or None, list(g.layer_group) or None)
 
 
-@pytest.mark.parametrize("i", [0, 1, 2, 3, 4])
-def test_geometry_and_namespace_match_oracle(i):
-    cfg = wl.CONFIGS[i]
+@pytest.mark.parametrize("name", list(wl.WORKLOADS))
+def test_geometry_and_namespace_match_oracle(name):
+    cfg = wl.WORKLOADS[name]
     lay = _layout(cfg)
     c = _ctx(cfg)
     assert (c.record_bytes, c.payload_offset, c.slab_bytes) == (lay.record_bytes, lay.payload_offset,
@@ -102,7 +102,7 @@ def test_identity_gate_and_layout_errors():
 
 
 def test_keys_match_oracle():
-    cfg = wl.CONFIGS[2]
+    cfg = wl.PAPER_CORPUS
     c = _ctx(cfg)
     lay = _layout(cfg)
     toks = wl.tokens(cfg.n_tokens, cfg.seed)
@@ -118,7 +118,7 @@ def test_keys_match_oracle():
 
 
 def test_block_keys_capacity_error():
-    c = _ctx(wl.CONFIGS[0])
+    c = _ctx(wl.TINY)
     n = ctypes.c_size_t(0)
     buf = bytes(64 * 3)
     out = (ctypes.c_uint8 * 64)()
@@ -130,7 +130,7 @@ def test_block_keys_capacity_error():
 
 
 def test_batch_keys_match_single_chains():
-    cfg = wl.CONFIGS[3]
+    cfg = wl.MULTI_REQUEST
     c = _ctx(cfg)
     docs = [wl.tokens(n, 5, i) for i, n in enumerate([0, 15, 16, 17, 1000, 4096, 33])]
     got = T.tl_block_keys_batch(c, docs, n_threads=4)
@@ -144,7 +144,7 @@ def test_batch_keys_match_single_chains():
 
 def test_tail_keys_match_oracle():
     """Partial last blocks: the library's keys equal the oracle's, single and batched."""
-    cfg = wl.CONFIGS[3]
+    cfg = wl.MULTI_REQUEST
     c = _ctx(cfg)
     ns = T.tl_ns_digest(c)
     docs = [wl.tokens(n, 6, i) for i, n in enumerate([0, 1, 15, 16, 17, 1000, 4099])]
@@ -178,7 +178,7 @@ def test_index_put_get():
 
 
 def test_save_load_argument_validation_enqueues_nothing():
-    c = _ctx(wl.CONFIGS[0])
+    c = _ctx(wl.TINY)
     L = T.lib()
     good_cache = T.make_cache(0x10000, 0x20000, c.slab_bytes, 128)
     good_blk = T.make_blocks(0x30000, 0x40000, 0x50000, 0x60000)

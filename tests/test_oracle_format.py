@@ -34,10 +34,10 @@ def rand_bytes(n, seed):
 # ---------------------------------------------------------------- geometry
 def test_geometry_of_the_five_workloads():
     # slab, metadata and record sizes of the five workloads
-    cases = {0: (8192, 512, 66048), 1: (32768, 1024, 2098176), 2: (65536, 1280, 7865600),
-             4: (1048576, 13568, 100676864)}
-    for i, (slab, meta, rec) in cases.items():
-        g = wl.CONFIGS[i].geom
+    cases = {"tiny": (8192, 512, 66048), "mid": (32768, 1024, 2098176), "paper_corpus": (65536, 1280, 7865600),
+             "hybrid": (1048576, 13568, 100676864)}
+    for name, (slab, meta, rec) in cases.items():
+        g = wl.WORKLOADS[name].geom
         lay = ref.Layout(g.n_layers, g.n_kv_heads, g.head_dim, 1, g.page_tokens,
                          g.layer_window, g.layer_group)
         assert (lay.slab_bytes, lay.meta_bytes, lay.record_bytes) == (slab, meta, rec)

@@ -78,13 +78,12 @@ class Config:
 
 
 # The five workloads (shapes of the paper's corpus scaled to its 31B-class model).
-CONFIGS = {
-    0: Config("tiny", Geometry(4, 4, 64, 16), 1024, 128, 128, n_flips=2, seed=0),
-    1: Config("mid", Geometry(32, 8, 128, 16), 8192, 1024, 1024, seed=1),
-    2: Config("paper_corpus", Geometry(60, 16, 128, 16), 97000, 6062, 6062, seed=2),
-    3: Config("multi_request", Geometry(32, 8, 128, 16), 0, 0, 0, seed=3),
-    4: Config("hybrid", hybrid_geometry(), 65536, 256, 256, seed=4),
-}
+TINY = Config("tiny", Geometry(4, 4, 64, 16), 1024, 128, 128, n_flips=2, seed=0)
+MID = Config("mid", Geometry(32, 8, 128, 16), 8192, 1024, 1024, seed=1)
+PAPER_CORPUS = Config("paper_corpus", Geometry(60, 16, 128, 16), 97000, 6062, 6062, seed=2)
+MULTI_REQUEST = Config("multi_request", Geometry(32, 8, 128, 16), 0, 0, 0, seed=3)
+HYBRID = Config("hybrid", hybrid_geometry(), 65536, 256, 256, seed=4)
+WORKLOADS = {c.name: c for c in (TINY, MID, PAPER_CORPUS, MULTI_REQUEST, HYBRID)}
 
 
 def rng(seed: int, *stream: int) -> np.random.Generator:
@@ -198,7 +197,7 @@ def multi_request(n_requests=256, n_base=8, base_tokens=32768, median=4096, sigm
     are copied from one of `n_base` seeded base documents; `corrupt_frac` of the
     stored base records are damaged, half by one bit flip, half by truncation.
     Record ids are doc * blocks_per_doc + block."""
-    geom = geom or CONFIGS[3].geom
+    geom = geom or MULTI_REQUEST.geom
     P = geom.page_tokens
     base_docs = [tokens(base_tokens, seed, 100 + d) for d in range(n_base)]
     r = rng(seed, 4)
