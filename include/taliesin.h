@@ -30,8 +30,9 @@
  *   - Return value: TL_OK (0) or a negative TL_E* status. On a negative status
  *     nothing was enqueued, except TL_EDEVICE, which reports a failed launch.
  *     A problem with one block is never a status: it is that block's verdict.
- *   - One call handles fewer than 2^24 blocks, and n_blocks times the number
- *     of chunk digests per record must be below 2^32 (TL_ERANGE otherwise).
+ *   - One call handles fewer than 2^24 blocks, and n_blocks times one more
+ *     than the number of chunk digests per record must be below 2^31
+ *     (TL_ERANGE otherwise).
  *   - No call throws; a context is immutable after creation and may be used
  *     from several host threads; concurrent tl_load calls need separate
  *     workspaces.

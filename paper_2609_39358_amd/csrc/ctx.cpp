@@ -309,9 +309,11 @@ static int check_blocks(const tl_ctx* ctx, size_t n, const tl_blocks* b, bool ne
   if (need_tokens && !b->d_tokens) return TL_EINVAL;
   if (((uintptr_t)b->d_keys | (uintptr_t)b->d_tokens | (uintptr_t)b->d_tables) & 3) return TL_EINVAL;
   if ((uintptr_t)b->d_block_index & 7) return TL_EINVAL;
-  // (block, chunk) work items are indexed with 32 bits; per-block kernels
-  // launch one workgroup of up to 256 work-items per block
-  if ((uint64_t)n * ctx->geo.n_seg >= (1ull << 32) || n >= (1ull << 24)) return TL_ERANGE;
+  // work items (one per block and one per (block, chunk)) are counted in 32
+  // bits and the kernels stride over them by at most 2^24 workgroups: below
+  // 2^31 items no index can wrap. Per-block kernels launch one workgroup per
+  // block.
+  if ((uint64_t)n * ((uint64_t)ctx->geo.n_seg + 1) >= (1ull << 31) || n >= (1ull << 24)) return TL_ERANGE;
   return TL_OK;
 }
 

@@ -221,6 +221,22 @@ def test_save_load_argument_validation_enqueues_nothing():
     assert seal(good_blk, n_pages=-1) == T.TL_EINVAL
     # grid index must fit in 32 bits
     assert load(n=(1 << 32) // c.n_segments + 1, wsb=1 << 40) == T.TL_ERANGE
+    # work items (blocks plus (block, chunk) pairs) stay below 2^31, so that a
+    # kernel's strided item index cannot wrap: records of 550 pages have
+    # 66,000 chunk digests, and 40,000 of them are refused although
+    # 40,000 x 66,000 is below 2^32
+    g = wl.PAPER_CORPUS.geom
+    big = T.tl_ctx_create(TEN, FP, g.n_layers, g.n_kv_heads, g.head_dim, "bf16", g.page_tokens,
+                          pages_per_block=550)
+    assert big.n_segments == 66000
+    lim = (1 << 31) // (big.n_segments + 1)
+    big_cache = T.make_cache(0x10000, 0x20000, big.slab_bytes, 128)
+    for n, want in ((40000, T.TL_ERANGE), (lim + 1, T.TL_ERANGE)):
+        assert n * big.n_segments < 1 << 32
+        assert L.tl_load(big.handle, None, n, 0x70000, 0x80000, P(good_blk), P(big_cache), 0x90000, 0xA0000,
+                         1 << 40) == want
+        assert L.tl_save(big.handle, None, n, P(big_cache), P(good_blk), 0x70000, None) == want
+        assert L.tl_save_layers(big.handle, None, n, P(big_cache), P(good_blk), 0x70000, 0, 1, 0) == want
 
 
 def test_status_and_verdict_strings():
