@@ -19,6 +19,18 @@ The paper withholds the storage format (Sec. 1, last paragraph of the
 contributions), so the record layout, the key chain and the tree-mode
 checksum below are this project's readings of what the paper leaves open.
 
+Parity unpinned (by the paper): the byte positions of the header fields, the
+namespace encoding, the verdict codes and their precedence, and the
+zero-fill of a rejected block's pages. The paper prints no worked example
+of any of them. The tests pin only their properties: every single-bit flip
+and every truncation of a record is rejected; restore equals the permutation
+copy; keys are deterministic and chained; tenants are separated. A golden
+record written by this module guards the layout against accidental change.
+The hashes (hashlib SHA-256, xxhash XXH64), the tree checksum's column
+orientation and the reuse walk are pinned independently: by known-answer
+vectors, a second XXH64 written from its published definition, closed-form
+inputs and brute force.
+
 Library primitives used as steps: hashlib.sha256 (FIPS 180-4) and
 xxhash.xxh64 (the published XXH64 algorithm). Both are pinned by known-answer
 vectors in tests/golden.
