@@ -6,6 +6,7 @@ checked are the library's. Paper Sec. 2.2 (a later request that contains the
 same block loads it instead of recomputing) and Fig. 1."""
 from __future__ import annotations
 
+from contextlib import contextmanager
 from dataclasses import dataclass
 from typing import List, Sequence
 
@@ -16,6 +17,19 @@ from . import taliesin as T
 from .device import PagedCache, RecordStore
 
 MISS = np.uint64(2**64 - 1)
+
+
+@contextmanager
+def _on(stream):
+    """Runs a call's torch work (allocations, copies, index arithmetic, status
+    checks) on `stream`, the stream its library calls are enqueued on, after
+    everything the caller has already enqueued on its current stream (the
+    inputs). Results are valid once `stream` has caught up."""
+    cur = torch.cuda.current_stream()
+    if stream != cur:
+        stream.wait_stream(cur)
+    with torch.cuda.stream(stream):
+        yield
 
 
 @dataclass
@@ -78,23 +92,24 @@ class RestorePipeline:
         n = int(rid.size)
         if n > self.pool.n_pages:
             raise ValueError("batch needs %d pages, pool has %d" % (n, self.pool.n_pages))
-        verd = torch.zeros(max(n, 1), dtype=torch.uint8, device=self.dev)
-        res = BatchResult(list(request_ids), hits, rid, np.concatenate(pos) if pos else rid,
-                          np.concatenate(req) if req else np.zeros(0, np.int64), verd[:n], t1 - t0)
-        if n == 0:
-            return res
-        base = np.uint64(self.store.records.buf.data_ptr())
-        ptrs = (base + rid * np.uint64(self.ctx.record_bytes)).view(np.int64)
-        lens = self.store.lens[rid].view(np.int64)
-        to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(self.dev, non_blocking=False)
-        d_ptrs, d_lens = to_dev(ptrs), to_dev(lens)
-        d_keys = to_dev(np.concatenate(kk))
-        d_pos = to_dev(res.positions.view(np.int64))
-        d_tok = to_dev(np.concatenate(tk).view(np.int32))
-        d_tab = to_dev(np.arange(n, dtype=np.int32)[None, :])
-        T.tl_load(self.ctx, self.stream, n, d_ptrs, d_lens, T.make_blocks(d_keys, d_pos, d_tok, d_tab),
-                  self.pool.tl(), verd, self.ws, self.ws_bytes)
-        res._keep = (d_ptrs, d_lens, d_keys, d_pos, d_tok, d_tab)
+        with _on(self.stream):
+            verd = torch.empty(max(n, 1), dtype=torch.uint8, device=self.dev)  # tl_load writes all n
+            res = BatchResult(list(request_ids), hits, rid, np.concatenate(pos) if pos else rid,
+                              np.concatenate(req) if req else np.zeros(0, np.int64), verd[:n], t1 - t0)
+            if n == 0:
+                return res
+            base = np.uint64(self.store.records.buf.data_ptr())
+            ptrs = (base + rid * np.uint64(self.ctx.record_bytes)).view(np.int64)
+            lens = self.store.lens[rid].view(np.int64)
+            to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(self.dev, non_blocking=False)
+            d_ptrs, d_lens = to_dev(ptrs), to_dev(lens)
+            d_keys = to_dev(np.concatenate(kk))
+            d_pos = to_dev(res.positions.view(np.int64))
+            d_tok = to_dev(np.concatenate(tk).view(np.int32))
+            d_tab = to_dev(np.arange(n, dtype=np.int32)[None, :])
+            T.tl_load(self.ctx, self.stream, n, d_ptrs, d_lens, T.make_blocks(d_keys, d_pos, d_tok, d_tab),
+                      self.pool.tl(), verd, self.ws, self.ws_bytes)
+            res._keep = (d_ptrs, d_lens, d_keys, d_pos, d_tok, d_tab)
         return res
 
 
@@ -137,16 +152,17 @@ class DeviceStore:
         blocks. Returns the device save status [n]."""
         stream = stream or torch.cuda.current_stream()
         n = d_keys.shape[0]
-        status = torch.zeros(max(n, 1), dtype=torch.uint8, device=self.device)
-        if n == 0:
-            return status[:0]
-        ptrs = self.records.ptrs.index_select(0, d_slots)
-        T.tl_save(self.ctx, stream, n, src.tl(), T.make_blocks(d_keys, d_positions, d_tokens, d_tables, d_n_tokens),
-                  ptrs, status)
-        if not bool((status[:n] == T.ACCEPT).all()):
-            raise RuntimeError("save refused some blocks (bad page ids)")
-        self.records.lens.index_fill_(0, d_slots, self.ctx.record_bytes)
-        self.add(d_keys, d_tokens, d_positions, d_slots, stream, d_n_tokens)
+        with _on(stream):
+            status = torch.empty(max(n, 1), dtype=torch.uint8, device=self.device)  # tl_save writes all n
+            if n == 0:
+                return status[:0]
+            ptrs = self.records.ptrs.index_select(0, d_slots)
+            T.tl_save(self.ctx, stream, n, src.tl(),
+                      T.make_blocks(d_keys, d_positions, d_tokens, d_tables, d_n_tokens), ptrs, status)
+            if not bool((status[:n] == T.ACCEPT).all()):
+                raise RuntimeError("save refused some blocks (bad page ids)")
+            self.records.lens.index_fill_(0, d_slots, self.ctx.record_bytes)
+            self.add(d_keys, d_tokens, d_positions, d_slots, stream, d_n_tokens)
         return status[:n]
 
     def add(self, d_keys: torch.Tensor, d_tokens: torch.Tensor, d_positions: torch.Tensor,
@@ -158,16 +174,17 @@ class DeviceStore:
         n = d_keys.shape[0]
         if n == 0:
             return
-        self.slot_keys.index_copy_(0, d_slots, d_keys)
-        fps = torch.empty((n, 32), dtype=torch.uint8, device=self.device)
-        T.tl_block_fingerprints(self.ctx, stream, n, d_tokens, d_positions, fps, d_n_tokens)
-        wsb = T.tl_dindex_workspace_bytes(n)
-        ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
-        st = torch.empty(n, dtype=torch.uint8, device=self.device)
-        for idx, k in ((self.key_index, d_keys), (self.token_index, fps)):
-            idx.put(stream, n, k, d_slots, st, ws, wsb)
-            if not bool((st == T.TL_INDEX_STORED).all()):
-                raise RuntimeError("device index refused keys (full or tag clash)")
+        with _on(stream):
+            self.slot_keys.index_copy_(0, d_slots, d_keys)
+            fps = torch.empty((n, 32), dtype=torch.uint8, device=self.device)
+            T.tl_block_fingerprints(self.ctx, stream, n, d_tokens, d_positions, fps, d_n_tokens)
+            wsb = T.tl_dindex_workspace_bytes(n)
+            ws = torch.empty(wsb, dtype=torch.uint8, device=self.device)
+            st = torch.empty(n, dtype=torch.uint8, device=self.device)
+            for idx, k in ((self.key_index, d_keys), (self.token_index, fps)):
+                idx.put(stream, n, k, d_slots, st, ws, wsb)
+                if not bool((st == T.TL_INDEX_STORED).all()):
+                    raise RuntimeError("device index refused keys (full or tag clash)")
 
 
 @dataclass
@@ -202,32 +219,33 @@ class DeviceRestorePipeline:
         n, S = len(lengths), int(slot_off[-1])
         if S * ctx.pages_per_block > self.pool.n_pages:
             raise ValueError("batch needs %d pages, pool has %d" % (S * ctx.pages_per_block, self.pool.n_pages))
-        d_toff = torch.from_numpy(tok_off).to(dev, non_blocking=True)
-        d_soff = torch.from_numpy(slot_off).to(dev, non_blocking=True)
-        chains = T.make_chains(d_tokens, int(tok_off[-1]), d_toff, d_soff, S, None, d_first_block)
-        hits = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
-        verd = torch.empty(max(S, 1), dtype=torch.uint8, device=dev)
-        out = DeviceBatch(S, hits[:n], verd[:S], slot_off)
-        if n == 0:
-            return out
-        Sx = max(S, 1)
-        keys = torch.empty((Sx, 32), dtype=torch.uint8, device=dev)
-        handles = torch.empty(Sx, dtype=torch.int64, device=dev)
-        ptrs, lens, bidx = (torch.empty(Sx, dtype=torch.int64, device=dev) for _ in range(3))
-        toks = torch.empty((Sx, bt), dtype=torch.int32, device=dev)
-        ntok = torch.empty(Sx, dtype=torch.int32, device=dev)
-        tab = torch.empty((ctx.n_groups, Sx * ctx.pages_per_block), dtype=torch.int32, device=dev)
-        st = self.store
-        T.tl_chain_lookup_par(ctx, s, n, chains, st.key_index, st.token_index, st.slot_keys, st.capacity, keys,
-                              handles, hits, self.flags)
-        T.tl_chain_stage(ctx, s, n, chains, hits, handles, st.records.ptrs, st.records.lens, st.capacity, ptrs,
-                         lens, bidx, toks, None, tab, self.flags, ntok)
-        if S:
-            ws_b = T.tl_workspace_bytes(ctx, S)
-            ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
-            T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab, ntok), self.pool.tl(), verd, ws,
-                      ws_b)
-            out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, ntok, tab, ws)
+        with _on(s):
+            d_toff = torch.from_numpy(tok_off).to(dev, non_blocking=True)
+            d_soff = torch.from_numpy(slot_off).to(dev, non_blocking=True)
+            chains = T.make_chains(d_tokens, int(tok_off[-1]), d_toff, d_soff, S, None, d_first_block)
+            hits = torch.empty(max(n, 1), dtype=torch.int32, device=dev)
+            verd = torch.empty(max(S, 1), dtype=torch.uint8, device=dev)
+            out = DeviceBatch(S, hits[:n], verd[:S], slot_off)
+            if n == 0:
+                return out
+            Sx = max(S, 1)
+            keys = torch.empty((Sx, 32), dtype=torch.uint8, device=dev)
+            handles = torch.empty(Sx, dtype=torch.int64, device=dev)
+            ptrs, lens, bidx = (torch.empty(Sx, dtype=torch.int64, device=dev) for _ in range(3))
+            toks = torch.empty((Sx, bt), dtype=torch.int32, device=dev)
+            ntok = torch.empty(Sx, dtype=torch.int32, device=dev)
+            tab = torch.empty((ctx.n_groups, Sx * ctx.pages_per_block), dtype=torch.int32, device=dev)
+            st = self.store
+            T.tl_chain_lookup_par(ctx, s, n, chains, st.key_index, st.token_index, st.slot_keys, st.capacity, keys,
+                                  handles, hits, self.flags)
+            T.tl_chain_stage(ctx, s, n, chains, hits, handles, st.records.ptrs, st.records.lens, st.capacity, ptrs,
+                             lens, bidx, toks, None, tab, self.flags, ntok)
+            if S:
+                ws_b = T.tl_workspace_bytes(ctx, S)
+                ws = torch.empty(ws_b, dtype=torch.uint8, device=dev)
+                T.tl_load(ctx, s, S, ptrs, lens, T.make_blocks(keys, bidx, toks, tab, ntok), self.pool.tl(), verd, ws,
+                          ws_b)
+                out._keep = (chains, keys, handles, ptrs, lens, bidx, toks, ntok, tab, ws)
         return out
 
 
@@ -258,23 +276,24 @@ class FileRestore:
         Returns the device verdicts [n] (valid after the stream syncs)."""
         ids = np.asarray(record_ids, dtype=np.uint64)
         n, B, ppb = ids.size, self.batch, self.ctx.pages_per_block
-        verd = torch.empty(max(n, 1), dtype=torch.uint8, device=self.dev)
-        spans = [(lo, min(lo + B, n)) for lo in range(0, n, B)]
-        keep = []  # per-batch arrays the enqueued loads read, alive until the end
-        if spans:
-            self.file.read(ids[spans[0][0]:spans[0][1]], self.bufs[0])
-        for i, (lo, hi) in enumerate(spans):
-            k = i & 1
-            tabs = d_tables[:, lo * ppb:hi * ppb].contiguous()
-            blk = T.make_blocks(d_keys[lo:hi], d_positions[lo:hi], None if d_tokens is None else d_tokens[lo:hi],
-                                tabs)
-            keep.append((tabs, blk))
-            T.tl_load(self.ctx, self.stream, hi - lo, self.ptrs[k], self.lens, blk, self.pool.tl(), verd[lo:hi],
-                      self.ws[k], self.ws_bytes)
-            self.done[k].record(self.stream)
-            if i + 1 < len(spans):
-                nlo, nhi = spans[i + 1]
-                self.done[k ^ 1].synchronize()  # the load that last read the other buffer is finished
-                self.file.read(ids[nlo:nhi], self.bufs[k ^ 1])
-        self.stream.synchronize()
+        with _on(self.stream):
+            verd = torch.empty(max(n, 1), dtype=torch.uint8, device=self.dev)
+            spans = [(lo, min(lo + B, n)) for lo in range(0, n, B)]
+            keep = []  # per-batch arrays the enqueued loads read, alive until the end
+            if spans:
+                self.file.read(ids[spans[0][0]:spans[0][1]], self.bufs[0])
+            for i, (lo, hi) in enumerate(spans):
+                k = i & 1
+                tabs = d_tables[:, lo * ppb:hi * ppb].contiguous()
+                blk = T.make_blocks(d_keys[lo:hi], d_positions[lo:hi], None if d_tokens is None else d_tokens[lo:hi],
+                                    tabs)
+                keep.append((tabs, blk))
+                T.tl_load(self.ctx, self.stream, hi - lo, self.ptrs[k], self.lens, blk, self.pool.tl(), verd[lo:hi],
+                          self.ws[k], self.ws_bytes)
+                self.done[k].record(self.stream)
+                if i + 1 < len(spans):
+                    nlo, nhi = spans[i + 1]
+                    self.done[k ^ 1].synchronize()  # the load that last read the other buffer is finished
+                    self.file.read(ids[nlo:nhi], self.bufs[k ^ 1])
+            self.stream.synchronize()
         return verd[:n]
