@@ -470,15 +470,35 @@ class RecordFile:
     def _ids(ids) -> np.ndarray:
         return np.ascontiguousarray(np.asarray(ids, dtype=np.uint64))
 
+    def _host(self, buf, n: int) -> int:
+        """Address of a contiguous host buffer (numpy array or CPU tensor)
+        that holds n records; a raw integer address is taken as is."""
+        if isinstance(buf, int):
+            return buf
+        if isinstance(buf, np.ndarray):
+            ok, nbytes = buf.flags.c_contiguous, buf.nbytes
+        elif hasattr(buf, "data_ptr"):
+            if buf.device.type != "cpu":
+                raise ValueError("record files read and write host memory, got a %s tensor" % buf.device.type)
+            ok, nbytes = buf.is_contiguous(), buf.numel() * buf.element_size()
+        else:
+            raise TypeError("expected a numpy array, a CPU tensor or an address, got %r" % type(buf))
+        if not ok:
+            raise ValueError("record buffer must be contiguous")
+        if nbytes < n * self.record_bytes:
+            raise ValueError("record buffer holds %d bytes, %d records need %d" % (nbytes, n, n * self.record_bytes))
+        return _addr(buf)
+
     def read(self, ids, dst):
-        """Records `ids` into host memory `dst` (a tensor or array of at least
-        len(ids) * record_bytes bytes)."""
+        """Records `ids` into host memory `dst` (a contiguous tensor or array
+        of at least len(ids) * record_bytes bytes)."""
         a = self._ids(ids)
-        _check(_lib.tl_file_read(self._h, a.ctypes.data, a.size, _addr(dst)), "tl_file_read")
+        _check(_lib.tl_file_read(self._h, a.ctypes.data, a.size, self._host(dst, a.size)), "tl_file_read")
 
     def write(self, ids, src):
+        """Records `ids` from host memory `src` (as for read)."""
         a = self._ids(ids)
-        _check(_lib.tl_file_write(self._h, a.ctypes.data, a.size, _addr(src)), "tl_file_write")
+        _check(_lib.tl_file_write(self._h, a.ctypes.data, a.size, self._host(src, a.size)), "tl_file_write")
 
     def drop_cache(self):
         _check(_lib.tl_file_drop_cache(self._h), "tl_file_drop_cache")

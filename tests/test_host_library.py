@@ -8,6 +8,7 @@ import os
 import re
 
 import numpy as np
+import torch
 import pytest
 
 from oracle import taliesin_ref as ref
@@ -274,6 +275,19 @@ def test_record_file_round_trip_and_errors(tmp_path):
     one = np.zeros((1, rb), np.uint8)
     ro.read([49], one)
     assert np.array_equal(one[0], src[49])
+    # the binding refuses host buffers too small for the records, or not
+    # contiguous, before the library touches them
+    with pytest.raises(ValueError):
+        ro.read([1, 2], one)
+    with pytest.raises(ValueError):
+        ro.read([1], np.zeros((1, rb - 1), np.uint8))
+    with pytest.raises(ValueError):
+        ro.read([1], np.zeros((1, 2 * rb), np.uint8)[:, ::2])
+    with pytest.raises(ValueError):
+        ro.read([1], torch.zeros((1, rb - 16), dtype=torch.uint8))
+    t = torch.zeros((1, rb), dtype=torch.uint8)
+    ro.read([7], t)
+    assert np.array_equal(t.numpy()[0], src[7])
     ro.close()
     for kw in ({"n_threads": 0}, {"n_threads": 257}):
         with pytest.raises(T.TaliesinError) as e:
