@@ -295,14 +295,57 @@ def make_blocks(d_keys, d_block_index, d_tokens, d_tables, d_n_tokens=None) -> t
     return b
 
 
+def _fits(x, nbytes: int, what: str):
+    """A tensor argument must be contiguous device memory of at least nbytes:
+    the kernels index it up to there. Raw addresses (ints) and None are the
+    caller's responsibility, as in the C ABI."""
+    if x is None or isinstance(x, int) or not hasattr(x, "data_ptr"):
+        return
+    if x.device.type != "cuda":
+        raise ValueError("%s must be device memory, got a %s tensor" % (what, x.device.type))
+    if not x.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    have = x.numel() * x.element_size()
+    if have < nbytes:
+        raise ValueError("%s holds %d bytes, %d needed" % (what, have, nbytes))
+
+
+def _check_blocks(ctx: Ctx, n: int, blocks: tl_blocks):
+    keep = getattr(blocks, "_keep", None)
+    if keep is None:
+        return
+    keys, bidx, toks, tabs, ntok = keep
+    _fits(keys, 32 * n, "keys")
+    _fits(bidx, 8 * n, "block index")
+    _fits(toks, n * ctx.block_bytes, "tokens")
+    _fits(tabs, 4 * ctx.n_groups * n * ctx.pages_per_block, "block tables")
+    _fits(ntok, 4 * n, "token counts")
+
+
+def _check_cache(ctx: Ctx, cache: tl_cache):
+    keep = getattr(cache, "_keep", None)
+    if keep is None:
+        return
+    n_layers = ctx.n_slabs // (2 * ctx.pages_per_block)
+    _fits(keep[0], 8 * n_layers, "K layer addresses")
+    _fits(keep[1], 8 * n_layers, "V layer addresses")
+
+
 def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
             d_status=None):
+    _check_blocks(ctx, n_blocks, blocks)
+    _check_cache(ctx, src)
+    _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
+    _fits(d_status, n_blocks, "save status")
     _check(_lib.tl_save(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src), ctypes.byref(blocks),
                         _addr(d_record_ptrs), _addr(d_status)), "tl_save")
 
 
 def tl_save_layers(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
                    layer_begin: int, layer_end: int, shared: bool = False):
+    _check_blocks(ctx, n_blocks, blocks)
+    _check_cache(ctx, src)
+    _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
     _check(_lib.tl_save_layers(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src),
                                ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end,
                                TL_SAVE_SHARED if shared else 0),
@@ -311,12 +354,21 @@ def tl_save_layers(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_bl
 
 def tl_save_seal(ctx: Ctx, stream, n_blocks: int, n_pages: int, blocks: tl_blocks, d_record_ptrs,
                  d_status=None):
+    _check_blocks(ctx, n_blocks, blocks)
+    _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
+    _fits(d_status, n_blocks, "save status")
     _check(_lib.tl_save_seal(ctx.handle, _stream(stream), n_blocks, n_pages, ctypes.byref(blocks),
                              _addr(d_record_ptrs), _addr(d_status)), "tl_save_seal")
 
 
 def tl_load(ctx: Ctx, stream, n_blocks: int, d_record_ptrs, d_record_lens, blocks: tl_blocks,
             dst: tl_cache, d_verdicts, d_workspace, workspace_bytes: int):
+    _check_blocks(ctx, n_blocks, blocks)
+    _check_cache(ctx, dst)
+    _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
+    _fits(d_record_lens, 8 * n_blocks, "record lengths")
+    _fits(d_verdicts, n_blocks, "verdicts")
+    _fits(d_workspace, workspace_bytes, "workspace")
     _check(_lib.tl_load(ctx.handle, _stream(stream), n_blocks, _addr(d_record_ptrs),
                         _addr(d_record_lens), ctypes.byref(blocks), ctypes.byref(dst),
                         _addr(d_verdicts), _addr(d_workspace), workspace_bytes), "tl_load")

@@ -213,6 +213,43 @@ def test_empty_calls_are_noops():
         assert np.array_equal(a, b)
 
 
+def test_binding_refuses_short_device_buffers():
+    """Tensors too small for n blocks are refused by the binding before any
+    kernel is enqueued (the kernels would index past them)."""
+    geom = wl.Geometry(2, 2, 64, 16)
+    n = 6
+    c = Case(geom, n, 8, 8, seed=5)
+    c.make_src()
+    store, st = c.save()
+    assert (st == ref.ACCEPT).all()
+    dst = random_fill(PagedCache(2, 8, c.stride, DEV), 10)
+    before = host_layers(dst)
+    ws_b = T.tl_workspace_bytes(c.ctx, n)
+    ws = torch.empty(ws_b, dtype=torch.uint8, device=DEV)
+    verd = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    tab = i32(c.t_dst)
+    s = torch.cuda.current_stream()
+    load = lambda **kw: T.tl_load(c.ctx, s, n, kw.get("ptrs", store.ptrs), kw.get("lens", store.lens),
+                                  kw.get("blk", c.blocks(tab)), dst.tl(), kw.get("verd", verd), ws, ws_b)
+    bad = [dict(verd=verd[:n - 1]), dict(ptrs=store.ptrs[:n - 1]), dict(lens=store.lens[:2]),
+           dict(blk=c.blocks(tab[:, :n - 1].contiguous())), dict(blk=c.blocks(tab, keys=c.d_keys[:n - 1])),
+           dict(blk=c.blocks(tab, bidx=c.d_bidx[:1])), dict(verd=torch.zeros(2 * n, dtype=torch.uint8, device=DEV)[::2])]
+    for kw in bad:
+        with pytest.raises(ValueError):
+            load(**kw)
+    with pytest.raises(ValueError):
+        T.tl_load(c.ctx, s, n, store.ptrs, store.lens, c.blocks(tab), dst.tl(), verd, ws, ws_b + 256)
+    with pytest.raises(ValueError):
+        T.tl_save(c.ctx, s, n, c.src.tl(), c.blocks(i32(c.t_src)), store.ptrs[:n - 1])
+    torch.cuda.synchronize()
+    after = host_layers(dst)
+    for a, b in zip(before[0] + before[1], after[0] + after[1]):
+        assert np.array_equal(a, b)  # nothing was enqueued
+    load()  # the same call with whole buffers restores
+    torch.cuda.synchronize()
+    assert (verd.cpu().numpy() == ref.ACCEPT).all()
+
+
 def test_mid_workload_parity():
     cfg = wl.MID
     c = Case(cfg.geom, cfg.n_tokens // cfg.geom.page_tokens, cfg.src_pages, cfg.dst_pages, cfg.seed)

@@ -240,6 +240,25 @@ def test_save_load_argument_validation_enqueues_nothing():
         assert L.tl_save_layers(big.handle, None, n, P(big_cache), P(good_blk), 0x70000, 0, 1, 0) == want
 
 
+def test_binding_refuses_host_tensors_for_device_arguments():
+    """Save and load arguments given as tensors must be device memory: the
+    binding refuses CPU tensors before calling the library."""
+    c = _ctx(wl.TINY)
+    n = 8
+    cache = T.make_cache(0x10000, 0x20000, c.slab_bytes, 128)
+    host_keys = T.make_blocks(torch.zeros((n, 32), dtype=torch.uint8), 0x40000, 0x50000, 0x60000)
+    good = T.make_blocks(0x30000, 0x40000, 0x50000, 0x60000)
+    with pytest.raises(ValueError, match="device memory"):
+        T.tl_load(c, None, n, 0x70000, 0x80000, host_keys, cache, 0x90000, 0xA0000, 256)
+    with pytest.raises(ValueError, match="device memory"):
+        T.tl_load(c, None, n, 0x70000, 0x80000, good, cache, torch.zeros(n, dtype=torch.uint8), 0xA0000, 256)
+    with pytest.raises(ValueError, match="device memory"):
+        T.tl_save(c, None, n, cache, good, torch.zeros(n, dtype=torch.int64))
+    with pytest.raises(ValueError, match="device memory"):
+        T.tl_save(c, None, n, T.make_cache(torch.zeros(4, dtype=torch.int64), 0x20000, c.slab_bytes, 128),
+                  good, 0x70000)
+
+
 def test_status_and_verdict_strings():
     assert T.verdict_name(T.ACCEPT) == "ACCEPT"
     assert T.verdict_name(T.SEGMENT) == "SEGMENT"
