@@ -395,8 +395,12 @@ int tl_block_fingerprints(const tl_ctx* ctx, void* stream, size_t n, const uint3
  * first block whose proposal is missing or differs the chain goes on one
  * block after another. A stale or incomplete token index costs time, never
  * correctness. Other key slots of a chain's range hold unspecified bytes.
- * Positions are d_first_block[c] + k, as in tl_chain_stage. One workgroup per
- * chain; fewer than 2^24 chains. */
+ * Positions are d_first_block[c] + k, as in tl_chain_stage. A chain is
+ * walked in tiles of 1,024 blocks: with few, long chains (at least two tiles'
+ * worth of slots, at most 16 (chain, tile) pairs per compute unit, fewer than
+ * 2^29 slots) every tile runs on a workgroup of its own, otherwise one
+ * workgroup walks each chain; d_hits serves as scratch until the call
+ * completes. Fewer than 2^24 chains. */
 int tl_chain_lookup_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chains* chains,
                         const tl_dindex* idx, const tl_dindex* tok_idx, const uint8_t* d_handle_keys,
                         uint64_t n_handles, uint32_t flags, uint8_t* d_keys, uint64_t* d_handles,

@@ -576,6 +576,143 @@ __global__ __launch_bounds__(kParThreads) void k_chain_par(ParArgs a) {
   }
 }
 
+// The same walk with the tiles of a chain spread over workgroups, for a few
+// long chains (one workgroup per chain would walk their tiles one after
+// another). Pass 1 runs one workgroup per (chain, tile): the candidate of the
+// block before the tile comes from the token index like every other
+// candidate, the tile's blocks are hashed, probed and compared as above, and
+// the tile's first flagged block k goes to hits[c] as min(k << 2 | flag)
+// (k_par_init sets every hits[c] to all ones first). A tile that starts
+// after a block already flagged is skipped: only the first flag counts.
+// Pass 2 (k_chain_par_finish, one workgroup per chain) turns hits[c] into
+// the hit count: for a disagreement at block m it continues the chain
+// sequentially from m + 1, whose predecessor's key pass 1 stored and is
+// true; it sets the handles after the last hit to misses. Results equal
+// k_chain_par's.
+__global__ __launch_bounds__(256) void k_par_init(uint32_t* hits, uint32_t n) {
+  for (uint32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) hits[i] = 0xffffffffu;
+}
+
+template <uint32_t kParThreads>
+__global__ __launch_bounds__(kParThreads) void k_chain_par_tiles(ParArgs a, uint32_t n_tiles) {
+  __shared__ uint32_t cand[kParThreads + 1][8];  // [0]: candidate of the block before the tile
+  __shared__ uint32_t has[kParThreads + 1];
+  __shared__ uint32_t first;
+  __shared__ uint32_t skip;
+  const uint32_t tid = threadIdx.x;
+  const uint64_t maxp = a.x.mem[1], tmaxp = a.t.mem[1];
+  const uint64_t pairs = (uint64_t)a.in.n_chains * n_tiles;
+  for (uint64_t q = blockIdx.x; q < pairs; q += gridDim.x) {
+    const uint32_t c = (uint32_t)(q % a.in.n_chains);
+    const uint64_t t0 = (q / a.in.n_chains) * kParThreads;
+    const Range r = chain_range(a.in, c);
+    if (t0 >= r.n) continue;  // uniform: every thread computed the same range
+    const uint64_t pos0 = a.in.first_block ? a.in.first_block[c] : 0;
+    if (tid == 0) {
+      first = 0xffffffffu;
+      const uint32_t seen = __hip_atomic_load(&a.hits[c], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      skip = seen != 0xffffffffu && (uint64_t)(seen >> 2) < t0;
+      uint32_t hc0 = 0;
+      if (!skip) {
+        if (t0 == 0) {
+          uint32_t p[8];
+          parent_words(p, a.in, c);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) cand[0][i] = p[i];
+          hc0 = 1;
+        } else {
+          const uint64_t k = t0 - 1;
+          uint32_t f[8];
+          fingerprint(f, a.in, pos0 + k, a.in.tokens + r.t0 + k * a.in.bt, block_len(r, k, a.in.bt));
+          uint64_t fw[4];
+          key_words(fw, f);
+          const uint64_t h = probe_from(a.t, fw, tmaxp, 0);
+          if (h < a.n_handles) {
+            const uint32_t* hk = (const uint32_t*)(a.hkeys + 32 * h);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) cand[0][i] = __builtin_bswap32(hk[i]);
+            hc0 = 1;
+          }
+        }
+      }
+      has[0] = hc0;
+    }
+    __syncthreads();
+    if (skip) {
+      __syncthreads();  // nobody reads this tile's LDS any more
+      continue;
+    }
+    const uint64_t k = t0 + tid;
+    const bool live = k < r.n;
+    const uint32_t* tok = a.in.tokens + r.t0 + k * a.in.bt;
+    const uint32_t len = block_len(r, k, a.in.bt);
+    uint32_t hc = 0;
+    if (live) {
+      uint32_t f[8];
+      fingerprint(f, a.in, pos0 + k, tok, len);
+      uint64_t fw[4];
+      key_words(fw, f);
+      const uint64_t h = probe_from(a.t, fw, tmaxp, 0);
+      if (h < a.n_handles) {
+        const uint32_t* hk = (const uint32_t*)(a.hkeys + 32 * h);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) cand[tid + 1][i] = __builtin_bswap32(hk[i]);
+        hc = 1;
+      }
+    }
+    has[tid + 1] = hc;
+    __syncthreads();
+    if (live && has[tid]) {
+      uint32_t prev[8], ck[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) prev[i] = cand[tid][i];
+      chain_key(ck, a.in, prev, tok, len);
+      store_key(a.keys, r.s0 + k, ck);
+      uint64_t kw[4];
+      key_words(kw, ck);
+      const uint64_t hv = probe_from(a.x, kw, maxp, 0);
+      a.handles[r.s0 + k] = hv;
+      bool same = hc != 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) same = same && cand[tid + 1][i] == ck[i];
+      const uint32_t flag = hv == kMiss ? 1u : (same ? 0u : 2u);
+      if (flag) atomicMin(&first, tid << 2 | flag);
+    }
+    __syncthreads();
+    if (tid == 0 && first != 0xffffffffu)
+      atomicMin(&a.hits[c], (uint32_t)((t0 + (first >> 2)) << 2) | (first & 3));
+    __syncthreads();  // LDS is reused by the next tile
+  }
+}
+
+__global__ __launch_bounds__(256) void k_chain_par_finish(ParArgs a) {
+  __shared__ uint64_t seq_hits;
+  const uint32_t tid = threadIdx.x;
+  for (uint32_t c = blockIdx.x; c < a.in.n_chains; c += gridDim.x) {
+    const Range r = chain_range(a.in, c);
+    const uint32_t f = a.hits[c];  // final: pass 1 has completed
+    const uint64_t stop = f == 0xffffffffu ? r.n : (uint64_t)(f >> 2);
+    const uint32_t kind = f == 0xffffffffu ? 0u : (f & 3);
+    uint64_t n_hit = kind == 1 ? stop : r.n;
+    if (kind == 2) {
+      // block stop is a hit with a true key, but its candidate differs
+      if (tid == 0) {
+        const uint32_t* sk = (const uint32_t*)(a.keys + 32 * (r.s0 + stop));
+        uint32_t cur[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) cur[i] = __builtin_bswap32(sk[i]);
+        seq_hits = stop + 1 + seq_walk(a.in, a.x, false, r, stop + 1, cur, a.keys, a.handles);
+      }
+      __syncthreads();
+      n_hit = seq_hits;
+    }
+    for (uint64_t j = n_hit + tid; j < r.n; j += 256) a.handles[r.s0 + j] = kMiss;
+    __syncthreads();  // every thread has read hits[c]
+    if (tid == 0) a.hits[c] = (uint32_t)n_hit;
+    __syncthreads();
+  }
+}
+
 // ---- staging of tl_load's inputs --------------------------------------------
 struct StageArgs {
   const uint32_t* tokens;
@@ -801,11 +938,26 @@ int launch_chain_par(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_
   a.handles = d_handles;
   a.hits = d_hits;
   (void)hipGetLastError();
+  // Tiles of 1024 blocks per chain, at most: a chain's blocks never exceed the
+  // call's slots. With at least two of them per chain and few (chain, tile)
+  // pairs, the tiles of each chain go to workgroups of their own.
+  const uint64_t tiles = (ch->n_slots + 1023) / 1024;
+  const int cus = sm_count();
+  const bool spread = tiles >= 2 && (uint64_t)n_chains * tiles <= (uint64_t)cus * 16 &&
+                      ch->n_slots < (1ull << 29);
   {
     TimedLaunch t(TL_KERNEL_CHAIN, stream);
-    const dim3 grid(grid_for(n_chains, 1, 1u << 16));
-    if (n_chains <= (size_t)sm_count() * 4) hipLaunchKernelGGL(k_chain_par<1024>, grid, dim3(1024), 0, s, a);
-    else hipLaunchKernelGGL(k_chain_par<256>, grid, dim3(256), 0, s, a);
+    if (spread) {
+      hipLaunchKernelGGL(k_par_init, dim3(grid_for(n_chains, 256, 4096)), dim3(256), 0, s, d_hits,
+                         (uint32_t)n_chains);
+      hipLaunchKernelGGL(k_chain_par_tiles<1024>, dim3((uint32_t)(n_chains * tiles)), dim3(1024), 0, s, a,
+                         (uint32_t)tiles);
+      hipLaunchKernelGGL(k_chain_par_finish, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(256), 0, s, a);
+    } else {
+      const dim3 grid(grid_for(n_chains, 1, 1u << 16));
+      if (n_chains <= (size_t)cus * 4) hipLaunchKernelGGL(k_chain_par<1024>, grid, dim3(1024), 0, s, a);
+      else hipLaunchKernelGGL(k_chain_par<256>, grid, dim3(256), 0, s, a);
+    }
   }
   return launched();
 }

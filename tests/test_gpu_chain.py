@@ -548,6 +548,57 @@ def test_parallel_walk_equals_the_oracle_walk(case):
     assert np.array_equal(hits, hits2)
     log(case, "hits", total, "of", ch.n_slots, "slots")
     assert total > 3000
+    # the same chains followed by thousands of empty ones: one workgroup per
+    # chain instead of one per (chain, tile), the same results
+    padded = pad_chains(ctx, ch, bt, 4100)
+    kp, hp, hitsp = par_lookup(ctx, padded, two)
+    check_walk(padded, ns, bt, two.index, kp, hp, hitsp)
+    assert np.array_equal(hitsp[:ch.n], hits) and np.array_equal(hp[:ch.n_slots], handles[:ch.n_slots])
+
+
+def pad_chains(ctx, ch, bt, extra):
+    """ch followed by `extra` empty chains (no tokens, no slots)."""
+    p = Chains(ctx, ch.lengths + [0] * extra, 0, bt)
+    p.tokens[:] = ch.tokens
+    p.d_tok.copy_(torch.from_numpy(p.tokens.view(np.int32)))
+    assert p.n_slots == ch.n_slots
+    return p
+
+
+@pytest.mark.parametrize("case", ["complete", "key_hole_at_tile_start", "token_hole_at_tile_end",
+                                  "token_hole_at_tile_start", "decoy"])
+def test_parallel_walk_one_long_chain(case):
+    """One chain of 6,100 blocks (the paper corpus is 6,062): its six tiles go
+    to workgroups of their own. Holes and disagreements sit at tile
+    boundaries, where a tile's first block depends on the candidate of the
+    previous tile's last block."""
+    ctx, ns, bt = ctx_bt(16)
+    n_doc = 6100
+    docs, _ = stored_docs(ns, bt, 1, n_doc, 130)
+    kw, want = {}, n_doc
+    if case == "key_hole_at_tile_start":
+        kw["skip"], want = {1024}, 1024
+    if case == "token_hole_at_tile_end":
+        kw["token_skip"] = {1023}
+    if case == "token_hole_at_tile_start":
+        kw["token_skip"] = {1024}
+    if case == "decoy":
+        dec = docs[0].copy()
+        dec[2048 * bt:2049 * bt] = wl.tokens(bt, 131)  # same tokens as the document after block 2048
+        kw["decoys"] = [dec]
+    two = TwoIndexes(ctx, ns, bt, docs, cap=32768, **kw)
+    req = np.concatenate([docs[0], wl.tokens(7, 132)])
+    ch = Chains(ctx, [req.size], 0, bt)
+    ch.tokens[:] = req
+    ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    log("one long chain:", case)
+    keys, handles, hits = par_lookup(ctx, ch, two)
+    check_walk(ch, ns, bt, two.index, keys, handles, hits)
+    assert list(hits) == [want]
+    padded = pad_chains(ctx, ch, bt, 4100)
+    kp, hp, hitsp = par_lookup(ctx, padded, two)
+    check_walk(padded, ns, bt, two.index, kp, hp, hitsp)
+    assert hitsp[0] == want and np.array_equal(hp[:ch.n_slots], handles[:ch.n_slots])
 
 
 def test_parallel_walk_with_parents_and_positions():
