@@ -307,6 +307,54 @@ def _oracle_slice(task):
         shm.close()
 
 
+def device_keys_leg(T, ctx, tokens, keys, n, P, dev, reps=20):
+    """a1 + a2 on the device for the corpus: the verified parallel walk over
+    its 6,062 blocks (one chain) against a key index and a token index of
+    the stored blocks, as an engine with the token ids already in HBM would
+    run it before tl_load."""
+    import numpy as np
+    import torch
+
+    stream = torch.cuda.current_stream()
+    cap = 1 << max(2, (2 * n - 1).bit_length())
+    d_keys = torch.from_numpy(keys).to(dev)
+    handles = torch.arange(n, dtype=torch.int64, device=dev)
+    d_tok = torch.from_numpy(tokens[:n * P].view(np.int32).reshape(n, P).copy()).to(dev)
+    fps = torch.empty((n, 32), dtype=torch.uint8, device=dev)
+    T.tl_block_fingerprints(ctx, stream, n, d_tok, handles, fps)
+    idx = []
+    for k in (d_keys, fps):
+        mem = torch.empty(T.tl_dindex_bytes(cap), dtype=torch.uint8, device=dev)
+        x = T.DeviceIndex(mem, cap, stream)
+        st = torch.empty(n, dtype=torch.uint8, device=dev)
+        wsb = T.tl_dindex_workspace_bytes(n)
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+        x.put(stream, n, k, handles, st, ws, wsb)
+        torch.cuda.synchronize()
+        assert (st == T.TL_INDEX_STORED).all().item()
+        idx.append(x)
+    d_all = torch.from_numpy(tokens.view(np.int32).copy()).to(dev)
+    toff = torch.tensor([0, tokens.size], dtype=torch.int64, device=dev)
+    soff = torch.tensor([0, n], dtype=torch.int64, device=dev)
+    ch = T.make_chains(d_all, tokens.size, toff, soff, n)
+    out_k = torch.empty((n, 32), dtype=torch.uint8, device=dev)
+    out_h = torch.empty(n, dtype=torch.int64, device=dev)
+    hits = torch.empty(1, dtype=torch.int32, device=dev)
+    call = lambda: T.tl_chain_lookup_par(ctx, stream, 1, ch, idx[0], idx[1], d_keys, n, out_k, out_h, hits)
+    call()
+    torch.cuda.synchronize()
+    assert int(hits.item()) == n and torch.equal(out_k, d_keys) and torch.equal(out_h, handles)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        call()
+    e1.record(stream)
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    log("device keys + lookup of the corpus (one chain of %d blocks): %.3f ms" % (n, ms))
+    return {"ms": ms, "blocks": n, "hits": n, "how": "tl_chain_lookup_par, one chain, key and token indexes"}
+
+
 def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
     """Save and restore of the other workloads (tiny, mid, hybrid) in the same
     library calls. Load bytes count what the load must move: every block's
@@ -651,6 +699,7 @@ def main():
         t_look.append((t2 - t1) * 1e3)
     host = {"keys_ms": sorted(t_keys)[2], "lookup_ms": sorted(t_look)[2],
             "sha256_extensions": T.sha256_selftest(b"", 1) is not None}
+    device_keys = device_keys_leg(T, ctx, tokens, keys0, n, P, dev)
 
     # ---- practical ceilings with torch's own kernels over the same byte count:
     # a device-to-device copy, a read-only reduction and a write-only fill
@@ -845,6 +894,7 @@ def main():
         "save": save,
         "layerwise_save": layerwise,
         "host_ms": host,
+        "device_keys": device_keys,
         "host_tier": host_tier,
         "disk_tier": disk,
         "paper_blocks": pb,
