@@ -748,15 +748,18 @@ __device__ __forceinline__ bool stage_hit(const StageArgs& a, uint64_t slot, uin
   return *h < a.n_handles;
 }
 
-// One wavefront per chain; lanes stride over the chain's slots.
-__global__ __launch_bounds__(64) void k_chain_stage(StageArgs a) {
-  const uint32_t lane = threadIdx.x;
+// One workgroup of kStageThreads per chain; its threads stride over the
+// chain's slots, token ids and table entries.
+constexpr uint32_t kStageThreads = 256;
+
+__global__ __launch_bounds__(kStageThreads) void k_chain_stage(StageArgs a) {
+  const uint32_t tid = threadIdx.x;
   for (uint32_t c = blockIdx.x; c < a.n_chains; c += gridDim.x) {
     const Range r = chain_range(a.tok_off, a.slot_off, a.n_tokens, a.n_slots, a.bt, a.tail, c);
     const uint64_t hits_raw = a.hits[c];
     const uint64_t hits = hits_raw < r.n ? hits_raw : r.n;
     const uint64_t first = a.first_block ? a.first_block[c] : 0;
-    for (uint64_t k = lane; k < r.slots; k += 64) {
+    for (uint64_t k = tid; k < r.slots; k += kStageThreads) {
       const uint64_t q = r.s0 + k;
       uint64_t h = 0;
       const bool hit = stage_hit(a, q, k, hits, &h);
@@ -769,13 +772,13 @@ __global__ __launch_bounds__(64) void k_chain_stage(StageArgs a) {
       const uint64_t n_tok = r.slots * a.bt, have = r.full * a.bt + r.tail_tok;
       uint32_t* dst = a.tokens_out + r.s0 * a.bt;
       const uint32_t* src = a.tokens + r.t0;
-      for (uint64_t e = lane; e < n_tok; e += 64) dst[e] = e < have ? src[e] : 0;
+      for (uint64_t e = tid; e < n_tok; e += kStageThreads) dst[e] = e < have ? src[e] : 0;
     }
     if (a.tables_out) {
       const uint64_t per = r.slots * a.ppb, row = a.n_slots * a.ppb;
       // a restored partial block restores only the pages holding its tokens
       const uint64_t tail_pages = (r.tail_tok + a.page_tokens - 1) / a.page_tokens;
-      for (uint64_t e = lane; e < per; e += 64) {
+      for (uint64_t e = tid; e < per; e += kStageThreads) {
         const uint64_t k = e / a.ppb, j = e - k * a.ppb, at = r.s0 * a.ppb + e;
         uint64_t h = 0;
         const bool hit = stage_hit(a, r.s0 + k, k, hits, &h) && !(r.tail_tok && k == r.full && j >= tail_pages);
@@ -1014,7 +1017,7 @@ int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
   (void)hipGetLastError();
   {
     TimedLaunch t(TL_KERNEL_STAGE, stream);
-    hipLaunchKernelGGL(k_chain_stage, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(64), 0, s, a);
+    hipLaunchKernelGGL(k_chain_stage, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(kStageThreads), 0, s, a);
   }
   return launched();
 }
