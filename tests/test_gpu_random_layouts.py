@@ -1,4 +1,4 @@
-"""Save and verified restore on 24 layouts drawn from fixed seeds: element
+"""Save and verified restore on 200 layouts drawn from fixed seeds: element
 types, heads, head dims and page sizes whose slabs hold 1 to 128 rows (whole
 and ragged chunks), 1-9 layers, 1-3 pages per block, up to three layer groups
 with a table of their own each, padded page strides, destination entries
@@ -38,7 +38,7 @@ def draw(seed: int):
     return wl.Geometry(L, H, D, P, dtype, windows, groups, ppb), n, extra, r
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(200))
 def test_random_layout_round_trip(seed):
     geom, n, extra, r = draw(seed)
     E = n * geom.pages_per_block
