@@ -641,6 +641,47 @@ def test_parallel_walk_many_chains():
     assert max(hits) > 600 and total > 100000
 
 
+@pytest.mark.parametrize("seed", range(40))
+def test_parallel_walk_random(seed):
+    """Seeded random cases: block sizes of 1, 5, 13 and 16 tokens, up to four
+    stored documents of 20-2,600 blocks, key-index holes, token-index holes,
+    decoys (a stored copy of a document with one block changed) and up to
+    120 requests. Both walk paths (tiles on workgroups of their own and one
+    workgroup per chain, forced by empty chains) equal the oracle walk."""
+    r = np.random.default_rng(9000 + seed)
+    ctx, ns, bt = ctx_bt(int(r.choice([16, 5, 13, 1])))
+    n_docs, per = int(r.integers(1, 5)), int(r.integers(20, 2600))
+    docs, _ = stored_docs(ns, bt, n_docs, per, 100 + seed)
+    total = n_docs * per
+    kw = {}
+    if r.random() < 0.5:
+        kw["skip"] = set(int(x) for x in r.choice(total, size=int(r.integers(1, 6)), replace=False))
+    if r.random() < 0.5:
+        kw["token_skip"] = set(int(x) for x in r.choice(total, size=int(r.integers(1, max(2, total // 20))),
+                                                         replace=False))
+    if r.random() < 0.5:
+        decs = []
+        for _ in range(int(r.integers(1, 3))):
+            d = docs[int(r.integers(n_docs))].copy()
+            k = int(r.integers(0, per))
+            d[k * bt:(k + 1) * bt] = wl.tokens(bt, 5000 + seed + k)
+            decs.append(d)
+        kw["decoys"] = decs
+    n_keys = total * (1 + len(kw.get("decoys", [])))
+    two = TwoIndexes(ctx, ns, bt, docs, cap=1 << max(4, (2 * n_keys).bit_length()), **kw)
+    reqs = requests_for(docs, bt, int(r.integers(1, 120)), 200 + seed)
+    ch = Chains(ctx, [x.size for x in reqs], 0, bt)
+    if ch.tokens.size:
+        ch.tokens[:] = np.concatenate(reqs)
+        ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+    log("random walk seed", seed, "block tokens", bt, "chains", ch.n, "slots", ch.n_slots)
+    keys, handles, hits = par_lookup(ctx, ch, two)
+    check_walk(ch, ns, bt, two.index, keys, handles, hits)
+    padded = pad_chains(ctx, ch, bt, 4100)
+    kp, hp, hitsp = par_lookup(ctx, padded, two)
+    check_walk(padded, ns, bt, two.index, kp, hp, hitsp)
+
+
 def _device_path_case(seed):
     geom = wl.Geometry(2, 4, 64, 16)
     c = Case(geom, 24, 24, 24, seed=seed)
