@@ -91,3 +91,72 @@ def test_random_layout_round_trip(seed):
     # (a slab whose page is left out for this block)
     log("verdicts", [ref.VERDICT_NAMES[v] for v in vo])
     assert sum(v == ref.ACCEPT for v in vo) >= n - 2
+
+
+@pytest.mark.parametrize("seed", range(120))
+def test_random_layout_random_damage(seed):
+    """Seeded random layouts with every block drawn one of twelve outcomes:
+    intact, a flipped bit anywhere, a metadata bit flipped under a recomputed
+    root, truncated, overlong, missing, misaligned, a wrong expected key,
+    position or token, another block's record, or a page id out of range.
+    Verdicts and both caches whole equal the oracle's."""
+    from tests.test_gpu_parity import check_restore, upload_records
+    geom, n, extra, r = draw(500 + seed)
+    ppb, G = geom.pages_per_block, geom.n_groups
+    E = n * ppb
+    dst_pages = E + int(r.integers(0, 6))
+    c = Case(geom, n, E + int(r.integers(0, 6)), dst_pages, seed=500 + seed, stride_extra=extra)
+    c.t_src = np.stack([wl.page_table(E, c.src_pages, seed, 70 + g) for g in range(G)])
+    c.t_dst = np.stack([wl.page_table(E, dst_pages, seed, 80 + g) for g in range(G)])
+    c.make_src()
+    store, st = c.save()
+    recs_o, st_o = c.oracle_save()
+    assert [int(x) for x in st] == st_o == [ref.ACCEPT] * n
+    lay, rb, po = c.lay, c.lay.record_bytes, c.lay.payload_offset
+    recs = [bytearray(x) for x in recs_o]
+    lens = np.full(n, rb, np.uint64)
+    keys, bidx, toks, tables = c.keys.copy(), c.bidx.copy(), c.tokens.copy(), c.t_dst.copy()
+    missing, misaligned, kinds = set(), set(), []
+    for b in range(n):
+        kind = int(r.integers(0, 12))
+        kinds.append(kind)
+        if kind == 1:
+            bit = int(r.integers(0, rb * 8))
+            recs[b][bit >> 3] ^= 1 << (bit & 7)
+        elif kind == 2:
+            bit = int(r.integers(0, po * 8))
+            m = bytearray(recs[b][:po])
+            m[bit >> 3] ^= 1 << (bit & 7)
+            m[144:152] = ref.root_digest(bytes(m)).to_bytes(8, "little")
+            recs[b][:po] = m
+        elif kind == 3:
+            lens[b] = int(r.integers(0, rb))
+        elif kind == 4:
+            lens[b] = rb + int(r.integers(1, 65))
+        elif kind == 5:
+            missing.add(b)
+        elif kind == 6:
+            misaligned.add(b)
+        elif kind == 7:
+            keys[b, int(r.integers(0, 32))] ^= 1 << int(r.integers(0, 8))
+        elif kind == 8:
+            bidx[b] = bidx[b] + np.uint64(int(r.integers(1, 1000)))
+        elif kind == 9:
+            toks[b, int(r.integers(0, toks.shape[1]))] ^= 1
+        elif kind == 10 and n > 1:
+            recs[b] = bytearray(recs_o[(b + 1 + int(r.integers(0, n - 1))) % n])
+        elif kind == 11:
+            tables[int(r.integers(0, G)), b * ppb + int(r.integers(0, ppb))] = dst_pages
+    store2 = upload_records([bytes(x) for x in recs], rb)
+    ptrs = store2.ptrs.clone()
+    for b in missing:
+        ptrs[b] = 0
+    for b in misaligned:
+        ptrs[b] += 8
+    c.tokens, c.d_tokens = toks, i32(toks.view(np.int32))
+    dst = random_fill(PagedCache(geom.n_layers, dst_pages, c.stride, DEV), 90 + seed)
+    hk0, hv0 = host_layers(dst)
+    log("random damage, seed", seed, geom, "blocks", n, "kinds", kinds)
+    host_recs = [None if b in missing else bytes(recs[b]) for b in range(n)]
+    check_restore(c, host_recs, ptrs, i64(lens), tables, dst, hk0, hv0, keys=keys, bidx=bidx,
+                  misaligned=misaligned, lens_host=lens)
