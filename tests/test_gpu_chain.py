@@ -197,6 +197,39 @@ def test_device_index_full_and_tag_clash():
     assert got == ([1, T.MISS] if st[0] == T.TL_INDEX_STORED else [T.MISS, 2])
 
 
+@pytest.mark.parametrize("seed", range(30))
+def test_device_index_random_batches(seed):
+    """Seeded sequences of put batches into a device index of 64-4,096 slots:
+    repeated keys across batches (overwrites), duplicates inside a batch, and
+    more keys than slots. Every put's status says whether the key is stored;
+    the stored ones must map to the handle of their last occurrence, and
+    after every batch lookups of every key used (and of absent ones) and the
+    occupied count equal a dictionary built from those statuses."""
+    r = np.random.default_rng(300 + seed)
+    cap = 1 << int(r.integers(6, 13))
+    idx = new_index(cap)
+    pool = rand_keys(int(cap * r.uniform(0.5, 1.6)), 400 + seed)
+    absent = rand_keys(50, 800 + seed)
+    model = {}
+    for step in range(int(r.integers(3, 9))):
+        m = int(r.integers(1, max(2, cap // 2)))
+        batch = [pool[int(i)] for i in r.integers(0, len(pool), m)]
+        handles = [int(h) for h in r.integers(0, 1 << 40, m)]
+        st = dput(idx, batch, handles)
+        assert set(st.tolist()) <= {T.TL_INDEX_STORED, T.TL_INDEX_FULL}
+        last = {}
+        for k, h, s in zip(batch, handles, st):
+            if s == T.TL_INDEX_STORED:
+                last[k] = h
+            else:
+                assert k not in model  # a stored key is always found again
+        model.update(last)
+        used = sorted(set(batch) | set(model))
+        assert dget(idx, used + absent) == [model.get(k, T.MISS) for k in used] + [T.MISS] * len(absent)
+        n_used, maxp = dstats(idx)
+        assert n_used == len(model) <= cap and 0 <= maxp < 1024
+
+
 def stored_docs(ns, bt, n_docs, blocks_per_doc, seed):
     docs = [wl.tokens(blocks_per_doc * bt, seed + d) for d in range(n_docs)]
     keys = [ref.block_keys(ns, d.tobytes(), 4 * bt) for d in docs]
