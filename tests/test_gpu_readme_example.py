@@ -1,0 +1,64 @@
+"""The README's usage example, run as written (on a small model shape): keys,
+save after prefill, index, lookup for a later request, verified restore,
+verdicts. Results are checked against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as wl
+from oracle import taliesin_ref as ref
+
+pytestmark = pytest.mark.gpu
+
+
+def test_readme_usage_example():
+    from paper_2609_39358_amd import taliesin as T
+    from paper_2609_39358_amd.device import PagedCache, RecordStore
+
+    L, H, D, P = 4, 4, 64, 16  # layers, KV heads, head dim, tokens per page
+    prompt = wl.tokens(40 * P + 5, 1)  # token ids of a first request (u32)
+    kv = PagedCache(L, 128, P * H * D * 2)  # the engine's paged K/V cache (bf16 bytes)
+    for t in kv.k + kv.v:  # stands in for the prefill's KV
+        t.copy_(torch.randint(0, 256, t.shape, dtype=torch.uint8, device="cuda"))
+    pages = np.arange(40, dtype=np.int32)  # where prefill put block b: page pages[b]
+    request = np.concatenate([prompt[:25 * P], wl.tokens(300, 2)])  # shares the first 25 blocks
+
+    # --- README example -----------------------------------------------------
+    ctx = T.tl_ctx_create(b"tenant-a", b"model-fingerprint", L, H, D, "bf16", P)
+    cuda = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a).view(dt)).cuda()
+
+    # after prefill: save every full block of the prompt and index it
+    keys = T.tl_block_keys(ctx, prompt)  # [n, 32] chained keys, one per full block
+    n = len(keys)
+    blocks = T.make_blocks(cuda(keys, np.uint8), torch.arange(n, device="cuda"),
+                           cuda(prompt[:n * P].reshape(n, P), np.int32), cuda(pages[None, :n], np.int32))
+    store = RecordStore(n, ctx.record_bytes)
+    T.tl_save(ctx, torch.cuda.current_stream(), n, kv.tl(), blocks, store.ptrs)
+    index = T.tl_index_create(1 << 16)
+    index.put_many(keys, range(n))  # key -> record slot
+
+    # a later request: restore its stored leading blocks into pages of its own
+    rkeys = T.tl_block_keys(ctx, request)
+    slots = index.get_batch(rkeys)  # UINT64_MAX where absent
+    miss = slots == np.iinfo(np.uint64).max
+    hit = int(miss.argmax()) if miss.any() else len(slots)  # reuse stops at the first miss
+    new_pages = np.arange(64, 64 + hit, dtype=np.int32)  # pages the engine gives the request
+    ptrs = store.ptrs[torch.from_numpy(slots[:hit].astype(np.int64)).cuda()]
+    lens = store.lens[:hit]
+    rblocks = T.make_blocks(cuda(rkeys[:hit], np.uint8), torch.arange(hit, device="cuda"),
+                            cuda(request[:hit * P].reshape(hit, P), np.int32), cuda(new_pages[None, :], np.int32))
+    ws = torch.empty(T.tl_workspace_bytes(ctx, hit), dtype=torch.uint8, device="cuda")
+    verdicts = torch.empty(hit, dtype=torch.uint8, device="cuda")
+    T.tl_load(ctx, torch.cuda.current_stream(), hit, ptrs, lens, rblocks, kv.tl(), verdicts, ws, ws.numel())
+    torch.cuda.synchronize()
+    recompute = np.nonzero(verdicts.cpu().numpy() != T.ACCEPT)[0]  # blocks that go back to prefill
+    # --- end of the README example ------------------------------------------
+
+    lay = ref.Layout(L, H, D, 1, P)
+    ns = ref.namespace_digest(b"tenant-a", b"model-fingerprint", lay)
+    assert [k.tobytes() for k in rkeys] == ref.block_keys(ns, request.tobytes(), lay.block_bytes)
+    assert hit == 25 and recompute.size == 0
+    for l in range(L):
+        for t in (kv.k[l], kv.v[l]):
+            assert torch.equal(t[torch.from_numpy(new_pages.astype(np.int64)).cuda()],
+                               t[torch.from_numpy(pages[:hit].astype(np.int64)).cuda()])
