@@ -6,7 +6,7 @@
  * Sabotage testing (paper, Sec. 3): each defence is attacked with the defence
  * on (the attack must fail), switched off (the attack must succeed) and
  * restored (it must fail again). A defence counts only if all three hold.
- * This build lets a test switch individual load checks off.
+ * The sabotage library (built with TL_SABOTAGE) lets a test switch individual load checks off.
  */
 #ifndef TALIESIN_DEBUG_H
 #define TALIESIN_DEBUG_H
