@@ -307,11 +307,13 @@ def _oracle_slice(task):
         shm.close()
 
 
-def device_keys_leg(T, ctx, tokens, keys, n, P, dev, reps=20):
+def device_keys_leg(T, ctx, tokens, keys, n, P, dev, store, dst, d_tdst, step_bytes, reps=20):
     """a1 + a2 on the device for the corpus: the verified parallel walk over
     its 6,062 blocks (one chain) against a key index and a token index of
     the stored blocks, as an engine with the token ids already in HBM would
-    run it before tl_load."""
+    run it before tl_load. Then the whole restore step on the device: the
+    walk, staging of tl_load's inputs (tl_chain_stage) and tl_load into the
+    same destination cache, with no host step."""
     import numpy as np
     import torch
 
@@ -352,7 +354,39 @@ def device_keys_leg(T, ctx, tokens, keys, n, P, dev, reps=20):
     e1.synchronize()
     ms = e0.elapsed_time(e1) / reps
     log("device keys + lookup of the corpus (one chain of %d blocks): %.3f ms" % (n, ms))
-    return {"ms": ms, "blocks": n, "hits": n, "how": "tl_chain_lookup_par, one chain, key and token indexes"}
+    out = {"ms": ms, "blocks": n, "hits": n, "how": "tl_chain_lookup_par, one chain, key and token indexes"}
+
+    ptrs_o, lens_o, bidx_o = (torch.empty(n, dtype=torch.int64, device=dev) for _ in range(3))
+    toks_o = torch.empty((n, P), dtype=torch.int32, device=dev)
+    tab_o = torch.empty((1, n), dtype=torch.int32, device=dev)
+    wsb = T.tl_workspace_bytes(ctx, n)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    verd = torch.empty(n, dtype=torch.uint8, device=dev)
+    blk = T.make_blocks(out_k, bidx_o, toks_o, tab_o)
+    cache = dst.tl()
+
+    def step():
+        call()
+        T.tl_chain_stage(ctx, stream, 1, ch, hits, out_h, store.ptrs, store.lens, n, ptrs_o, lens_o, bidx_o,
+                         toks_o, d_tdst, tab_o)
+        T.tl_load(ctx, stream, n, ptrs_o, lens_o, blk, cache, verd, ws, wsb)
+
+    step()
+    torch.cuda.synchronize()
+    assert (verd == T.ACCEPT).all().item() and torch.equal(tab_o, d_tdst)
+    steps = 10
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    e1.synchronize()
+    sms = e0.elapsed_time(e1) / steps
+    out["device_step"] = {"ms": sms, "GBps": step_bytes / (sms * 1e-3) / 1e9,
+                          "hbm_frac": step_bytes / (sms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                          "how": "tl_chain_lookup_par + tl_chain_stage + tl_load per step, token ids in HBM"}
+    log("device restore step of the corpus (walk + staging + tl_load): %.3f ms, %.0f GB/s"
+        % (sms, out["device_step"]["GBps"]))
+    return out
 
 
 def other_configs_leg(T, PagedCache, RecordStore, wl, dev, reps=10):
@@ -699,7 +733,7 @@ def main():
         t_look.append((t2 - t1) * 1e3)
     host = {"keys_ms": sorted(t_keys)[2], "lookup_ms": sorted(t_look)[2],
             "sha256_extensions": T.sha256_selftest(b"", 1) is not None}
-    device_keys = device_keys_leg(T, ctx, tokens, keys0, n, P, dev)
+    device_keys = device_keys_leg(T, ctx, tokens, keys0, n, P, dev, store, dst, d_tdst, step_bytes)
 
     # ---- practical ceilings with torch's own kernels over the same byte count:
     # a device-to-device copy, a read-only reduction and a write-only fill
