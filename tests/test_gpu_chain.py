@@ -974,6 +974,41 @@ def test_walks_with_tails_equal_the_oracle_walk():
     assert [int(x) for x in hits_np[0:12:3]] == [41, 301, 70, 2]
 
 
+def test_long_chains_with_tails_on_both_walk_paths():
+    """Chains of 2,500 full blocks and a partial last one: three tiles each,
+    the tail in the last tile. The walk with its tiles on workgroups of their
+    own and the one-workgroup walk (forced by empty chains) equal the oracle
+    walk, tails included."""
+    ctx, ns, bt = ctx_bt(16)
+    docs = [wl.tokens(2500 * 16 + 9, 140), wl.tokens(2100 * 16 + 15, 141)]
+    ts = TailStore(ctx, ns, bt, docs)
+    reqs = [docs[0].copy(), np.concatenate([docs[0], wl.tokens(3, 142)]), docs[1][:1500 * 16 + 4], docs[1].copy()]
+    two = type("Two", (), {"idx": ts.idx, "tidx": ts.tidx, "d_hkeys": ts.d_hkeys, "n": ts.n})()
+    for extra in (0, 4100):
+        lengths = [r.size for r in reqs] + [0] * extra
+        ch = Chains(ctx, lengths, 0, bt, slot_counts=_tail_slots(lengths, bt))
+        ch.tokens[:] = np.concatenate(reqs)
+        ch.d_tok.copy_(torch.from_numpy(ch.tokens.view(np.int32)))
+        S = max(ch.n_slots, 1)
+        keys = torch.full((S, 32), SENT, dtype=torch.uint8, device=DEV)
+        handles = torch.full((S,), 0x7777, dtype=torch.int64, device=DEV)
+        hits = torch.full((ch.n,), -1, dtype=torch.int32, device=DEV)
+        log("long chains with tails, empty chains added:", extra)
+        T.tl_chain_lookup_par(ctx, torch.cuda.current_stream(), ch.n, ch.tl, ts.idx, ts.tidx, ts.d_hkeys, ts.n,
+                              keys, handles, hits, T.TL_CHAIN_TAIL)
+        torch.cuda.synchronize()
+        k_np, h_np, hits_np = keys.cpu().numpy(), handles.cpu().numpy().view(np.uint64), hits.cpu().numpy()
+        for c in range(len(reqs)):
+            want_keys, want_hits, want_h = ref.chain_walk(ns, ch.data(c), 4 * bt, ts.index, tail=True)
+            s0, nk = int(ch.slot_off[c]), len(want_keys)
+            assert hits_np[c] == want_hits, (extra, c)
+            assert list(h_np[s0:s0 + want_hits]) == want_h
+            assert (h_np[s0 + want_hits:s0 + nk] == np.uint64(T.MISS)).all()
+            kept = min(want_hits + 1, nk)
+            assert [k_np[s0 + k].tobytes() for k in range(kept)] == want_keys[:kept], (extra, c)
+        assert [int(x) for x in hits_np[:4]] == [2501, 2500, 1500, 2101]
+
+
 def test_stage_with_tails():
     ctx, ns, bt = ctx_bt(4, ppb=3, n_layers=2, groups=[0, 1])  # 12-token blocks of three 4-token pages
     docs = [wl.tokens(n_tok, 130 + i) for i, n_tok in enumerate([5 * 12 + 5, 3 * 12 + 1, 4 * 12])]
