@@ -620,19 +620,21 @@ def main():
     ws_bytes = T.tl_workspace_bytes(ctx, n)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     verd = torch.zeros(n, dtype=torch.uint8, device=dev)
-    # double-buffered pinned staging for the per-step host->device arrays
+    # double-buffered pinned staging for the per-step host->device arrays,
+    # uploaded on a copy stream while the previous step's load runs
+    copy_stream = torch.cuda.Stream()
     stage = []
     for _ in range(2):
         h = {"ptrs": torch.empty(n, dtype=torch.int64, pin_memory=True),
              "lens": torch.empty(n, dtype=torch.int64, pin_memory=True),
              "keys": torch.empty((n, 32), dtype=torch.uint8, pin_memory=True)}
         d = {k: torch.empty_like(v, device=dev) for k, v in h.items()}
-        stage.append((h, d, torch.cuda.Event()))
+        stage.append((h, d, torch.cuda.Event(), torch.cuda.Event()))
     miss = np.uint64(2**64 - 1)
 
     def step(i):
-        h, d, ev = stage[i & 1]
-        ev.synchronize()  # the copy that last read this staging set is done
+        h, d, copied, loaded = stage[i & 1]
+        copied.synchronize()  # the copy that last read this host set is done
         keys = T.tl_block_keys(ctx, tokens)  # a1
         handles = idx.get_batch(keys)  # a2
         hit = handles != miss
@@ -640,11 +642,15 @@ def main():
         h["ptrs"].numpy()[:] = ptrs.view(np.int64)
         h["lens"].numpy()[:] = np.where(hit, rb, 0)
         h["keys"].numpy()[:] = keys
-        for k in d:
-            d[k].copy_(h[k], non_blocking=True)
-        ev.record(stream)
+        copy_stream.wait_event(loaded)  # the load that last read this device set is done
+        with torch.cuda.stream(copy_stream):
+            for k in d:
+                d[k].copy_(h[k], non_blocking=True)
+        copied.record(copy_stream)
+        stream.wait_event(copied)
         blocks = T.make_blocks(d["keys"], d_bidx, d_tokens, d_tdst)
         T.tl_load(ctx, stream, n, d["ptrs"], d["lens"], blocks, dst.tl(), verd, ws, ws_bytes)  # a3-a5
+        loaded.record(stream)
 
     for i in range(args.warmup):
         step(i)
