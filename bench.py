@@ -649,13 +649,21 @@ def main():
         copied.record(copy_stream)
         stream.wait_event(copied)
         blocks = T.make_blocks(d["keys"], d_bidx, d_tokens, d_tdst)
+        if call_events is not None:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
         T.tl_load(ctx, stream, n, d["ptrs"], d["lens"], blocks, dst.tl(), verd, ws, ws_bytes)  # a3-a5
+        if call_events is not None:
+            e1.record(stream)
+            call_events.append((e0, e1))
         loaded.record(stream)
 
+    call_events = None  # HIP event pairs around each timed tl_load call
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
     assert (verd == T.ACCEPT).all().item(), "verification rejected blocks of an undamaged corpus"
+    call_events = []
     for k in T.KERNELS:
         T.tl_timing_read(k)
     torch.cuda.synchronize()
@@ -670,6 +678,9 @@ def main():
         ms, cnt = T.tl_timing_read(k)
         kern[k] = ms / max(cnt, 1)
     T.tl_timing(False)
+    call_ms = sorted(a.elapsed_time(b) for a, b in call_events)
+    call_events = None
+    tl_load_ms = {"median": call_ms[len(call_ms) // 2], "min": call_ms[0], "max": call_ms[-1], "calls": len(call_ms)}
     assert (verd == T.ACCEPT).all().item()
     gbps = step_bytes / (ms_step * 1e-3) / 1e9
     tokens_avoided = n * P
@@ -929,6 +940,7 @@ def main():
         "hbm_frac": gbps / HBM_PEAK_GBPS,
         "tokens_avoided_per_s": tokens_avoided / (ms_step * 1e-3),
         "kernel_ms": kern,
+        "tl_load_ms": tl_load_ms,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "save": save,
