@@ -20,16 +20,21 @@ contributions), so the record layout, the key chain and the tree-mode
 checksum below are this project's readings of what the paper leaves open.
 
 Parity unpinned (by the paper): the byte positions of the header fields, the
-namespace encoding, the verdict codes and their precedence, and the
-zero-fill of a rejected block's pages. The paper prints no worked example
-of any of them. The tests pin only their properties: every single-bit flip
+namespace encoding, the message order of the key chain (the previous key's
+32 bytes, then the block's token ids as u32 little-endian; a partial last
+block hashes exactly its own tokens), the verdict codes and their
+precedence, and the zero-fill of a rejected block's pages. The paper prints
+no worked example of any of them. The tests pin only their properties: every single-bit flip
 and every truncation of a record is rejected; restore equals the permutation
 copy; keys are deterministic and chained; tenants are separated. A golden
 record written by this module guards the layout against accidental change.
 The hashes (hashlib SHA-256, xxhash XXH64), the tree checksum's column
 orientation and the reuse walk are pinned independently: by known-answer
-vectors, a second XXH64 written from its published definition, closed-form
-inputs and brute force.
+vectors, a second XXH64 and a second SHA-256 written from their published
+definitions, closed-form inputs and brute force. The key chain's message
+order is checked against messages assembled byte by byte and hashed by the
+second SHA-256, so a chain that hashed the block before the previous key
+(which keeps every property above) is caught.
 
 Library primitives used as steps: hashlib.sha256 (FIPS 180-4) and
 xxhash.xxh64 (the published XXH64 algorithm). Both are pinned by known-answer

@@ -17,6 +17,7 @@ import numpy as np
 import pytest
 
 from oracle import taliesin_ref as ref
+from tests.sha256_spec import sha256 as spec_sha256
 from tests.xxh64_spec import xxh64 as spec_xxh64
 import workloads as wl
 
@@ -102,6 +103,35 @@ def test_keys_are_chained_prefix_fingerprints():
     ns_b = ref.namespace_digest(b"tenant-b", FP, lay)
     assert not set(ka) & set(ref.block_keys(ns_b, a, B))
     assert ref.block_keys(ns, b"", B) == []
+
+
+def test_key_chain_message_is_previous_key_then_block_bytes():
+    """Brute force over a tiny chain with the message of every key assembled
+    by hand: 32 bytes of the previous key (the namespace digest before the
+    first block), then the block's token ids, each packed as a 4-byte
+    little-endian integer; a partial last block contributes only its own
+    tokens. The hash is the pure-Python SHA-256, not the library the oracle
+    calls. This fixes the byte order of the chain (previous key first) and
+    of the token ids, which the paper leaves open (Sec. 2.2 fixes only that
+    the fingerprint covers the exact input bytes, Sec. 5 that reuse is
+    positional, i.e. chained)."""
+    lay = micro(P=2, D=256)  # 2-token blocks (1 KiB slabs)
+    ns = ref.namespace_digest(TEN, FP, lay)
+    toks = [7, 0x01020304, 65535, 31999, 0, 12, 0xFFFFFFFF]  # 3 full blocks of 2, then a tail of 1
+    data = b"".join(struct.pack("<I", t) for t in toks)
+    want, prev = [], ns
+    for i in range(0, len(toks), 2):
+        msg = bytearray(prev)
+        for t in toks[i:i + 2]:
+            msg += bytes([t & 0xFF, (t >> 8) & 0xFF, (t >> 16) & 0xFF, t >> 24])
+        prev = spec_sha256(bytes(msg))
+        want.append(prev)
+    assert ref.block_keys(ns, data, lay.block_bytes) == want[:3]
+    assert ref.block_keys(ns, data, lay.block_bytes, tail=True) == want
+    # the same chain from a caller-given parent
+    parent = bytes(range(32))
+    m0 = parent + struct.pack("<2I", *toks[:2])
+    assert ref.block_keys(parent, data[:8], lay.block_bytes) == [spec_sha256(m0)]
 
 
 # ---------------------------------------------------------------- tree checksum

@@ -94,6 +94,28 @@ def test_unchained_keys_caught(monkeypatch):
         pins.test_keys_are_chained_prefix_fingerprints()
 
 
+def _block_then_key(parent, data, block_bytes, tail=False):
+    # wrong reading of the chain: the block's bytes before the previous key
+    keys, k = [], bytes(parent)
+    n = -(-len(data) // block_bytes) if tail else len(data) // block_bytes
+    for i in range(n):
+        k = __import__("hashlib").sha256(bytes(data[i * block_bytes:(i + 1) * block_bytes]) + k).digest()
+        keys.append(k)
+    return keys
+
+
+def test_swapped_chain_order_caught(monkeypatch):
+    """SHA-256(block || k) keeps every property pin (determinism, prefix
+    sharing, chaining, positions, tenants); the explicit-message pin and the
+    golden record must both catch it."""
+    monkeypatch.setattr(ref, "block_keys", _block_then_key)
+    pins.test_keys_are_chained_prefix_fingerprints()  # the properties hold for the mutant too
+    with pytest.raises(AssertionError):
+        pins.test_key_chain_message_is_previous_key_then_block_bytes()
+    with pytest.raises(AssertionError):
+        test_golden_record_regression()
+
+
 def test_root_without_zeroed_field_caught(monkeypatch):
     monkeypatch.setattr(ref, "root_digest", lambda meta: ref.xxh64(bytes(meta), 0))
     with pytest.raises(AssertionError):

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import taliesin_ref as ref
+from tests.sha256_spec import sha256 as spec_sha256
 from tests.xxh64_spec import xxh64 as spec_xxh64
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -45,9 +46,21 @@ def test_xxh64_known_answers():
 def test_sha256_known_answers():
     n = 0
     for data, want in _kat("sha256_kat.txt"):
-        assert hashlib.sha256(_spec_bytes(data)).hexdigest() == want
+        d = _spec_bytes(data)
+        assert hashlib.sha256(d).hexdigest() == want
+        if len(d) < 10000:  # the pure-Python SHA-256 is slow
+            assert spec_sha256(d).hex() == want
         n += 1
     assert n >= 4
+
+
+def test_sha256_library_matches_spec_all_padding_lengths():
+    # every padding case: lengths around the 55/56/64-byte boundaries, one to
+    # three message blocks
+    rng = np.random.default_rng(7)
+    for n in list(range(0, 130)) + [183, 184, 191, 192, 200]:
+        d = rng.integers(0, 256, n, dtype=np.uint8).tobytes()
+        assert hashlib.sha256(d).digest() == spec_sha256(d), n
 
 
 @pytest.mark.parametrize("seed", [0, 1, 63, 2**32 + 5, 2**64 - 1])
