@@ -121,8 +121,11 @@ typedef struct tl_geometry {
 /* A paged KV cache in HBM. Page p of layer l's K cache starts at device
  * address d_layer_k[l] + p * page_stride (same for V). The caller guarantees
  * these addresses are valid and 16-byte aligned for every p in [0, n_pages)
- * that the block tables name; the library checks table entries against
- * n_pages but cannot check device pointers from the host. */
+ * that the block tables name: every layer base d_layer_k[l], d_layer_v[l]
+ * must be a multiple of 16 (page_stride is checked to be one), since the
+ * kernels move each page in 16-byte granules. The library checks table
+ * entries against n_pages, the stride and the alignment of the two address
+ * arrays, but cannot read the device-resident bases from the host. */
 typedef struct tl_cache {
   const uint64_t* d_layer_k; /* device [n_layers] base addresses */
   const uint64_t* d_layer_v; /* device [n_layers] base addresses */

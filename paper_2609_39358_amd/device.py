@@ -31,6 +31,9 @@ class PagedCache:
         self.v = layers_v if layers_v is not None else [mk() for _ in range(n_layers)]
         for t in self.k + self.v:
             assert t.dtype == torch.uint8 and t.shape == (n_pages, page_stride) and t.is_contiguous()
+            if t.data_ptr() % 16:
+                # the kernels move every page in 16-byte granules
+                raise ValueError("layer tensors must start on a 16-byte boundary")
         self.d_k = torch.tensor([t.data_ptr() for t in self.k], dtype=torch.int64, device=device)
         self.d_v = torch.tensor([t.data_ptr() for t in self.v], dtype=torch.int64, device=device)
 

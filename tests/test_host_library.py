@@ -259,6 +259,22 @@ def test_binding_refuses_host_tensors_for_device_arguments():
                   good, 0x70000)
 
 
+def test_paged_cache_refuses_misaligned_layer_tensors():
+    """Layer bases must be 16-byte aligned (the kernels move 16-byte
+    granules): a cache built on a view 8 bytes into a buffer is refused
+    before any device array is made."""
+    from paper_2609_39358_amd.device import PagedCache
+    buf = torch.zeros(4 * 1024 + 16, dtype=torch.uint8)
+    good = buf[:4 * 1024].view(4, 1024)
+    bad = buf[8:8 + 4 * 1024].view(4, 1024)
+    assert good.data_ptr() % 16 == 0 and bad.data_ptr() % 16 == 8
+    PagedCache(1, 4, 1024, "cpu", layers_k=[good], layers_v=[good])
+    with pytest.raises(ValueError, match="16-byte"):
+        PagedCache(1, 4, 1024, "cpu", layers_k=[bad], layers_v=[good])
+    with pytest.raises(ValueError, match="16-byte"):
+        PagedCache(1, 4, 1024, "cpu", layers_k=[good], layers_v=[bad])
+
+
 def test_status_and_verdict_strings():
     assert T.verdict_name(T.ACCEPT) == "ACCEPT"
     assert T.verdict_name(T.SEGMENT) == "SEGMENT"
