@@ -44,3 +44,14 @@ def _release_gpu_memory(request):
                 torch.cuda.empty_cache()
         except Exception:
             pass
+
+
+@pytest.fixture(scope="session")
+def record_checker():
+    """Spawned oracle workers that check every record of a full-size save
+    (tests/record_check.py); started on first use."""
+    from tests.record_check import RecordChecker
+
+    c = RecordChecker()
+    yield c
+    c.close()

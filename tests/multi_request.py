@@ -16,6 +16,7 @@ from paper_2609_39358_amd import pipeline
 from paper_2609_39358_amd import taliesin as T
 from paper_2609_39358_amd.device import PagedCache
 from tests.gpu_case import DEV, FP, TEN, ctx_of, fill_cache, i32, i64, layout_of, log
+from tests.record_check import Damage, lay_args
 
 
 @dataclass
@@ -26,7 +27,11 @@ class Batch:
 
 
 class MultiRun:
-    def __init__(self, w: wl.MultiWorkload, pool_pages: int, seed: int = 3):
+    """checker: a RecordChecker; when given, every stored record is compared
+    with the oracle's after the save, and `want[rid]` holds the oracle's
+    verdict on record rid as the loads find it (damaged or not)."""
+
+    def __init__(self, w: wl.MultiWorkload, pool_pages: int, seed: int = 3, checker=None):
         self.w, self.g = w, w.geom
         g = self.g
         self.lay = layout_of(g)
@@ -42,6 +47,8 @@ class MultiRun:
         log("multi-request: %d stored records of %d B, pool %d pages" % (self.n_stored, self.rb, pool_pages))
         self.src = fill_cache(PagedCache(g.n_layers, self.n_stored, self.lay.slab_bytes, DEV), g, seed)
         base_keys = T.tl_block_keys_batch(self.ctx, w.base_docs)
+        for d, k in zip(w.base_docs, base_keys):  # every base key against the oracle's chain
+            assert [x.tobytes() for x in k] == ref.block_keys(self.ns, d.tobytes(), self.lay.block_bytes)[:self.bpd]
         self.keys = np.concatenate(base_keys)
         self.bidx = np.tile(np.arange(self.bpd, dtype=np.uint64), len(w.base_docs))
         self.tokens = np.concatenate([d[:self.bpd * P].reshape(self.bpd, P) for d in w.base_docs])
@@ -54,6 +61,16 @@ class MultiRun:
                   T.make_blocks(*self._save_in), self.store.ptrs, st)
         torch.cuda.synchronize()
         assert (st == ref.ACCEPT).all().item()
+        self.want = None
+        if checker is not None:
+            dmg = {rid: Damage(bits=[wl.scale_bit(frac, self.rb)]) for rid, frac in w.corrupt_flip}
+            for rid, frac in w.corrupt_trunc:
+                dmg.setdefault(rid, Damage()).length = wl.scale_len(frac, self.rb)
+            tab = self.src_table[None, :]
+            eq, self.want = checker.check(lay_args(self.lay), self.ns, self.src.k, self.src.v, tab, self.store.buf,
+                                          [k.tobytes() for k in self.keys], self.bidx, self.tokens, tab,
+                                          damage=dmg, log=log)
+            assert eq.all(), ("records differ from the oracle's", np.nonzero(~eq)[0][:20])
         # damage: bit flips in place, truncations as shorter reported lengths
         self.lens = self.st.lens
         self.flip_bits: Dict[int, int] = {}
@@ -75,8 +92,11 @@ class MultiRun:
         out = []
         for bi, reqs in enumerate(wl.admission_batches(w.requests, self.pool_pages)):
             res = self.pipe.restore([w.requests[r].tokens for r in reqs], reqs)
-            for r, h in zip(reqs, res.hits):
+            for r, h, k in zip(reqs, res.hits, res.keys):
                 assert h == w.requests[r].shared_blocks, (r, h, w.requests[r].shared_blocks)
+                # the keys the pipeline looked up are the oracle's chain of the request
+                assert [x.tobytes() for x in k] == ref.block_keys(self.ns, w.requests[r].tokens.tobytes(),
+                                                                  self.lay.block_bytes), r
             torch.cuda.synchronize()
             b = Batch(reqs)
             b.blocks = [(int(r), int(p), int(rid), page) for page, (r, p, rid) in
@@ -88,11 +108,15 @@ class MultiRun:
             out.append(b)
         return out
 
-    def oracle_verdict(self, rid: int) -> int:
-        """The oracle's verdict for stored record rid loaded at its own position."""
-        rec = self.store.buf[rid].cpu().numpy().tobytes()[:int(self.lens[rid])]
-        return ref.verify(self.lay, self.ns, rec, self.keys[rid].tobytes(), int(self.bidx[rid]),
-                          self.tokens[rid], range(self.lay.n_slabs))
+    def check_block_identity(self, b: Batch):
+        """Every restored block asks for exactly what its record holds: the
+        request's key, position and token ids at that block equal the stored
+        record's (so the oracle's verdict on the record is the block's)."""
+        P = self.g.page_tokens
+        for req, pos, rid, page in b.blocks:
+            q = self.w.requests[req]
+            assert pos == int(self.bidx[rid]), (req, pos, rid)
+            assert np.array_equal(q.tokens[pos * P:(pos + 1) * P], self.tokens[rid]), (req, pos, rid)
 
     def check_pages(self, b: Batch, rejected: set):
         """Accepted blocks' pool pages equal their source pages; rejected ones are zero."""

@@ -1,8 +1,11 @@
 """Full-size GPU parity on the paper-corpus and hybrid workloads, in the same
-library calls the benchmark times. At these sizes the oracle checks sampled
-blocks one by one (records byte for byte, verdicts, restored pages); every
-block is checked by properties that hold at any size (all verdicts, and
-destination pages equal the source pages under the two block tables)."""
+library calls the benchmark times. Every record of the save is compared with
+the oracle's record byte for byte, and every block's verdict with the
+oracle's verdict on that record as the load finds it (damaged or not, with
+the slabs the load reads), on spawned oracle workers (tests/record_check.py).
+Restored pages are checked against the closed form of the oracle's restore:
+destination pages equal the source pages under the two block tables,
+rejected blocks' pages are zero, untouched pages keep their bytes."""
 import numpy as np
 import pytest
 import torch
@@ -12,6 +15,7 @@ from oracle import taliesin_ref as ref
 from paper_2609_39358_amd import taliesin as T
 from paper_2609_39358_amd.device import PagedCache, RecordStore
 from tests.gpu_case import DEV, Case, i32, i64, log
+from tests.record_check import Damage, lay_args
 
 pytestmark = pytest.mark.gpu
 
@@ -19,20 +23,6 @@ pytestmark = pytest.mark.gpu
 def sample_blocks(n, k, seed):
     r = np.random.default_rng(seed)
     return sorted({0, n - 1, *r.choice(n, size=k, replace=False).tolist()})
-
-
-def oracle_record(c: Case, b: int):
-    """The oracle's record for block b, from host copies of just its pages."""
-    G = c.geom.n_groups
-    hk, hv = [], []
-    for l in range(c.geom.n_layers):
-        p = int(c.t_src[c.geom.group(l)][b])
-        hk.append(c.src.k[l][p:p + 1].cpu().numpy())
-        hv.append(c.src.v[l][p:p + 1].cpu().numpy())
-    recs, st = ref.save(c.lay, c.ns, hk, hv, np.zeros((G, 1), np.int32), [c.keys[b].tobytes()],
-                        [int(c.bidx[b])], c.tokens[b:b + 1], n_pages=1)
-    assert st == [ref.ACCEPT]
-    return recs[0]
 
 
 def check_pages_equal(c: Case, dst: PagedCache, tables, blocks=None):
@@ -50,7 +40,7 @@ def check_pages_equal(c: Case, dst: PagedCache, tables, blocks=None):
             assert torch.equal(d_t[tdd, :slab], s_t[ts, :slab]), ("layer", l)
 
 
-def test_paper_corpus_full_scale():
+def test_paper_corpus_full_scale(record_checker):
     cfg = wl.PAPER_CORPUS
     n = cfg.n_tokens // cfg.geom.page_tokens
     c = Case(cfg.geom, n, cfg.src_pages, cfg.dst_pages, cfg.seed)
@@ -64,32 +54,31 @@ def test_paper_corpus_full_scale():
     assert (st == ref.ACCEPT).all()
     samp = sample_blocks(n, 10, 1)
     rb = c.lay.record_bytes
-    for b in samp:
-        assert store.buf[b].cpu().numpy().tobytes() == oracle_record(c, b), b
-    # damage three sampled records (metadata bit, payload bit, truncation)
-    dmg = {samp[1]: ("bit", 77 * 8 + 3), samp[2]: ("bit", (rb - 5) * 8 + 6), samp[3]: ("trunc", rb - 1)}
+    # damage three records (metadata bit, payload bit, truncation) and a
+    # fourth with two payload bits in one chunk column
+    dmg = {samp[1]: Damage(bits=[77 * 8 + 3]), samp[2]: Damage(bits=[(rb - 5) * 8 + 6]),
+           samp[3]: Damage(length=rb - 1),
+           samp[4]: Damage(bits=[(c.lay.payload_offset + 4096) * 8, (c.lay.payload_offset + 4096 + 1024) * 8])}
+    # every record against the oracle's, and the oracle's verdict for every block
+    eq, want = record_checker.check(lay_args(c.lay), c.ns, c.src.k, c.src.v, c.t_src, store.buf,
+                                    [k.tobytes() for k in c.keys], c.bidx, c.tokens, c.t_dst, damage=dmg, log=log)
+    assert eq.all(), ("records differ from the oracle's", np.nonzero(~eq)[0][:20])
+    assert [int(want[b]) for b in dmg] == [ref.ROOT, ref.SEGMENT, ref.TRUNCATED, ref.SEGMENT]
+    host_rec = {b: bytearray(store.buf[b].cpu().numpy().tobytes()) for b in samp}
     lens = np.full(n, rb, np.uint64)
-    host_rec = {}
-    for b in samp:
-        host_rec[b] = bytearray(store.buf[b].cpu().numpy().tobytes())
-    for b, (kind, x) in dmg.items():
-        if kind == "bit":
+    for b, d in dmg.items():
+        for x in d.bits:
             store.buf[b, x >> 3] ^= 1 << (x & 7)
             host_rec[b][x >> 3] ^= 1 << (x & 7)
-        else:
-            lens[b] = x
+        if d.length is not None:
+            lens[b] = d.length
     dst = PagedCache(c.geom.n_layers, cfg.dst_pages, c.stride, DEV)
     for t in dst.k + dst.v:
         t.fill_(0x5A)
     v = c.load(store.ptrs, i64(lens), c.t_dst, dst)
-    want = {b: ref.verify(c.lay, c.ns, bytes(host_rec[b][:int(lens[b])]), c.keys[b].tobytes(), b,
-                          c.tokens[b], range(c.lay.n_slabs)) for b in samp}
-    for b in samp:
-        assert int(v[b]) == want[b], (b, want[b])
-    assert [want[b] for b in dmg] == [ref.ROOT, ref.SEGMENT, ref.TRUNCATED]
-    ok = np.ones(n, bool)
-    ok[list(dmg)] = False
-    assert (v[ok] == ref.ACCEPT).all()
+    assert np.array_equal(v, want), np.nonzero(v != want)[0][:20]
+    ok = v == ref.ACCEPT
+    assert ok.sum() == n - len(dmg)
     # every accepted block restored exactly; rejected blocks' pages are zero
     good = np.nonzero(ok)[0]
     check_pages_equal(c, dst, c.t_dst, blocks=good)
@@ -97,7 +86,7 @@ def test_paper_corpus_full_scale():
         p = int(c.t_dst[0][b])
         for l in range(c.geom.n_layers):
             assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
-    # sampled accepted blocks: restored pages are the oracle record's slabs
+    # sampled accepted blocks: restored pages are the record's slabs
     for b in samp:
         if b in dmg:
             continue
@@ -109,7 +98,7 @@ def test_paper_corpus_full_scale():
             assert dst.v[l][p].cpu().numpy().tobytes() == bytes(rec[po + (2 * l + 1) * S: po + (2 * l + 2) * S])
 
 
-def test_hybrid_full_scale():
+def test_hybrid_full_scale(record_checker):
     cfg = wl.HYBRID
     g = cfg.geom
     n = cfg.n_tokens // g.page_tokens
@@ -119,30 +108,28 @@ def test_hybrid_full_scale():
     c.make_src()
     store, st = c.save()
     assert (st == ref.ACCEPT).all()
-    samp = [0, 100, 252, 255]
-    for b in samp:
-        assert store.buf[b].cpu().numpy().tobytes() == oracle_record(c, b), b
     tables = wl.hybrid_tables(cfg, c.t_dst[0])
     assert (tables[1] >= 0).sum() == 4 and (tables[0] >= 0).sum() == n
     rb, po, S = c.lay.record_bytes, c.lay.payload_offset, c.lay.slab_bytes
-    # block 10: flip inside layer 0 K (a sliding-window layer; not read for block 10)
-    store.buf[10, po + 12345] ^= 1
-    # block 253: flip inside layer 0 K (read: block 253 is window-resident)
-    store.buf[253, po + 12345] ^= 1
-    # block 20: flip inside layer 5 V (a global layer; always read)
-    store.buf[20, po + 11 * S + 999] ^= 8
+    dmg = {10: Damage(bits=[(po + 12345) * 8]),      # layer 0 K: a sliding-window layer, not read for block 10
+           253: Damage(bits=[(po + 12345) * 8]),     # the same flip, read: block 253 is window-resident
+           20: Damage(bits=[(po + 11 * S + 999) * 8 + 3]),  # layer 5 V: a global layer, always read
+           30: Damage(bits=[(po + 7 * S + 5) * 8 + 1])}     # layer 3 V: sliding window, not read for block 30
+    eq, want = record_checker.check(lay_args(c.lay), c.ns, c.src.k, c.src.v, c.t_src, store.buf,
+                                    [k.tobytes() for k in c.keys], c.bidx, c.tokens, tables, damage=dmg, log=log)
+    assert eq.all(), ("records differ from the oracle's", np.nonzero(~eq)[0][:20])
+    for b, d in dmg.items():
+        for x in d.bits:
+            store.buf[b, x >> 3] ^= 1 << (x & 7)
+    exp = np.full(n, ref.ACCEPT)
+    exp[253] = ref.SEGMENT
+    exp[20] = ref.SEGMENT
+    assert np.array_equal(want, exp), np.nonzero(want != exp)
     dst = PagedCache(g.n_layers, cfg.dst_pages, c.stride, DEV)
     for t in dst.k + dst.v:
         t.fill_(0x3C)
     v = c.load(store.ptrs, store.lens, tables, dst)
-    exp = np.full(n, ref.ACCEPT)
-    exp[253] = ref.SEGMENT
-    exp[20] = ref.SEGMENT
-    assert np.array_equal(v, exp), np.nonzero(v != exp)
-    for b in (10, 20, 253, 254):
-        rec = store.buf[b].cpu().numpy().tobytes()
-        read = [s for s, *_ in ref.read_slabs(c.lay, tables, b)]
-        assert int(v[b]) == ref.verify(c.lay, c.ns, rec, c.keys[b].tobytes(), b, c.tokens[b], read), b
+    assert np.array_equal(v, want), np.nonzero(v != want)
     good = [b for b in range(n) if b not in (20, 253)]
     check_pages_equal(c, dst, tables, blocks=good)
     # pages a load never touches keep their bytes: local layers, non-window blocks
