@@ -282,6 +282,20 @@ int tl_index_put(tl_index* idx, const uint8_t key[TL_KEY_BYTES], uint64_t handle
 /* handles_out[i] = handle of keys[i], or UINT64_MAX when absent */
 int tl_index_get_batch(const tl_index* idx, const uint8_t* keys, size_t n, uint64_t* handles_out);
 size_t tl_index_size(const tl_index* idx);
+/* The reuse rule of a2 for a batch of requests (Sec. 2.2: a later request
+ * loads the stored state of the blocks it shares; Sec. 5: whole blocks at
+ * exact positions, so a request's reuse ends at its first block with no
+ * stored state, since every later key covers that block). Request d owns
+ * keys [key_off[d], key_off[d] + n_keys[d]) of `keys` (host, 32 bytes each,
+ * in block order, e.g. from tl_block_keys_batch). Its keys are looked up in
+ * order up to the first one that is not in the index: hits_out[d] = the
+ * number of leading keys found, handles_out[key_off[d] + i] = the handle of
+ * key i for i < hits_out[d], and UINT64_MAX at key_off[d] + hits_out[d] when
+ * that slot exists; later slots of the request are not written. Host arrays;
+ * n_docs up to 2^32. TL_EINVAL for NULL arrays with n_docs > 0 (keys and
+ * handles_out may be NULL when every n_keys[d] is 0). */
+int tl_index_lookup_prefix(const tl_index* idx, const uint8_t* keys, const uint64_t* key_off,
+                           const uint64_t* n_keys, size_t n_docs, uint64_t* hits_out, uint64_t* handles_out);
 
 /* ---- a1 + a2 on the device: key chains and a device index ----------------
  * For engines whose token ids are already in HBM. The same chained keys as

@@ -295,6 +295,28 @@ int tl_index_get_batch(const tl_index* idx, const uint8_t* keys, size_t n, uint6
 
 size_t tl_index_size(const tl_index* idx) { return idx ? idx->size : 0; }
 
+int tl_index_lookup_prefix(const tl_index* idx, const uint8_t* keys, const uint64_t* key_off,
+                           const uint64_t* n_keys, size_t n_docs, uint64_t* hits_out, uint64_t* handles_out) {
+  if (!idx || (n_docs && (!key_off || !n_keys || !hits_out))) return TL_EINVAL;
+  if (n_docs >= (1ull << 32)) return TL_ERANGE;
+  bool any = false;
+  for (size_t d = 0; d < n_docs; ++d) any |= n_keys[d] != 0;
+  if (any && (!keys || !handles_out)) return TL_EINVAL;
+  for (size_t d = 0; d < n_docs; ++d) {
+    const uint8_t* k = keys + 32 * key_off[d];
+    uint64_t* h = handles_out + key_off[d];
+    uint64_t i = 0;
+    for (; i < n_keys[d]; ++i) {
+      const tl_index::Slot& s = idx->slots[idx->find(k + 32 * i)];
+      if (!s.used) break;  // reuse ends at the first block with no stored state
+      h[i] = s.handle;
+    }
+    if (i < n_keys[d]) h[i] = UINT64_MAX;
+    hits_out[d] = i;
+  }
+  return TL_OK;
+}
+
 // ---- a3-a6: validation in front of the launches ------------------------------
 static int check_cache(const tl_ctx* ctx, const tl_cache* c) {
   if (!c || !c->d_layer_k || !c->d_layer_v) return TL_EINVAL;

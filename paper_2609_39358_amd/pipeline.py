@@ -41,6 +41,7 @@ class BatchResult:
     request_of: np.ndarray   # [n] which request a restored block belongs to
     verdicts: torch.Tensor   # [n] device verdict bytes (valid after the stream syncs)
     keys_lookup_s: float = 0.0
+    keys: List[np.ndarray] = None  # every request's block keys [n_i, 32]
 
 
 class Store:
@@ -58,7 +59,14 @@ class Store:
 
 class RestorePipeline:
     """Restores the stored prefix blocks of batches of requests into `pool`
-    (pages 0 .. n-1 of the pool, in request order)."""
+    (pages 0 .. n-1 of the pool, in request order).
+
+    Each call runs the keys (tl_block_keys_batch, host threads) and the reuse
+    lookup (tl_index_lookup_prefix) on the host, writes tl_load's per-block
+    arrays into one of two pinned host sets, uploads them on a copy stream
+    and enqueues tl_load on `stream` behind the upload. Nothing waits for the
+    GPU except the reuse of a set two calls later, so the host work of a batch
+    overlaps the previous batch's restore when calls follow each other."""
 
     def __init__(self, store: Store, pool: PagedCache, stream=None, threads: int = 0):
         self.store, self.pool, self.threads = store, pool, threads
@@ -66,50 +74,73 @@ class RestorePipeline:
         self.stream = stream or torch.cuda.current_stream()
         dev = pool.k[0].device
         cap = pool.n_pages
+        self.cap = cap
         self.ws_bytes = max(T.tl_workspace_bytes(self.ctx, cap), 4)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
         self.dev = dev
+        self.copy_stream = torch.cuda.Stream(device=dev)
+        P, G = self.ctx.block_bytes // 4, self.ctx.n_groups
+        shapes = {"ptrs": ((cap,), torch.int64), "lens": ((cap,), torch.int64), "keys": ((cap, 32), torch.uint8),
+                  "pos": ((cap,), torch.int64), "tok": ((cap, P), torch.int32), "tab": ((G * cap,), torch.int32)}
+        self._sets = []
+        for _ in range(2):
+            h = {k: torch.empty(sh, dtype=dt, pin_memory=True) for k, (sh, dt) in shapes.items()}
+            d = {k: torch.empty(sh, dtype=dt, device=dev) for k, (sh, dt) in shapes.items()}
+            self._sets.append((h, d, torch.cuda.Event(), torch.cuda.Event()))
+        self._calls = 0
 
     def restore(self, tokens: Sequence[np.ndarray], request_ids: Sequence[int]) -> BatchResult:
         import time
 
-        P = self.ctx.block_bytes // 4
+        ctx = self.ctx
+        P, G = ctx.block_bytes // 4, ctx.n_groups
         t0 = time.perf_counter()
-        keys = T.tl_block_keys_batch(self.ctx, tokens, n_threads=self.threads)
-        hits, rids, pos, req, kk, tk = [], [], [], [], [], []
-        for i, (k, toks) in enumerate(zip(keys, tokens)):
-            h = self.store.index.get_batch(k)
-            miss = np.nonzero(h == MISS)[0]
-            n_hit = int(miss[0]) if miss.size else len(h)  # reuse stops at the first miss
-            hits.append(n_hit)
-            rids.append(h[:n_hit])
-            pos.append(np.arange(n_hit, dtype=np.uint64))
-            req.append(np.full(n_hit, request_ids[i], dtype=np.int64))
-            kk.append(k[:n_hit])
-            tk.append(np.asarray(toks[:n_hit * P], dtype="<u4").reshape(n_hit, P))
+        keys, koff, nk = T.tl_block_keys_batch(ctx, tokens, n_threads=self.threads, flat=True)  # a1
+        hits, handles = self.store.index.lookup_prefix(keys, koff, nk)  # a2: each request's leading stored run
         t1 = time.perf_counter()
-        rid = np.concatenate(rids) if rids else np.zeros(0, np.uint64)
+        # marshalling: the hit blocks of every request, in request order
+        nk_i = nk.astype(np.int64)
+        pos_all = np.arange(keys.shape[0], dtype=np.int64) - np.repeat(koff.astype(np.int64), nk_i)
+        sel = pos_all < np.repeat(hits.astype(np.int64), nk_i)
+        rid = handles[sel]
         n = int(rid.size)
-        if n > self.pool.n_pages:
-            raise ValueError("batch needs %d pages, pool has %d" % (n, self.pool.n_pages))
+        if n > self.cap:
+            raise ValueError("batch needs %d pages, pool has %d" % (n, self.cap))
+        res = BatchResult(list(request_ids), [int(h) for h in hits], rid, pos_all[sel].astype(np.uint64),
+                          np.repeat(np.asarray(request_ids, dtype=np.int64), nk_i)[sel], None, t1 - t0,
+                          [keys[int(o):int(o) + int(k)] for o, k in zip(koff, nk)])
         with _on(self.stream):
             verd = torch.empty(max(n, 1), dtype=torch.uint8, device=self.dev)  # tl_load writes all n
-            res = BatchResult(list(request_ids), hits, rid, np.concatenate(pos) if pos else rid,
-                              np.concatenate(req) if req else np.zeros(0, np.int64), verd[:n], t1 - t0)
+            res.verdicts = verd[:n]
             if n == 0:
                 return res
+            h, d, copied, loaded = self._sets[self._calls & 1]
+            self._calls += 1
+            copied.synchronize()  # the upload that last read this host set is done
             base = np.uint64(self.store.records.buf.data_ptr())
-            ptrs = (base + rid * np.uint64(self.ctx.record_bytes)).view(np.int64)
-            lens = self.store.lens[rid].view(np.int64)
-            to_dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(self.dev, non_blocking=False)
-            d_ptrs, d_lens = to_dev(ptrs), to_dev(lens)
-            d_keys = to_dev(np.concatenate(kk))
-            d_pos = to_dev(res.positions.view(np.int64))
-            d_tok = to_dev(np.concatenate(tk).view(np.int32))
-            d_tab = to_dev(np.arange(n, dtype=np.int32)[None, :])
-            T.tl_load(self.ctx, self.stream, n, d_ptrs, d_lens, T.make_blocks(d_keys, d_pos, d_tok, d_tab),
-                      self.pool.tl(), verd, self.ws, self.ws_bytes)
-            res._keep = (d_ptrs, d_lens, d_keys, d_pos, d_tok, d_tab)
+            h["ptrs"].numpy()[:n] = (base + rid * np.uint64(ctx.record_bytes)).view(np.int64)
+            h["lens"].numpy()[:n] = self.store.lens[rid].view(np.int64)
+            h["keys"].numpy()[:n] = keys[sel]
+            h["pos"].numpy()[:n] = res.positions.view(np.int64)
+            tok = h["tok"].numpy()
+            row = 0
+            for t, k in zip(tokens, hits):
+                k = int(k)
+                if k:
+                    tok[row:row + k] = np.asarray(t[:k * P], dtype="<u4").view(np.int32).reshape(k, P)
+                    row += k
+            h["tab"].numpy()[:G * n] = np.tile(np.arange(n, dtype=np.int32), G)
+            self.copy_stream.wait_event(loaded)  # the load that last read this device set is done
+            with torch.cuda.stream(self.copy_stream):
+                for k in ("ptrs", "lens", "keys", "pos", "tok"):
+                    d[k][:n].copy_(h[k][:n], non_blocking=True)
+                d["tab"][:G * n].copy_(h["tab"][:G * n], non_blocking=True)
+            copied.record(self.copy_stream)
+            self.stream.wait_event(copied)
+            blk = T.make_blocks(d["keys"][:n], d["pos"][:n], d["tok"][:n], d["tab"][:G * n])
+            T.tl_load(ctx, self.stream, n, d["ptrs"][:n], d["lens"][:n], blk, self.pool.tl(), verd, self.ws,
+                      self.ws_bytes)
+            loaded.record(self.stream)
         return res
 
 

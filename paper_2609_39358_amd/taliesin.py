@@ -96,6 +96,7 @@ def _load():
         "tl_index_put": (c.c_int, [P, P, c.c_uint64]),
         "tl_index_get_batch": (c.c_int, [P, P, c.c_size_t, P]),
         "tl_index_size": (c.c_size_t, [P]),
+        "tl_index_lookup_prefix": (c.c_int, [P, P, P, P, c.c_size_t, P, P]),
         "tl_dindex_bytes": (c.c_size_t, [c.c_size_t]),
         "tl_dindex_create": (P, [P, c.c_size_t, c.c_size_t, P, c.POINTER(c.c_int)]),
         "tl_dindex_destroy": (None, [P]),
@@ -133,7 +134,7 @@ _lib = _load()
 EXPORTED = (
     "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
     "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_save_layers", "tl_save_seal", "tl_load", "tl_index_create",
-    "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size",
+    "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size", "tl_index_lookup_prefix",
     "tl_dindex_bytes", "tl_dindex_create", "tl_dindex_destroy", "tl_dindex_workspace_bytes",
     "tl_dindex_put", "tl_dindex_get", "tl_dindex_stats", "tl_chain_lookup", "tl_chain_stage",
     "tl_block_fingerprints", "tl_chain_lookup_par", "tl_file_open", "tl_file_close", "tl_file_records",
@@ -259,8 +260,10 @@ def tl_block_keys(ctx: Ctx, data, parent: Optional[bytes] = None, block_bytes: i
 
 
 def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int = 0,
-                        n_threads: int = 0, tail: bool = False):
-    """Keys for several documents in parallel; returns a list of [n_i, 32] arrays."""
+                        n_threads: int = 0, tail: bool = False, flat: bool = False):
+    """Keys for several documents in parallel; returns a list of [n_i, 32]
+    arrays, or with flat=True (keys [N, 32], first key of each document [n],
+    key count of each document [n]) over one array."""
     bufs = [_host_buf(d) for d in docs]
     B = block_bytes or ctx.block_bytes
     lens = np.array([len(b) for b in bufs], dtype=np.uint64)
@@ -278,6 +281,8 @@ def tl_block_keys_batch(ctx: Ctx, docs: Sequence, parents=None, block_bytes: int
                                     TL_KEYS_TAIL if tail else 0, keys.ctypes.data, koff.ctypes.data,
                                     nout.ctypes.data, n_threads),
            "tl_block_keys_batch")
+    if flat:
+        return keys, koff, nk
     return [keys[int(o):int(o) + int(k)] for o, k in zip(koff, nk)]
 
 
@@ -394,6 +399,20 @@ class Index:
         _check(_lib.tl_index_get_batch(self._h, k.ctypes.data, k.shape[0], out.ctypes.data),
                "tl_index_get_batch")
         return out
+
+    def lookup_prefix(self, keys: np.ndarray, key_off: np.ndarray, n_keys: np.ndarray):
+        """Leading stored keys of each request (tl_index_lookup_prefix): keys
+        [N, 32] u8 back to back, request d at rows [key_off[d], key_off[d] +
+        n_keys[d]). Returns (hits [n_docs] u64, handles [N] u64; the slots
+        past each request's hits + 1 are unspecified)."""
+        k = np.ascontiguousarray(np.asarray(keys, dtype=np.uint8).reshape(-1, 32))
+        off = np.ascontiguousarray(key_off, dtype=np.uint64)
+        cnt = np.ascontiguousarray(n_keys, dtype=np.uint64)
+        hits = np.empty(off.size, dtype=np.uint64)
+        h = np.empty(k.shape[0], dtype=np.uint64)
+        _check(_lib.tl_index_lookup_prefix(self._h, k.ctypes.data, off.ctypes.data, cnt.ctypes.data, off.size,
+                                           hits.ctypes.data, h.ctypes.data), "tl_index_lookup_prefix")
+        return hits, h
 
     def __len__(self):
         return int(_lib.tl_index_size(self._h))

@@ -130,6 +130,19 @@ int main() {
   std::vector<uint64_t> h(600);
   EXPECT(tl_index_get_batch(idx, ik.data(), 600, h.data()) == TL_OK);
   EXPECT(h[0] == 77 && h[499] == 499 && h[550] == UINT64_MAX);
+  // leading run per request: [0, 10) all stored; [10, 20) with key 505 (not
+  // stored) at position 3; an empty request; [490, 510) ends at 500
+  memcpy(&ik[32 * 13], &ik[32 * 505], 32);
+  uint64_t pkoff[4] = {0, 10, 20, 490}, pkn[4] = {10, 10, 0, 20}, phits[4];
+  std::vector<uint64_t> hh(600, 12345);
+  EXPECT(tl_index_lookup_prefix(idx, ik.data(), pkoff, pkn, 4, phits, hh.data()) == TL_OK);
+  EXPECT(phits[0] == 10 && phits[1] == 3 && phits[2] == 0 && phits[3] == 10);
+  EXPECT(hh[0] == 77 && hh[9] == 9 && hh[12] == 12 && hh[13] == UINT64_MAX && hh[14] == 12345);
+  EXPECT(hh[499] == 499 && hh[500] == UINT64_MAX && hh[501] == 12345);
+  EXPECT(tl_index_lookup_prefix(idx, ik.data(), nullptr, pkn, 4, phits, hh.data()) == TL_EINVAL);
+  EXPECT(tl_index_lookup_prefix(idx, nullptr, pkoff, pkn, 4, phits, hh.data()) == TL_EINVAL);
+  EXPECT(tl_index_lookup_prefix(idx, nullptr, pkoff, pkn + 2, 1, phits, nullptr) == TL_OK && phits[0] == 0);
+  EXPECT(tl_index_lookup_prefix(idx, nullptr, nullptr, nullptr, 0, nullptr, nullptr) == TL_OK);
   tl_index_destroy(idx);
   EXPECT(!tl_index_create(0));
 

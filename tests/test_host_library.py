@@ -178,6 +178,48 @@ def test_index_put_get():
     assert np.array_equal(j.get_batch(k2), np.arange(100, 120, dtype=np.uint64))
 
 
+def test_lookup_prefix_equals_the_oracle_walk():
+    """tl_index_lookup_prefix over requests built from stored documents with
+    holes (blocks whose records were never stored), other tenants' prefixes,
+    empty and one-block requests: hits and handles equal the oracle's reuse
+    walk (the leading run of stored keys, Sec. 5)."""
+    c = _ctx(wl.TINY)
+    ns = T.tl_ns_digest(c)
+    B = c.block_bytes
+    rng = np.random.default_rng(11)
+    docs = [wl.tokens(16 * 40, s) for s in range(4)]
+    idx = T.tl_index_create(400)
+    oracle_index, h = {}, 0
+    for d in docs:
+        keys = ref.block_keys(ns, d.tobytes(), B)
+        stored = [k for i, k in enumerate(keys) if rng.random() > 0.08]  # holes
+        idx.put_many(np.frombuffer(b"".join(stored), np.uint8).reshape(-1, 32), range(h, h + len(stored)))
+        ref.index_put(oracle_index, stored, range(h, h + len(stored)))
+        h += len(stored)
+    reqs = []
+    for r in range(60):
+        d = docs[r % 4]
+        cut = int(rng.integers(0, 41)) * 16
+        tail = wl.tokens(int(rng.integers(0, 200)), 100 + r)
+        reqs.append(np.concatenate([d[:cut], tail]).astype(np.uint32))
+    reqs += [np.zeros(0, np.uint32), docs[0][:16].copy(), docs[1][:15].copy()]
+    keys = T.tl_block_keys_batch(c, reqs)
+    n_keys = np.array([k.shape[0] for k in keys], np.uint64)
+    off = np.concatenate([[0], np.cumsum(n_keys)[:-1]]).astype(np.uint64)
+    hits, handles = idx.lookup_prefix(np.concatenate(keys), off, n_keys)
+    total = 0
+    for r, q in enumerate(reqs):
+        okeys, ohits, ohandles = ref.chain_walk(ns, q.tobytes(), B, oracle_index)
+        assert [k.tobytes() for k in keys[r]] == okeys
+        assert int(hits[r]) == ohits, r
+        o = int(off[r])
+        assert [int(x) for x in handles[o:o + ohits]] == ohandles
+        if ohits < len(okeys):
+            assert handles[o + ohits] == np.uint64(2**64 - 1)
+        total += ohits
+    assert total > 100 and (hits < n_keys).sum() > 20  # both long reuse and early misses occur
+
+
 def test_save_load_argument_validation_enqueues_nothing():
     c = _ctx(wl.TINY)
     L = T.lib()
