@@ -272,6 +272,24 @@ int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_
             const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
             uint8_t* d_verdicts, void* d_workspace, size_t workspace_bytes);
 
+/* The same verified restore for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): no workspace argument. The per-block status words live in a
+ * library-held device array of TL_LOAD_STATIC_MAX_BLOCKS words on each GPU
+ * (4 MiB, held until the process ends; its address is looked up once per
+ * device, on the first call whose stream belongs to that device). The call
+ * allocates nothing. Every call on one GPU shares that GPU's array: calls
+ * that overlap on one GPU (on different streams without ordering) race and
+ * must not be issued; calls ordered on a stream are safe, since the first
+ * kernel of each call clears the words it uses. Same arguments, checks,
+ * verdicts and restored bytes as tl_load. TL_ERANGE (nothing enqueued) when
+ * n_blocks > TL_LOAD_STATIC_MAX_BLOCKS; TL_EDEVICE if the stream's device
+ * or the array's address cannot be found. */
+#define TL_LOAD_STATIC_MAX_BLOCKS (1u << 20)
+int tl_load_static(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_record_ptrs,
+                   const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
+                   uint8_t* d_verdicts);
+
 /* ---- a2: key -> record index (host) --------------------------------------
  * Open addressing over 32-byte keys, 64-bit handles. Readers may run
  * concurrently; writers need external exclusion. */

@@ -391,6 +391,21 @@ int tl_load(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_
                          d_verdicts, (uint32_t*)d_workspace);
 }
 
+int tl_load_static(const tl_ctx* ctx, void* stream, size_t n_blocks, const uint64_t* d_record_ptrs,
+                   const uint64_t* d_record_lens, const tl_blocks* blocks, const tl_cache* dst,
+                   uint8_t* d_verdicts) {
+  if (!ctx) return TL_EINVAL;
+  if (n_blocks == 0) return TL_OK;
+  int r = check_cache(ctx, dst);
+  if (r) return r;
+  if ((r = check_blocks(ctx, n_blocks, blocks, false))) return r;
+  if (!d_record_ptrs || !d_record_lens || !d_verdicts) return TL_EINVAL;
+  if (((uintptr_t)d_record_ptrs | (uintptr_t)d_record_lens) & 7) return TL_EINVAL;
+  if (n_blocks > TL_LOAD_STATIC_MAX_BLOCKS) return TL_ERANGE;
+  return tl::launch_load_static(ctx, stream, n_blocks, d_record_ptrs, d_record_lens, blocks, dst,
+                                d_verdicts);
+}
+
 // ---- device index and key chains ---------------------------------------------
 static bool dindex_capacity_ok(size_t cap) {
   return cap >= 2 && cap <= (size_t(1) << 31) && (cap & (cap - 1)) == 0;

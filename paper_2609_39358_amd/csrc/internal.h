@@ -84,6 +84,10 @@ int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
 int launch_load(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,
                 const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
                 uint8_t* d_verdicts, uint32_t* d_ws);
+// tl_load with the library's per-device status array (kernels.hip).
+int launch_load_static(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,
+                       const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
+                       uint8_t* d_verdicts);
 // Device index and key chains; chain.hip.
 int launch_dindex_clear(void* mem, uint64_t capacity, void* stream);
 int launch_dindex_put(void* mem, uint64_t capacity, void* stream, size_t n, const uint8_t* d_keys,

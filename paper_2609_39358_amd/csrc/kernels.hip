@@ -858,7 +858,52 @@ uint32_t seg_grid(uint32_t total) {
 
 }  // namespace
 
+// Status words of tl_load_static: one array per device, shared by every call
+// on that device, for callers that cannot allocate a workspace. In host code
+// `scratch` names a host-side stand-in, never the device array: its device
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint32_t scratch[TL_LOAD_STATIC_MAX_BLOCKS];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint32_t* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device that runs `stream`, looked up
+// with that device current on the first call for it.
+int scratch_for(void* stream, uint32_t** out) {
+  int dev = -1;
+  if (hipStreamGetDevice((hipStream_t)stream, &dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return TL_EDEVICE;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return TL_EDEVICE;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return TL_EDEVICE;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p) return TL_EDEVICE;
+    g_scratch_ptr[dev] = (uint32_t*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return TL_OK;
+}
+
+}  // namespace
+
 namespace tl {
+
+int launch_load_static(const tl_ctx* ctx, void* stream, size_t n, const uint64_t* d_rec,
+                       const uint64_t* d_len, const tl_blocks* blk, const tl_cache* dst,
+                       uint8_t* d_verdicts) {
+  if (n > TL_LOAD_STATIC_MAX_BLOCKS) return TL_ERANGE;
+  uint32_t* ws = nullptr;
+  const int r = scratch_for(stream, &ws);
+  if (r) return r;
+  return launch_load(ctx, stream, n, d_rec, d_len, blk, dst, d_verdicts, ws);
+}
 
 int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                        const tl_blocks* blk, const uint64_t* d_rec, uint32_t layer_begin,

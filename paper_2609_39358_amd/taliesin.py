@@ -91,6 +91,7 @@ def _load():
         "tl_save_seal": (c.c_int, [P, P, c.c_size_t, c.c_int64, c.POINTER(tl_blocks), P, P]),
         "tl_load": (c.c_int, [P, P, c.c_size_t, P, P, c.POINTER(tl_blocks), c.POINTER(tl_cache),
                               P, P, c.c_size_t]),
+        "tl_load_static": (c.c_int, [P, P, c.c_size_t, P, P, c.POINTER(tl_blocks), c.POINTER(tl_cache), P]),
         "tl_index_create": (P, [c.c_size_t]),
         "tl_index_destroy": (None, [P]),
         "tl_index_put": (c.c_int, [P, P, c.c_uint64]),
@@ -133,7 +134,8 @@ def _load():
 _lib = _load()
 EXPORTED = (
     "tl_ctx_create", "tl_ctx_destroy", "tl_ctx_geometry", "tl_ns_digest", "tl_workspace_bytes",
-    "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_save_layers", "tl_save_seal", "tl_load", "tl_index_create",
+    "tl_block_keys", "tl_block_keys_batch", "tl_save", "tl_save_layers", "tl_save_seal", "tl_load",
+    "tl_load_static", "tl_index_create",
     "tl_index_destroy", "tl_index_put", "tl_index_get_batch", "tl_index_size", "tl_index_lookup_prefix",
     "tl_dindex_bytes", "tl_dindex_create", "tl_dindex_destroy", "tl_dindex_workspace_bytes",
     "tl_dindex_put", "tl_dindex_get", "tl_dindex_stats", "tl_chain_lookup", "tl_chain_stage",
@@ -377,6 +379,23 @@ def tl_load(ctx: Ctx, stream, n_blocks: int, d_record_ptrs, d_record_lens, block
     _check(_lib.tl_load(ctx.handle, _stream(stream), n_blocks, _addr(d_record_ptrs),
                         _addr(d_record_lens), ctypes.byref(blocks), ctypes.byref(dst),
                         _addr(d_verdicts), _addr(d_workspace), workspace_bytes), "tl_load")
+
+
+LOAD_STATIC_MAX_BLOCKS = 1 << 20
+
+
+def tl_load_static(ctx: Ctx, stream, n_blocks: int, d_record_ptrs, d_record_lens, blocks: tl_blocks,
+                   dst: tl_cache, d_verdicts):
+    """tl_load without a workspace: the library's per-device status array
+    (callers that cannot allocate; calls that overlap on one GPU race)."""
+    _check_blocks(ctx, n_blocks, blocks)
+    _check_cache(ctx, dst)
+    _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
+    _fits(d_record_lens, 8 * n_blocks, "record lengths")
+    _fits(d_verdicts, n_blocks, "verdicts")
+    _check(_lib.tl_load_static(ctx.handle, _stream(stream), n_blocks, _addr(d_record_ptrs),
+                               _addr(d_record_lens), ctypes.byref(blocks), ctypes.byref(dst),
+                               _addr(d_verdicts)), "tl_load_static")
 
 
 # ------------------------------------------------------------------ index

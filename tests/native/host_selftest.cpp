@@ -19,6 +19,8 @@ int launch_save_seal(const tl_ctx*, void*, size_t, int64_t, const tl_blocks*, co
                      uint8_t*) { return TL_EDEVICE; }
 int launch_load(const tl_ctx*, void*, size_t, const uint64_t*, const uint64_t*, const tl_blocks*,
                 const tl_cache*, uint8_t*, uint32_t*) { return TL_EDEVICE; }
+int launch_load_static(const tl_ctx*, void*, size_t, const uint64_t*, const uint64_t*, const tl_blocks*,
+                       const tl_cache*, uint8_t*) { return TL_EDEVICE; }
 int launch_dindex_clear(void*, uint64_t, void*) { return TL_EDEVICE; }
 int launch_dindex_put(void*, uint64_t, void*, size_t, const uint8_t*, const uint64_t*, uint8_t*,
                       uint32_t*) { return TL_EDEVICE; }
@@ -160,6 +162,13 @@ int main() {
   EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &cache, verd, ws, sizeof ws) == TL_EDEVICE);
   EXPECT(tl_load(c, nullptr, 1, rp, rl, &blk, &cache, verd, ws, 3) == TL_ERANGE);
   EXPECT(tl_save(c, nullptr, 1, &cache, &blk, rp, nullptr) == TL_EDEVICE);
+  // the allocation-free load: the same checks, no workspace, a block limit
+  EXPECT(tl_load_static(c, nullptr, 1, rp, rl, &blk, &cache, verd) == TL_EDEVICE);
+  EXPECT(tl_load_static(c, nullptr, 0, nullptr, nullptr, nullptr, nullptr, nullptr) == TL_OK);
+  EXPECT(tl_load_static(c, nullptr, 1, rp, rl, &blk, &cache, nullptr) == TL_EINVAL);
+  EXPECT(tl_load_static(c, nullptr, 1, nullptr, rl, &blk, &cache, verd) == TL_EINVAL);
+  EXPECT(tl_load_static(nullptr, nullptr, 1, rp, rl, &blk, &cache, verd) == TL_EINVAL);
+  EXPECT(tl_load_static(c, nullptr, TL_LOAD_STATIC_MAX_BLOCKS + 1, rp, rl, &blk, &cache, verd) == TL_ERANGE);
   tl_blocks no_tok = blk;
   no_tok.d_tokens = nullptr;
   EXPECT(tl_save(c, nullptr, 1, &cache, &no_tok, rp, nullptr) == TL_EINVAL);
