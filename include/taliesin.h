@@ -230,15 +230,19 @@ int tl_save(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* sr
  * and root, and d_status as tl_save does; n_pages is the source cache's page
  * count, used to report TL_BADARG. A record is valid only after its seal, and
  * only if every layer range was saved before the seal (stream order). tl_save
- * is exactly tl_save_layers(0, n_layers, 0) followed by tl_save_seal.
- * flags: 0, or TL_SAVE_SHARED for a save that runs while kernels of other
- * streams (the prefill of later layers) keep the device busy: it then uses a
- * kernel with a smaller footprint (two wavefronts per SIMD), which keeps
- * pace with such a prefill where the default kernel falls behind it and
- * finishes after it. Without other work on the device it is about as fast
- * as flags 0. The bytes written do not depend on flags. TL_EINVAL if
- * layer_begin >= layer_end, layer_end > n_layers or flags has other bits. */
+ * is exactly tl_save_layers(0, n_layers, TL_SAVE_EXCLUSIVE) followed by
+ * tl_save_seal.
+ * flags: 0 or TL_SAVE_SHARED (the same): a kernel with a small footprint
+ * (two wavefronts per SIMD) for saves that run while kernels of other
+ * streams (the prefill of later layers) keep the device busy; it keeps pace
+ * with such a prefill where a kernel holding a whole SIMD per wavefront
+ * falls behind it, and alone it is about as fast. TL_SAVE_EXCLUSIVE: that
+ * other kernel (a whole 64 KiB chunk in flight per wavefront), the one
+ * tl_save uses, for a save that has the device to itself. The bytes written
+ * do not depend on flags. TL_EINVAL if layer_begin >= layer_end, layer_end >
+ * n_layers, both flags are given or flags has other bits. */
 #define TL_SAVE_SHARED 1
+#define TL_SAVE_EXCLUSIVE 2
 int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_cache* src,
                    const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
                    uint32_t layer_end, uint32_t flags);

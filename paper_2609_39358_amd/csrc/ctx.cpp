@@ -354,7 +354,10 @@ int tl_save_layers(const tl_ctx* ctx, void* stream, size_t n_blocks, const tl_ca
                    const tl_blocks* blocks, const uint64_t* d_record_ptrs, uint32_t layer_begin,
                    uint32_t layer_end, uint32_t flags) {
   if (!ctx) return TL_EINVAL;
-  if (layer_begin >= layer_end || layer_end > ctx->L || (flags & ~TL_SAVE_SHARED)) return TL_EINVAL;
+  if (layer_begin >= layer_end || layer_end > ctx->L) return TL_EINVAL;
+  if ((flags & ~uint32_t(TL_SAVE_SHARED | TL_SAVE_EXCLUSIVE)) ||
+      (flags & (TL_SAVE_SHARED | TL_SAVE_EXCLUSIVE)) == (TL_SAVE_SHARED | TL_SAVE_EXCLUSIVE))
+    return TL_EINVAL;
   if (n_blocks == 0) return TL_OK;
   int r = check_cache(ctx, src);
   if (r) return r;

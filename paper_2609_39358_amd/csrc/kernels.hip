@@ -477,9 +477,10 @@ __global__ __launch_bounds__(64 * kSegWaves) void k_save_seg(SegArgs a) {
   save_chunks<TL_SAVE_BATCH_ROWS, TL_SAVE_PREFETCH>(a);
 }
 
-// Beside other kernels: half the chunk per batch and at most 256 registers
-// per lane (two wavefronts per SIMD, two workgroups per compute unit). Alone
-// it saves as fast as k_save_seg; while another stream keeps the device busy
+// Beside other kernels (tl_save_layers' default): half the chunk per batch
+// and at most 256 registers per lane (two wavefronts per SIMD, two
+// workgroups per compute unit). Alone it saves as fast as k_save_seg; while
+// another stream keeps the device busy
 // (a prefill of persistent bf16 GEMMs, one 512-register wavefront per SIMD on
 // every compute unit), its per-layer saves finish within the GEMMs they
 // overlap where k_save_seg's fall behind them.
@@ -914,10 +915,10 @@ int launch_save_layers(const tl_ctx* ctx, void* stream, size_t n, const tl_cache
   a.order = TL_SAVE_ORDER;
   (void)hipGetLastError();
   timed(TL_KERNEL_SAVE_SEG, s, [&] {
-    if (flags & TL_SAVE_SHARED)
-      hipLaunchKernelGGL(k_save_seg_shared, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
-    else
+    if (flags & TL_SAVE_EXCLUSIVE)
       hipLaunchKernelGGL(k_save_seg, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
+    else
+      hipLaunchKernelGGL(k_save_seg_shared, dim3(seg_grid(a.total)), dim3(64 * kSegWaves), 0, s, a);
   });
   return launched();
 }
@@ -936,7 +937,7 @@ int launch_save_seal(const tl_ctx* ctx, void* stream, size_t n, int64_t n_pages,
 
 int launch_save(const tl_ctx* ctx, void* stream, size_t n, const tl_cache* src,
                 const tl_blocks* blk, const uint64_t* d_rec, uint8_t* d_status) {
-  int r = launch_save_layers(ctx, stream, n, src, blk, d_rec, 0, ctx->geo.n_layers, 0);
+  int r = launch_save_layers(ctx, stream, n, src, blk, d_rec, 0, ctx->geo.n_layers, TL_SAVE_EXCLUSIVE);
   if (r) return r;
   return launch_save_seal(ctx, stream, n, src->n_pages, blk, d_rec, d_status);
 }

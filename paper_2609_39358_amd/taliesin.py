@@ -148,7 +148,7 @@ KERNELS = {"save_seg": 0, "save_meta": 1, "load_init": 2, "load_main": 3, "load_
 TL_INDEX_STORED, TL_INDEX_FULL, TL_INDEX_TAG_CLASH = 0x01, 0x20, 0x21
 TL_CHAIN_ALL_KEYS, TL_CHAIN_TAIL = 1, 2
 TL_KEYS_TAIL = 1
-TL_SAVE_SHARED = 1
+TL_SAVE_SHARED, TL_SAVE_EXCLUSIVE = 1, 2
 MISS = 2**64 - 1
 
 
@@ -349,13 +349,15 @@ def tl_save(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d
 
 
 def tl_save_layers(ctx: Ctx, stream, n_blocks: int, src: tl_cache, blocks: tl_blocks, d_record_ptrs,
-                   layer_begin: int, layer_end: int, shared: bool = False):
+                   layer_begin: int, layer_end: int, shared: Optional[bool] = None):
+    """shared: None (the library's default, the small-footprint kernel), True
+    (TL_SAVE_SHARED, the same) or False (TL_SAVE_EXCLUSIVE)."""
     _check_blocks(ctx, n_blocks, blocks)
     _check_cache(ctx, src)
     _fits(d_record_ptrs, 8 * n_blocks, "record pointers")
+    flags = 0 if shared is None else TL_SAVE_SHARED if shared else TL_SAVE_EXCLUSIVE
     _check(_lib.tl_save_layers(ctx.handle, _stream(stream), n_blocks, ctypes.byref(src),
-                               ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end,
-                               TL_SAVE_SHARED if shared else 0),
+                               ctypes.byref(blocks), _addr(d_record_ptrs), layer_begin, layer_end, flags),
            "tl_save_layers")
 
 

@@ -173,7 +173,9 @@ int main() {
   no_tok.d_tokens = nullptr;
   EXPECT(tl_save(c, nullptr, 1, &cache, &no_tok, rp, nullptr) == TL_EINVAL);
   EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 1, 1, 0) == TL_EINVAL);
-  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 0, 1, 2) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 0, 1, 4) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 0, 1, 3) == TL_EINVAL);
+  EXPECT(tl_save_layers(c, nullptr, 1, &cache, &blk, rp, 0, 1, TL_SAVE_EXCLUSIVE) == TL_EDEVICE);
   EXPECT(tl_save_seal(c, nullptr, 1, -5, &blk, rp, nullptr) == TL_EINVAL);
   tl_cache narrow = cache;
   narrow.page_stride = 4096;

@@ -257,8 +257,10 @@ def test_save_load_argument_validation_enqueues_nothing():
     # layer-wise save: a non-empty range inside [0, n_layers); the seal needs tokens
     sl = lambda a, b, n=64, f=0: L.tl_save_layers(c.handle, None, n, P(good_cache), P(good_blk), 0x70000, a, b, f)
     assert sl(0, 0) == T.TL_EINVAL and sl(3, 2) == T.TL_EINVAL and sl(0, 5) == T.TL_EINVAL
-    assert sl(0, 4, f=2) == T.TL_EINVAL and sl(0, 4, f=0x80000000) == T.TL_EINVAL  # unknown flags
+    assert sl(0, 4, f=4) == T.TL_EINVAL and sl(0, 4, f=0x80000000) == T.TL_EINVAL  # unknown flags
+    assert sl(0, 4, f=T.TL_SAVE_SHARED | T.TL_SAVE_EXCLUSIVE) == T.TL_EINVAL  # both kernels
     assert sl(0, 4, n=0) == T.TL_OK and sl(0, 4, n=0, f=T.TL_SAVE_SHARED) == T.TL_OK
+    assert sl(0, 4, n=0, f=T.TL_SAVE_EXCLUSIVE) == T.TL_OK
     seal = lambda blk, n_pages=128: L.tl_save_seal(c.handle, None, 64, n_pages, P(blk), 0x70000, None)
     assert seal(T.make_blocks(0x30000, 0x40000, None, 0x60000)) == T.TL_EINVAL
     assert seal(good_blk, n_pages=-1) == T.TL_EINVAL
