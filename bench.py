@@ -62,8 +62,8 @@ def layerwise_save_leg(T, ctx, n, src, blocks, store, d_status, step_bytes, whol
         stream; the save of layer l waits for layer l's GEMM. The stand-in
         only occupies the GPU; it does not write the pages. Reports the
         stand-in alone, the stand-in with the overlapped save, and how much
-        save time remains exposed, for both save kernels (flags 0 and
-        TL_SAVE_SHARED)."""
+        save time remains exposed, for both save kernels (the default,
+        TL_SAVE_SHARED, and TL_SAVE_EXCLUSIVE)."""
     import torch
 
     L = src.n_layers
@@ -141,7 +141,7 @@ def layerwise_save_leg(T, ctx, n, src, blocks, store, d_status, step_bytes, whol
             o_ms = timed(lambda: overlapped(shared))
             assert (d_status == T.ACCEPT).all().item() and torch.equal(store.buf[:, 144:152], roots)
             exposed = max(o_ms - p_ms, 0.0)
-            name = "shared" if shared else "default"
+            name = "shared" if shared else "exclusive"
             modes[name] = {"prefill_with_overlapped_save_ms": o_ms, "save_exposed_ms": exposed,
                            "save_hidden_frac": 1.0 - exposed / alone[shared]}
             log("layer-wise save (%s kernel) beside %d-token GEMMs: stand-in prefill %.2f ms, with the "
@@ -153,7 +153,7 @@ def layerwise_save_leg(T, ctx, n, src, blocks, store, d_status, step_bytes, whol
         del ga, gb, gc
     out = {"layers": L, "blocks": n, "whole_save_ms": whole_ms, "per_layer_calls_ms": lw_ms,
            "per_layer_GBps": step_bytes / (lw_ms * 1e-3) / 1e9,
-           "per_layer_alone_ms": {"default": alone[False], "shared": alone[True]}, "beside_prefill": runs}
+           "per_layer_alone_ms": {"exclusive": alone[False], "shared": alone[True]}, "beside_prefill": runs}
     return out
 
 
@@ -227,17 +227,22 @@ def multi_request_leg(T, PagedCache, wl, dev):
     torch.cuda.synchronize()
     piped = time.perf_counter() - t0
     assert sum(int((r.verdicts != T.ACCEPT).sum().item()) for r in results) == rejected
+    # headline: the batches back to back, as a server issues them (each
+    # batch's host keys and lookups run while the previous batch restores)
     out = {"requests": len(w.requests), "prompt_tokens": int(sum(q.n_tokens for q in w.requests)),
            "stored_records": n_st, "damaged_records": len(w.corrupt_flip) + len(w.corrupt_trunc),
            "batches": len(batches), "blocks_restored": blocks, "blocks_rejected": rejected,
-           "ms": total * 1e3, "keys_lookup_ms": host_s * 1e3, "GBps": moved / total / 1e9,
-           "tokens_avoided_per_s": (blocks - rejected) * P / total,
-           "back_to_back": {"ms": piped * 1e3, "GBps": moved / piped / 1e9,
-                            "tokens_avoided_per_s": (blocks - rejected) * P / piped},
-           "per_batch": per}
-    log("multi-request: %d batches, %d blocks (%d rejected) in %.1f ms, %.0f GB/s incl. keys+lookup %.1f ms; "
-        "back to back %.1f ms, %.0f GB/s" % (len(batches), blocks, rejected, total * 1e3, out["GBps"], host_s * 1e3,
-                                             piped * 1e3, out["back_to_back"]["GBps"]))
+           "how": "host keys (tl_block_keys_batch) + tl_index_lookup_prefix + upload + tl_load per batch, "
+                  "batches back to back",
+           "ms": piped * 1e3, "GBps": moved / piped / 1e9, "hbm_frac": moved / piped / 1e9 / HBM_PEAK_GBPS,
+           "tokens_avoided_per_s": (blocks - rejected) * P / piped,
+           "serialized": {"how": "each batch synchronised before the next one starts: keys and lookups on the "
+                                 "critical path",
+                          "ms": total * 1e3, "keys_lookup_ms": host_s * 1e3, "GBps": moved / total / 1e9,
+                          "tokens_avoided_per_s": (blocks - rejected) * P / total, "per_batch": per}}
+    log("multi-request: %d batches, %d blocks (%d rejected) back to back in %.1f ms, %.0f GB/s; one at a time "
+        "%.1f ms, %.0f GB/s incl. keys+lookup %.1f ms" % (len(batches), blocks, rejected, piped * 1e3, out["GBps"],
+                                                          total * 1e3, moved / total / 1e9, host_s * 1e3))
     # the same store and pool through the device pipeline: token ids already in
     # HBM, keys and lookup by the verified parallel walk, no host step per batch
     dstore = pipeline.DeviceStore(ctx, n_st, dev, records=store.records)
@@ -303,6 +308,47 @@ def _oracle_slice(task):
         vs = ref.restore(lay, ns, recs, keys, np.arange(lo, hi), toks, np.arange(m, dtype=np.int32)[None, :], hk, hv)
         del arr, recs
         return vs, time.perf_counter() - t0, time.process_time() - c0
+    finally:
+        shm.close()
+
+
+def _oracle_save_run(arr, lo, hi, lay_args, ns, keys, toks):
+    """The oracle's save of blocks [lo, hi) of the sample in `arr` ([m,
+    record bytes]), whose source pages are read from the records (a record's
+    payload holds its pages verbatim, slab s = 2 * layer + K|V). Returns
+    (records equal the sample's, seconds of the save, CPU seconds)."""
+    import numpy as np
+
+    from oracle import taliesin_ref as ref
+
+    lay = ref.Layout(*lay_args)
+    po, S = lay.payload_offset, lay.slab_bytes
+    hk = [arr[:, po + 2 * l * S: po + (2 * l + 1) * S] for l in range(lay.n_layers)]
+    hv = [arr[:, po + (2 * l + 1) * S: po + (2 * l + 2) * S] for l in range(lay.n_layers)]
+    t0, c0 = time.perf_counter(), time.process_time()
+    recs, st = ref.save(lay, ns, hk, hv, np.arange(lo, hi, dtype=np.int32)[None, :], keys,
+                        np.arange(lo, hi), toks, n_pages=arr.shape[0])
+    dt, cpu = time.perf_counter() - t0, time.process_time() - c0
+    ok = st == [ref.ACCEPT] * (hi - lo) and all(arr[lo + i].tobytes() == r for i, r in enumerate(recs))
+    return ok, dt, cpu
+
+
+def _oracle_save_slice(task):
+    """One worker of the multi-core CPU baseline of the save (a process forked
+    before the parent touched the GPU; uses no GPU): _oracle_save_run on the
+    sample held in shared memory."""
+    from multiprocessing import resource_tracker, shared_memory
+
+    import numpy as np
+
+    shm_name, m, lo, hi, rb, lay_args, ns, keys, toks = task
+    shm = shared_memory.SharedMemory(name=shm_name)
+    resource_tracker.unregister(shm._name, "shared_memory")  # the parent unlinks it
+    try:
+        arr = np.ndarray((m, rb), np.uint8, buffer=shm.buf)
+        out = _oracle_save_run(arr, lo, hi, lay_args, ns, keys, toks)
+        del arr
+        return out
     finally:
         shm.close()
 
@@ -478,7 +524,8 @@ def main():
     ap.add_argument("--save-steps", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=1536)
-    ap.add_argument("--cpu-workers", type=int, default=64)
+    ap.add_argument("--cpu-workers", type=int, default=16)
+    ap.add_argument("--cpu-save-single-blocks", type=int, default=256)
     ap.add_argument("--no-copy-ceiling", action="store_true")
     ap.add_argument("--no-host-tier", action="store_true")
     ap.add_argument("--no-paper-blocks", action="store_true")
@@ -897,11 +944,24 @@ def main():
             t0 = time.perf_counter()
             res = pool.map(_oracle_slice, tasks)
             wall = time.perf_counter() - t0
+            # the oracle's save of the same sample on the same workers: pages
+            # read from the records' payloads, records written and compared
+            # with the GPU's (outside the timed call)
+            stasks = [(shm.name, m, t[2], t[3], rb, lay_args, ns, t[6], t[7]) for t in tasks]
+            t0 = time.perf_counter()
+            sres = pool.map(_oracle_save_slice, stasks)
+            swall = time.perf_counter() - t0
+            # one process, a smaller part of the sample (the oracle's save is
+            # the slowest of its steps)
+            m1 = min(args.cpu_save_single_blocks, m)
+            sres1 = _oracle_save_run(arr, 0, m1, lay_args, ns, [k.tobytes() for k in keys0[:m1]],
+                                     tokens[:m1 * P].reshape(m1, P))
             del arr
         finally:
             shm.close()
             shm.unlink()
         assert all(v == ref.ACCEPT for vs, _, _ in res for v in vs)
+        assert all(ok for ok, _, _ in sres) and sres1[0], "the oracle's save differs from the GPU's records"
         cpu_all = sum(c for _, _, c in res)
         cpu = {"value": m * (rb + payload) / wall / 1e9, "unit": "GB/s", "cores": len(tasks), "kind": "oracle",
                "sample": "verify+restore of %d of %d blocks (%.2f GB of records) on the host, split over %d "
@@ -909,7 +969,27 @@ def main():
                          "records out of shared memory" % (m, n, m * rb / 1e9, len(tasks)),
                "seconds": wall, "cpu_seconds": cpu_all, "tokens_avoided_per_s": m * P / wall,
                "single_process": single}
-        log("cpu oracle, %d processes: %.2f GB/s over %.2f s (%.1f CPU s)" % (len(tasks), cpu["value"], wall, cpu_all))
+        save_slowest = max(dt for _, dt, _ in sres)
+        cpu["save"] = {
+            "value": m * (rb + payload) / swall / 1e9, "unit": "GB/s", "cores": len(stasks),
+            "sample": "save of the same %d blocks (pages read from the records' payloads, records built by the "
+                      "oracle and compared with the GPU's) on the same %d worker processes" % (m, len(stasks)),
+            "seconds": swall, "slowest_worker_save_seconds": save_slowest,
+            "cpu_seconds": sum(c for _, _, c in sres),
+            "single_process": {"value": m1 * (rb + payload) / sres1[1] / 1e9, "unit": "GB/s", "cores": 1,
+                               "blocks": m1, "seconds": sres1[1]}}
+        log("cpu oracle save: %d processes %.2f GB/s over %.2f s; one process %.2f GB/s over %.1f s (%d blocks)"
+            % (len(stasks), cpu["save"]["value"], swall, cpu["save"]["single_process"]["value"], sres1[1], m1))
+        # the oracle's key chain over the whole corpus, one core
+        t0 = time.perf_counter()
+        okeys = ref.block_keys(ns, tokens.tobytes(), 4 * P)
+        kms = (time.perf_counter() - t0) * 1e3
+        assert len(okeys) == n and all(okeys[i] == keys0[i].tobytes() for i in range(n))
+        cpu["keys"] = {"ms": kms, "blocks": n, "tokens": cfg.n_tokens, "cores": 1,
+                       "how": "the oracle's chained SHA-256 (hashlib) over the %d tokens; same unit as host_ms.keys_ms"
+                              % cfg.n_tokens}
+        log("cpu oracle, %d processes: %.2f GB/s over %.2f s (%.1f CPU s); oracle keys %.1f ms"
+            % (len(tasks), cpu["value"], wall, cpu_all, kms))
     if pool is not None:
         pool.terminate()
         pool.join()
