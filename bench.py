@@ -947,7 +947,7 @@ def main():
             # the oracle's save of the same sample on the same workers: pages
             # read from the records' payloads, records written and compared
             # with the GPU's (outside the timed call)
-            stasks = [(shm.name, m, t[2], t[3], rb, lay_args, ns, t[6], t[7]) for t in tasks]
+            stasks = [(shm.name, m, t[1], t[2], rb, lay_args, ns, t[6], t[7]) for t in tasks]
             t0 = time.perf_counter()
             sres = pool.map(_oracle_save_slice, stasks)
             swall = time.perf_counter() - t0
