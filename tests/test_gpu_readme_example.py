@@ -39,9 +39,8 @@ def test_readme_usage_example():
 
     # a later request: restore its stored leading blocks into pages of its own
     rkeys = T.tl_block_keys(ctx, request)
-    slots = index.get_batch(rkeys)  # UINT64_MAX where absent
-    miss = slots == np.iinfo(np.uint64).max
-    hit = int(miss.argmax()) if miss.any() else len(slots)  # reuse stops at the first miss
+    hits, slots = index.lookup_prefix(rkeys, [0], [len(rkeys)])  # reuse stops at the first block not stored
+    hit = int(hits[0])
     new_pages = np.arange(64, 64 + hit, dtype=np.int32)  # pages the engine gives the request
     ptrs = store.ptrs[torch.from_numpy(slots[:hit].astype(np.int64)).cuda()]
     lens = store.lens[:hit]
