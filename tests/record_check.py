@@ -82,6 +82,22 @@ def _work(task):
         sshm.close()
 
 
+def _digest_work(task):
+    """The oracle's chunk digests of the chunks [c0, c1) of the payload bytes
+    staged in a shared segment (chunk c at byte offset c * chunk_len)."""
+    from oracle import taliesin_ref as ref
+
+    name, nbytes, chunk_len, c0, c1 = task
+    shm = _attach(name)
+    try:
+        buf = np.ndarray((nbytes,), np.uint8, buffer=shm.buf)
+        out = [ref.chunk_digest(buf[c * chunk_len:(c + 1) * chunk_len]) for c in range(c0, c1)]
+        del buf
+        return c0, out
+    finally:
+        shm.close()
+
+
 def lay_args(lay) -> Tuple:
     """The oracle Layout's constructor arguments (what a worker rebuilds it from)."""
     return (lay.n_layers, lay.n_kv_heads, lay.head_dim, lay.dtype, lay.page_tokens, lay.layer_window,
@@ -100,6 +116,32 @@ class RecordChecker:
     def close(self):
         self.pool.terminate()
         self.pool.join()
+
+    def chunk_digests(self, payload, chunk_len: int, batch_bytes: int = 1 << 30) -> np.ndarray:
+        """The oracle's digest (`ref.chunk_digest`) of every chunk_len bytes of
+        `payload` (a flat torch uint8 tensor, device or host, whose length is
+        a multiple of chunk_len), computed on the workers in batches."""
+        import torch
+
+        n = payload.numel() // chunk_len
+        assert n * chunk_len == payload.numel()
+        per = max(1, batch_bytes // chunk_len)
+        out = np.zeros(n, np.uint64)
+        shm = shared_memory.SharedMemory(create=True, size=per * chunk_len)
+        try:
+            for lo in range(0, n, per):
+                hi = min(n, lo + per)
+                nb = (hi - lo) * chunk_len
+                torch.from_numpy(np.ndarray((nb,), np.uint8, buffer=shm.buf)).copy_(
+                    payload[lo * chunk_len:hi * chunk_len])
+                cuts = np.linspace(0, hi - lo, min(self.n_workers, hi - lo) + 1).astype(int)
+                tasks = [(shm.name, nb, chunk_len, int(a), int(b)) for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
+                for c0, ds in self.pool.map(_digest_work, tasks):
+                    out[lo + c0:lo + c0 + len(ds)] = ds
+        finally:
+            shm.close()
+            shm.unlink()
+        return out
 
     def check(self, lay_args: Tuple, ns: bytes, src_k, src_v, src_tables: np.ndarray, records,
               keys: Sequence[bytes], bidx: Sequence[int], tokens: Optional[np.ndarray],

@@ -145,12 +145,42 @@ def test_hybrid_full_scale(record_checker):
                 assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
 
 
-def test_paper_sized_blocks_full_scale():
+def check_records_in_full(c: Case, store: RecordStore, t_src, n_tok, checker):
+    """Every record equals the oracle's save, built in three parts that
+    together are `ref.make_record`: the payload holds the source pages in
+    the oracle's slab order (slab s = (2 * layer + K|V) * ppb + j; zeros for
+    pages a partial block leaves out), compared on the device; every chunk
+    digest is the oracle's `chunk_digest` of its payload bytes, computed by
+    the workers; the metadata is `ref.make_meta` of those digests."""
+    lay = c.lay
+    L, ppb, po, S = c.geom.n_layers, lay.pages_per_block, lay.payload_offset, lay.slab_bytes
+    clen = min(S, ref.CHUNK_BYTES)
+    n = store.n
+    for b in range(n):
+        t = lay.block_tokens if n_tok is None else int(n_tok[b])
+        for l in range(L):
+            tt = np.asarray(t_src[c.geom.group(l)][b * ppb:(b + 1) * ppb])
+            used = np.nonzero(tt >= 0)[0]
+            idx = torch.from_numpy(tt[used].astype(np.int64)).to(DEV)
+            for kv, src in ((0, c.src.k), (1, c.src.v)):
+                s0 = (2 * l + kv) * ppb
+                body = store.buf[b, po + s0 * S: po + (s0 + ppb) * S].view(ppb, S)
+                want = torch.zeros((ppb, S), dtype=torch.uint8, device=DEV)
+                want[torch.from_numpy(used).to(DEV)] = src[l].index_select(0, idx)[:, :S]
+                assert torch.equal(body, want), (b, l, kv)
+        dig = checker.chunk_digests(store.buf[b, po:], clen)
+        meta = ref.make_meta(lay, c.ns, c.keys[b].tobytes(), int(c.bidx[b]), c.tokens[b][:t], [int(x) for x in dig])
+        assert store.buf[b, :po].cpu().numpy().tobytes() == meta, b
+    log("every record checked against the oracle: %d of %.2f GB" % (n, lay.record_bytes / 1e9))
+
+
+def test_paper_sized_blocks_full_scale(record_checker):
     """The corpus as the paper stores it: blocks of ~8,800 tokens (11 blocks
     for the corpus), here 550 pages of 16 tokens per block, one 4.3 GB record
-    per block. Every block is checked by verdicts and the permutation-copy
-    property; the oracle recomputes the metadata of every record and the
-    digests of 256 sampled chunks from the record bytes."""
+    per block. Every record equals the oracle's save in full (payload,
+    66,000 chunk digests, metadata); damaged records get the oracle's
+    verdicts; every accepted block is restored as the permutation copy of
+    its pages, every rejected one zero-filled."""
     base = wl.PAPER_CORPUS.geom
     geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
     n = 97000 // geom.block_tokens
@@ -165,27 +195,23 @@ def test_paper_sized_blocks_full_scale():
     c.make_src()
     store, st = c.save()
     assert (st == ref.ACCEPT).all()
-    po, S, cps = lay.payload_offset, lay.slab_bytes, lay.chunks_per_slab
-    r = np.random.default_rng(3)
-    for b in range(n):
-        meta = store.buf[b, :po].cpu().numpy().tobytes()
-        assert meta[:256] == (lambda h: h[:144] + meta[144:152] + h[152:])(
-            ref.header_fields(lay, c.ns, c.keys[b].tobytes(), b))
-        assert int.from_bytes(meta[144:152], "little") == ref.root_digest(meta)
-        t0 = 256 + 8 * lay.n_segments
-        assert meta[t0:t0 + 4 * lay.block_tokens] == c.tokens[b].tobytes() and not any(meta[lay.meta_end:])
-        for s in r.choice(lay.n_slabs, 24, replace=False):
-            l, kv, j = (s // 550) >> 1, (s // 550) & 1, s % 550
-            page = int(c.t_src[0][b * 550 + j])
-            src = (c.src.k if kv == 0 else c.src.v)[l][page].cpu().numpy().tobytes()
-            body = store.buf[b, po + s * S: po + (s + 1) * S].cpu().numpy().tobytes()
-            assert body == src, (b, s)
-            for k in range(cps):
-                stored = int.from_bytes(meta[256 + 8 * (s * cps + k): 264 + 8 * (s * cps + k)], "little")
-                assert stored == ref.chunk_digest(body[k * 65536:(k + 1) * 65536]), (b, s, k)
-    # damage: one metadata bit in block 3, one payload bit in block 7
+    check_records_in_full(c, store, c.t_src, None, record_checker)
+    po = lay.payload_offset
+    # damage: one metadata bit in block 3, one payload bit in block 7; the
+    # oracle's checks on the damaged bytes: the root over the metadata, and
+    # the digest of the one chunk the flip lands in
+    meta3 = bytearray(store.buf[3, :po].cpu().numpy().tobytes())
+    meta3[1000] ^= 2
+    assert ref.check_meta(lay, c.ns, bytes(meta3) + bytes(lay.record_bytes - po), c.keys[3].tobytes(), 3,
+                          c.tokens[3]) == ref.ROOT
+    at = po + 12345678
+    k7 = (at - po) // ref.CHUNK_BYTES
+    chunk = bytearray(store.buf[7, po + k7 * ref.CHUNK_BYTES: po + (k7 + 1) * ref.CHUNK_BYTES].cpu().numpy().tobytes())
+    chunk[at - po - k7 * ref.CHUNK_BYTES] ^= 64
+    stored = int.from_bytes(store.buf[7, 256 + 8 * k7: 264 + 8 * k7].cpu().numpy().tobytes(), "little")
+    assert ref.chunk_digest(bytes(chunk)) != stored  # the oracle's verify finds SEGMENT
     store.buf[3, 1000] ^= 2
-    store.buf[7, po + 12345678] ^= 64
+    store.buf[7, at] ^= 64
     dst = PagedCache(geom.n_layers, pages, c.stride, DEV)
     for t in dst.k + dst.v:
         t.fill_(0x11)
@@ -197,17 +223,18 @@ def test_paper_sized_blocks_full_scale():
     ent = np.concatenate([np.arange(b * 550, (b + 1) * 550) for b in good])
     check_pages_equal(c, dst, c.t_dst, blocks=ent)
     for b in (3, 7):
-        for l in (0, geom.n_layers - 1):
-            p = torch.from_numpy(c.t_dst[0][b * 550:(b + 1) * 550].astype(np.int64)).to(DEV)
+        p = torch.from_numpy(c.t_dst[0][b * 550:(b + 1) * 550].astype(np.int64)).to(DEV)
+        for l in range(geom.n_layers):
             assert not dst.k[l][p].any().item() and not dst.v[l][p].any().item()
 
 
-def test_paper_sized_blocks_with_the_partial_last_block():
+def test_paper_sized_blocks_with_the_partial_last_block(record_checker):
     """The whole 97,000-token corpus at the paper's granularity: 11 blocks of
     8,800 tokens and a last block of the remaining 200 tokens (13 of its 550
     pages; the other 537 are left out of the save and not restored), each a
-    4.3 GB record. The tail record is checked field by field against the
-    oracle; every block by verdicts and the permutation copy of its pages."""
+    4.3 GB record. Every record equals the oracle's save in full; every block
+    is restored as the permutation copy of its pages; the tail record loaded
+    as a full block is refused."""
     base = wl.PAPER_CORPUS.geom
     geom = wl.Geometry(base.n_layers, base.n_kv_heads, base.head_dim, base.page_tokens, pages_per_block=550)
     bt, ppb = geom.block_tokens, 550
@@ -238,24 +265,7 @@ def test_paper_sized_blocks_with_the_partial_last_block():
               T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_src), d_ntok), store.ptrs, st)
     torch.cuda.synchronize()
     assert (st.cpu().numpy() == ref.ACCEPT).all()
-    po, S = lay.payload_offset, lay.slab_bytes
-    meta = store.buf[11, :po].cpu().numpy().tobytes()
-    want = ref.header_fields(lay, c.ns, keys[11].tobytes(), 11, 200)
-    assert meta[:144] == want[:144] and meta[152:256] == want[152:256]
-    assert int.from_bytes(meta[144:152], "little") == ref.root_digest(meta)
-    t0 = 256 + 8 * lay.n_segments
-    assert meta[t0:t0 + 800] == toks[11 * bt:].tobytes() and not any(meta[t0 + 800:])
-    r = np.random.default_rng(5)
-    for s in r.choice(lay.n_slabs, 40, replace=False):
-        l, kv, j = (s // ppb) >> 1, (s // ppb) & 1, s % ppb
-        body = store.buf[11, po + s * S: po + (s + 1) * S].cpu().numpy().tobytes()
-        if j < used:
-            page = int(t_src[0][11 * ppb + j])
-            assert body == (c.src.k if kv == 0 else c.src.v)[l][page].cpu().numpy().tobytes()
-        else:
-            assert not any(body)
-        stored = int.from_bytes(meta[256 + 8 * s: 264 + 8 * s], "little")
-        assert stored == ref.chunk_digest(body), s
+    check_records_in_full(c, store, t_src, n_tok, record_checker)
     dst = PagedCache(geom.n_layers, n * ppb, c.stride, DEV)
     for t in dst.k + dst.v:
         t.fill_(0x11)
@@ -271,7 +281,11 @@ def test_paper_sized_blocks_with_the_partial_last_block():
     # the pages the tail leaves out keep their bytes
     p = torch.from_numpy(c.t_dst[0][11 * ppb + used:12 * ppb].astype(np.int64)).to(DEV)
     assert (dst.k[0][p] == 0x11).all().item() and (dst.v[-1][p] == 0x11).all().item()
-    # loaded as a full block, the tail record is refused
+    # loaded as a full block, the tail record is refused: the oracle's
+    # metadata check of its metadata with a full-block count
+    meta11 = store.buf[11, :lay.payload_offset].cpu().numpy().tobytes()
+    assert ref.check_meta(lay, c.ns, meta11 + bytes(lay.record_bytes - lay.payload_offset), keys[11].tobytes(), 11,
+                          rows[11], bt) == ref.HEADER
     T.tl_load(c.ctx, torch.cuda.current_stream(), n, store.ptrs, store.lens,
               T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_dst)), dst.tl(), verd, ws, ws_b)
     torch.cuda.synchronize()

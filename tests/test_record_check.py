@@ -90,3 +90,14 @@ def test_groups_not_restored_are_not_verified(checker):
     eq, verd = checker.check(_lay_args(lay), ns, k, v, tab, records, keys, bidx, toks, load, damage=dmg)
     assert eq.all()
     assert list(verd) == [ref.ACCEPT, ref.ACCEPT, ref.ACCEPT, ref.SEGMENT]
+
+
+def test_chunk_digests_equal_the_oracle_in_batches(checker):
+    rng = np.random.default_rng(9)
+    data = torch.from_numpy(rng.integers(0, 256, 7 * 65536 + 0, dtype=np.uint8))
+    want = [ref.chunk_digest(data[i * 65536:(i + 1) * 65536].numpy().tobytes()) for i in range(7)]
+    got = checker.chunk_digests(data, 65536, batch_bytes=3 * 65536)  # batches of three chunks
+    assert [int(x) for x in got] == want
+    small = torch.from_numpy(rng.integers(0, 256, 5 * 3072, dtype=np.uint8))  # 3 KiB chunks
+    assert [int(x) for x in checker.chunk_digests(small, 3072)] == \
+        [ref.chunk_digest(small[i * 3072:(i + 1) * 3072].numpy().tobytes()) for i in range(5)]
