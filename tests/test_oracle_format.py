@@ -245,6 +245,20 @@ def test_multi_chunk_slab_flips_rejected():
         assert ref.verify(lay, ns, bytes(bad), key, 0, toks, range(2)) == ref.SEGMENT
 
 
+def test_ragged_slab_is_cut_into_full_chunks_then_the_rest():
+    """A slab that is not a multiple of 64 KiB is digested as full 64 KiB
+    chunks and one shorter last chunk (the definition of the chunking); a
+    flip in the short chunk is rejected."""
+    lay = micro(P=48, H=8, D=128)  # 96 KiB slab: 64 KiB + 32 KiB
+    assert lay.slab_bytes == 98304 and lay.chunks_per_slab == 2 and lay.n_segments == 4
+    slab = rand_bytes(lay.slab_bytes, 11).tobytes()
+    assert ref.slab_digests(lay, slab) == [ref.chunk_digest(slab[:65536]), ref.chunk_digest(slab[65536:])]
+    ns, key, toks, slabs, rec = make_block(lay, 12)
+    bad = bytearray(rec)
+    bad[lay.payload_offset + 65536 + 40000] ^= 8  # inside the 32 KiB chunk of slab 0
+    assert ref.verify(lay, ns, bytes(bad), key, 0, toks, range(2)) == ref.SEGMENT
+
+
 def test_every_truncation_and_overlength_rejected():
     lay = micro()
     ns, key, toks, slabs, rec = make_block(lay, 5)

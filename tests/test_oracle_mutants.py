@@ -206,3 +206,56 @@ def test_tail_mutants_caught(monkeypatch):
     monkeypatch.setattr(ref, "check_meta", lax)
     with pytest.raises(AssertionError):
         tail.test_tail_checks()
+
+
+def test_swapped_precedence_caught(monkeypatch):
+    # wrong: the key is checked before the position
+    real = ref.check_meta
+
+    def key_first(lay, ns, rec, key, block_index, tokens, n_tokens=None):
+        code = real(lay, ns, rec, key, block_index, tokens, n_tokens)
+        if code == ref.POSITION and rec[72:104] != key:
+            return ref.KEY
+        return code
+
+    monkeypatch.setattr(ref, "check_meta", key_first)
+    with pytest.raises(AssertionError):
+        pins.test_check_precedence()
+
+
+def test_restore_without_zero_fill_caught(monkeypatch):
+    # wrong: a rejected block's pages keep what was there
+    def no_fill(lay, ns, records, keys, block_index, tokens, tables, dst_k, dst_v, n_pages=None, misaligned=(),
+                n_tokens=None):
+        snap_k = [x.copy() for x in dst_k]
+        snap_v = [x.copy() for x in dst_v]
+        vs = _real_restore(lay, ns, records, keys, block_index, tokens, tables, dst_k, dst_v, n_pages, misaligned,
+                           n_tokens)
+        for b, v in enumerate(vs):
+            if v == ref.ACCEPT:
+                continue
+            for (_, l, kv, j) in ref.read_slabs(lay, tables, b):
+                p = ref.table_entry(lay, tables, l, b, j)
+                if 0 <= p < dst_k[0].shape[0]:
+                    (dst_k if kv == 0 else dst_v)[l][p] = (snap_k if kv == 0 else snap_v)[l][p]
+        return vs
+
+    monkeypatch.setattr(ref, "restore", no_fill)
+    with pytest.raises(AssertionError):
+        pins.test_restore_rejects_and_zero_fills_only_bad_blocks()
+
+
+_real_restore = ref.restore
+
+
+def test_equal_chunks_of_a_ragged_slab_caught(monkeypatch):
+    # wrong: a ragged slab cut into equal chunks (48 + 48 KiB) instead of 64 + 32
+    def halves(lay, slab):
+        s = bytes(slab)
+        k = lay.chunks_per_slab
+        w = len(s) // k
+        return [ref.chunk_digest(s[i * w:(i + 1) * w]) for i in range(k)]
+
+    monkeypatch.setattr(ref, "slab_digests", halves)
+    with pytest.raises(AssertionError):
+        pins.test_ragged_slab_is_cut_into_full_chunks_then_the_rest()
