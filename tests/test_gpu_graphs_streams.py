@@ -1,4 +1,5 @@
-"""tl_load under HIP graph capture and on concurrent streams.
+"""tl_load (and tl_load_static) under HIP graph capture, and tl_load on
+concurrent streams.
 
 The load issues three kernels and no memset, so a caller can capture it once
 and replay it: every replay below runs after eager work of the program itself
@@ -28,7 +29,11 @@ def _setup(seed=21):
     return c, store
 
 
-def test_captured_load_replays_match_eager():
+@pytest.mark.parametrize("static", [False, True])
+def test_captured_load_replays_match_eager(static):
+    """static: capture tl_load_static (no workspace; the library's per-device
+    status array), the entry point for callers that cannot allocate, against
+    the same eager tl_load."""
     T.tl_timing(False)
     c, store = _setup()
     n = c.n
@@ -44,15 +49,21 @@ def test_captured_load_replays_match_eager():
     def launch(stream):
         T.tl_load(c.ctx, stream, n, store.ptrs, lens, blk, cache, verd, ws, ws_bytes)
 
+    def captured(stream):
+        if static:
+            T.tl_load_static(c.ctx, stream, n, store.ptrs, lens, blk, cache, verd)
+        else:
+            launch(stream)
+
     g = torch.cuda.CUDAGraph()
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(s):
-        launch(s)  # warm-up on the capture stream
+        captured(s)  # warm-up on the capture stream
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     with torch.cuda.graph(g, stream=s):
-        launch(s)
+        captured(s)
     torch.cuda.synchronize()
 
     # a sequence of input changes made eagerly between replays
