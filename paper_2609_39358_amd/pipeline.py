@@ -58,8 +58,10 @@ class Store:
 
 
 class RestorePipeline:
-    """Restores the stored prefix blocks of batches of requests into `pool`
-    (pages 0 .. n-1 of the pool, in request order).
+    """Restores the stored prefix blocks of batches of requests into `pool`:
+    the i-th restored block of a batch (in request order) gets pool pages
+    i·ppb .. i·ppb + ppb − 1 in every layer group, ppb being the context's
+    pages per block.
 
     Each call runs the keys (tl_block_keys_batch, host threads) and the reuse
     lookup (tl_index_lookup_prefix) on the host, writes tl_load's per-block
@@ -73,7 +75,8 @@ class RestorePipeline:
         self.ctx = store.ctx
         self.stream = stream or torch.cuda.current_stream()
         dev = pool.k[0].device
-        cap = pool.n_pages
+        self.ppb = self.ctx.pages_per_block
+        cap = pool.n_pages // self.ppb  # blocks per batch
         self.cap = cap
         self.ws_bytes = max(T.tl_workspace_bytes(self.ctx, cap), 4)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
@@ -81,7 +84,8 @@ class RestorePipeline:
         self.copy_stream = torch.cuda.Stream(device=dev)
         P, G = self.ctx.block_bytes // 4, self.ctx.n_groups
         shapes = {"ptrs": ((cap,), torch.int64), "lens": ((cap,), torch.int64), "keys": ((cap, 32), torch.uint8),
-                  "pos": ((cap,), torch.int64), "tok": ((cap, P), torch.int32), "tab": ((G * cap,), torch.int32)}
+                  "pos": ((cap,), torch.int64), "tok": ((cap, P), torch.int32),
+                  "tab": ((G * cap * self.ppb,), torch.int32)}
         self._sets = []
         for _ in range(2):
             h = {k: torch.empty(sh, dtype=dt, pin_memory=True) for k, (sh, dt) in shapes.items()}
@@ -105,7 +109,7 @@ class RestorePipeline:
         rid = handles[sel]
         n = int(rid.size)
         if n > self.cap:
-            raise ValueError("batch needs %d pages, pool has %d" % (n, self.cap))
+            raise ValueError("batch needs %d pages, pool has %d" % (n * self.ppb, self.pool.n_pages))
         res = BatchResult(list(request_ids), [int(h) for h in hits], rid, pos_all[sel].astype(np.uint64),
                           np.repeat(np.asarray(request_ids, dtype=np.int64), nk_i)[sel], None, t1 - t0,
                           [keys[int(o):int(o) + int(k)] for o, k in zip(koff, nk)])
@@ -129,15 +133,16 @@ class RestorePipeline:
                 if k:
                     tok[row:row + k] = np.asarray(t[:k * P], dtype="<u4").view(np.int32).reshape(k, P)
                     row += k
-            h["tab"].numpy()[:G * n] = np.tile(np.arange(n, dtype=np.int32), G)
+            m = n * self.ppb  # table entries per group
+            h["tab"].numpy()[:G * m] = np.tile(np.arange(m, dtype=np.int32), G)
             self.copy_stream.wait_event(loaded)  # the load that last read this device set is done
             with torch.cuda.stream(self.copy_stream):
                 for k in ("ptrs", "lens", "keys", "pos", "tok"):
                     d[k][:n].copy_(h[k][:n], non_blocking=True)
-                d["tab"][:G * n].copy_(h["tab"][:G * n], non_blocking=True)
+                d["tab"][:G * m].copy_(h["tab"][:G * m], non_blocking=True)
             copied.record(self.copy_stream)
             self.stream.wait_event(copied)
-            blk = T.make_blocks(d["keys"][:n], d["pos"][:n], d["tok"][:n], d["tab"][:G * n])
+            blk = T.make_blocks(d["keys"][:n], d["pos"][:n], d["tok"][:n], d["tab"][:G * m])
             T.tl_load(ctx, self.stream, n, d["ptrs"][:n], d["lens"][:n], blk, self.pool.tl(), verd, self.ws,
                       self.ws_bytes)
             loaded.record(self.stream)

@@ -37,15 +37,17 @@ class MultiRun:
         self.lay = layout_of(g)
         self.ctx = ctx_of(g)
         self.ns = ref.namespace_digest(TEN, FP, self.lay)
-        P = g.page_tokens
+        P = g.block_tokens
+        self.ppb = ppb = g.pages_per_block
         self.bpd = len(w.base_docs[0]) // P  # full blocks per base document
         self.n_stored = len(w.base_docs) * self.bpd
         self.rb = self.lay.record_bytes
         self.pool_pages = pool_pages
-        # base documents: source pages (random placement), keys, records
-        self.src_table = wl.page_table(self.n_stored, self.n_stored, seed, 7)
+        # base documents: source pages (random placement; record r owns
+        # src_table[r*ppb : (r+1)*ppb]), keys, records
+        self.src_table = wl.page_table(self.n_stored * ppb, self.n_stored * ppb, seed, 7)
         log("multi-request: %d stored records of %d B, pool %d pages" % (self.n_stored, self.rb, pool_pages))
-        self.src = fill_cache(PagedCache(g.n_layers, self.n_stored, self.lay.slab_bytes, DEV), g, seed)
+        self.src = fill_cache(PagedCache(g.n_layers, self.n_stored * ppb, self.lay.slab_bytes, DEV), g, seed)
         base_keys = T.tl_block_keys_batch(self.ctx, w.base_docs)
         for d, k in zip(w.base_docs, base_keys):  # every base key against the oracle's chain
             assert [x.tobytes() for x in k] == ref.block_keys(self.ns, d.tobytes(), self.lay.block_bytes)[:self.bpd]
@@ -90,7 +92,7 @@ class MultiRun:
         `check(batch)` is called after each batch (pages still in the pool)."""
         w = self.w
         out = []
-        for bi, reqs in enumerate(wl.admission_batches(w.requests, self.pool_pages)):
+        for bi, reqs in enumerate(wl.admission_batches(w.requests, self.pool_pages // self.ppb)):
             res = self.pipe.restore([w.requests[r].tokens for r in reqs], reqs)
             for r, h, k in zip(reqs, res.hits, res.keys):
                 assert h == w.requests[r].shared_blocks, (r, h, w.requests[r].shared_blocks)
@@ -99,7 +101,7 @@ class MultiRun:
                                                                   self.lay.block_bytes), r
             torch.cuda.synchronize()
             b = Batch(reqs)
-            b.blocks = [(int(r), int(p), int(rid), page) for page, (r, p, rid) in
+            b.blocks = [(int(r), int(p), int(rid), j * self.ppb) for j, (r, p, rid) in
                         enumerate(zip(res.request_of, res.positions, res.record_ids))]
             b.verdicts = res.verdicts.cpu().numpy()
             log("batch %d: %d requests, %d blocks" % (bi, len(reqs), len(b.blocks)))
@@ -112,17 +114,20 @@ class MultiRun:
         """Every restored block asks for exactly what its record holds: the
         request's key, position and token ids at that block equal the stored
         record's (so the oracle's verdict on the record is the block's)."""
-        P = self.g.page_tokens
+        P = self.g.block_tokens
         for req, pos, rid, page in b.blocks:
             q = self.w.requests[req]
             assert pos == int(self.bidx[rid]), (req, pos, rid)
             assert np.array_equal(q.tokens[pos * P:(pos + 1) * P], self.tokens[rid]), (req, pos, rid)
 
     def check_pages(self, b: Batch, rejected: set):
-        """Accepted blocks' pool pages equal their source pages; rejected ones are zero."""
-        slab = self.lay.slab_bytes
-        acc = [(blk[2], blk[3]) for blk, v in zip(b.blocks, b.verdicts) if v == ref.ACCEPT]
-        rej = [blk[3] for blk, v in zip(b.blocks, b.verdicts) if v != ref.ACCEPT]
+        """Accepted blocks' pool pages equal their source pages; rejected ones
+        are zero. Block (record r, first pool page q) spans pool pages
+        q .. q + ppb − 1 and source pages src_table[r*ppb .. r*ppb + ppb − 1]."""
+        slab, ppb = self.lay.slab_bytes, self.ppb
+        j = np.arange(ppb)
+        acc = [(blk[2] * ppb + i, blk[3] + i) for blk, v in zip(b.blocks, b.verdicts) if v == ref.ACCEPT for i in j]
+        rej = [blk[3] + i for blk, v in zip(b.blocks, b.verdicts) if v != ref.ACCEPT for i in j]
         assert {blk[2] for blk, v in zip(b.blocks, b.verdicts) if v != ref.ACCEPT} <= rejected
         if acc:
             src_p = torch.from_numpy(self.src_table[[a for a, _ in acc]].astype(np.int64)).to(DEV)

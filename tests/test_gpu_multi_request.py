@@ -18,15 +18,21 @@ from tests.multi_request import MultiRun
 pytestmark = pytest.mark.gpu
 
 
-def test_multi_request_reduced_full_oracle():
-    geom = wl.Geometry(2, 2, 64, 16)
-    w = wl.multi_request(n_requests=16, n_base=3, base_tokens=512, median=200, lo=40, hi=512,
+# (pages per block, requests, base tokens, median prompt, longest prompt)
+REDUCED = {"one_page_blocks": (1, 16, 512, 200, 512), "three_page_blocks": (3, 16, 1536, 600, 1536)}
+
+
+@pytest.mark.parametrize("case", list(REDUCED))
+def test_multi_request_reduced_full_oracle(case):
+    ppb, n_req, base_tokens, median, hi = REDUCED[case]
+    geom = wl.Geometry(2, 2, 64, 16, pages_per_block=ppb)
+    w = wl.multi_request(n_requests=n_req, n_base=3, base_tokens=base_tokens, median=median, lo=40, hi=hi,
                          corrupt_frac=0.10, geom=geom, seed=21)
     run = MultiRun(w, pool_pages=128, seed=21)
     damaged = {r for r, _ in w.corrupt_flip} | {r for r, _ in w.corrupt_trunc}
     assert len(damaged) == int(0.10 * run.n_stored)
     lay = run.lay
-    slab = lay.slab_bytes
+    slab, B = lay.slab_bytes, geom.block_tokens
 
     def check(b):
         # the oracle restores the same batch into host copies of the pool
@@ -37,16 +43,18 @@ def test_multi_request_reduced_full_oracle():
         for r, i, rid, page in b.blocks:
             recs.append(run.store.buf[rid].cpu().numpy().tobytes()[:int(run.lens[rid])])
             q = w.requests[r]
-            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * 16].tobytes(), 64)[i])
+            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * B].tobytes(), lay.block_bytes)[i])
             bidx.append(i)
-            toks.append(q.tokens[i * 16:(i + 1) * 16])
-        # every pool page of this batch is written by the batch (accepted:
-        # the record's slabs, rejected: zeros), so the prior contents do not matter
-        vo = ref.restore(lay, run.ns, recs, keys, bidx, toks, np.arange(n)[None, :], hk, hv)
+            toks.append(q.tokens[i * B:(i + 1) * B])
+        # block j of the batch owns pool pages j*ppb .. j*ppb + ppb - 1; every
+        # one of them is written (accepted: the record's slabs, rejected:
+        # zeros), so the prior contents do not matter
+        m = n * ppb
+        vo = ref.restore(lay, run.ns, recs, keys, bidx, toks, np.arange(m)[None, :], hk, hv)
         assert [int(x) for x in b.verdicts] == vo
         for l in range(geom.n_layers):
-            assert np.array_equal(run.dst.k[l][:n].cpu().numpy()[:, :slab], hk[l][:n, :slab])
-            assert np.array_equal(run.dst.v[l][:n].cpu().numpy()[:, :slab], hv[l][:n, :slab])
+            assert np.array_equal(run.dst.k[l][:m].cpu().numpy()[:, :slab], hk[l][:m, :slab])
+            assert np.array_equal(run.dst.v[l][:m].cpu().numpy()[:, :slab], hv[l][:m, :slab])
 
     batches = run.run(check)
     assert len(batches) >= 2
@@ -99,9 +107,9 @@ def device_batches(run, pipe, check):
 
     from tests.gpu_case import DEV
     from tests.multi_request import Batch
-    w, P = run.w, run.g.page_tokens
+    w, ppb = run.w, run.ppb
     out = []
-    for bi, reqs in enumerate(wl.admission_batches(w.requests, run.pool_pages, whole_prompts=True)):
+    for bi, reqs in enumerate(wl.admission_batches(w.requests, run.pool_pages // ppb, whole_prompts=True)):
         for t in run.dst.k + run.dst.v:
             t.fill_(0x5D)
         toks = np.concatenate([w.requests[r].tokens for r in reqs])
@@ -116,24 +124,26 @@ def device_batches(run, pipe, check):
             s0 = int(res.slot_off[c])
             q = w.requests[r]
             for k in range(q.full_blocks):
-                if k < hits[c]:
-                    b.blocks.append((r, k, q.base * run.bpd + k, s0 + k))
+                if k < hits[c]:  # slot s0 + k owns pool pages from (s0 + k) * ppb on
+                    b.blocks.append((r, k, q.base * run.bpd + k, (s0 + k) * ppb))
                 else:
                     assert verd[s0 + k] == ref.MISSING
-        b.verdicts = np.array([verd[blk[3]] for blk in b.blocks], np.uint8)
+        b.verdicts = np.array([verd[blk[3] // ppb] for blk in b.blocks], np.uint8)
         log("device batch %d: %d requests, %d slots, %d restored" % (bi, len(reqs), res.n_slots, len(b.blocks)))
         check(b, res)
         out.append(b)
     return out
 
 
-def test_device_pipeline_reduced_full_oracle():
-    geom = wl.Geometry(2, 2, 64, 16)
-    w = wl.multi_request(n_requests=16, n_base=3, base_tokens=512, median=200, lo=40, hi=512,
+@pytest.mark.parametrize("case", list(REDUCED))
+def test_device_pipeline_reduced_full_oracle(case):
+    ppb, n_req, base_tokens, median, hi = REDUCED[case]
+    geom = wl.Geometry(2, 2, 64, 16, pages_per_block=ppb)
+    w = wl.multi_request(n_requests=n_req, n_base=3, base_tokens=base_tokens, median=median, lo=40, hi=hi,
                          corrupt_frac=0.10, geom=geom, seed=21)
     run = MultiRun(w, pool_pages=96, seed=21)
     pipe = device_run(run)
-    slab = run.lay.slab_bytes
+    B = geom.block_tokens
 
     def check(b, res):
         # every slot's pages as the oracle restores the batch: hits get the
@@ -144,10 +154,10 @@ def test_device_pipeline_reduced_full_oracle():
         for r, i, rid, page in b.blocks:
             recs.append(run.store.buf[rid].cpu().numpy().tobytes()[:int(run.lens[rid])])
             q = w.requests[r]
-            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * 16].tobytes(), 64)[i])
+            keys.append(ref.block_keys(run.ns, q.tokens[:(i + 1) * B].tobytes(), run.lay.block_bytes)[i])
             bidx.append(i)
-            toks.append(q.tokens[i * 16:(i + 1) * 16])
-            pages.append(page)
+            toks.append(q.tokens[i * B:(i + 1) * B])
+            pages.extend(range(page, page + ppb))
         vo = ref.restore(run.lay, run.ns, recs, keys, bidx, toks, np.array(pages)[None, :], hk, hv)
         assert [int(x) for x in b.verdicts] == vo
         for l in range(geom.n_layers):

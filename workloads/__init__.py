@@ -198,7 +198,7 @@ def multi_request(n_requests=256, n_base=8, base_tokens=32768, median=4096, sigm
     stored base records are damaged, half by one bit flip, half by truncation.
     Record ids are doc * blocks_per_doc + block."""
     geom = geom or MULTI_REQUEST.geom
-    P = geom.page_tokens
+    P = geom.block_tokens
     base_docs = [tokens(base_tokens, seed, 100 + d) for d in range(n_base)]
     r = rng(seed, 4)
     lens = np.clip(np.round(r.lognormal(np.log(median), sigma, n_requests)), lo, hi).astype(int)
