@@ -259,3 +259,87 @@ def test_equal_chunks_of_a_ragged_slab_caught(monkeypatch):
     monkeypatch.setattr(ref, "slab_digests", halves)
     with pytest.raises(AssertionError):
         pins.test_ragged_slab_is_cut_into_full_chunks_then_the_rest()
+
+
+def test_dropped_token_check_caught(monkeypatch):
+    # wrong: the record's token ids are never compared with the request's
+    real = ref.check_meta
+
+    def no_tokens(lay, ns, rec, key, block_index, tokens, n_tokens=None):
+        return real(lay, ns, rec, key, block_index, None, n_tokens)
+
+    monkeypatch.setattr(ref, "check_meta", no_tokens)
+    with pytest.raises(AssertionError):
+        pins.test_check_precedence()
+
+
+def test_overlong_record_accepted_caught(monkeypatch):
+    # wrong: bytes past the record's end are ignored instead of refused
+    real = ref.verify
+
+    def cut(lay, ns, rec, key, block_index, tokens, slabs_read, bad_arg=False, n_tokens=None):
+        if rec is not None:
+            rec = rec[:lay.record_bytes]
+        return real(lay, ns, rec, key, block_index, tokens, slabs_read, bad_arg, n_tokens)
+
+    monkeypatch.setattr(ref, "verify", cut)
+    with pytest.raises(AssertionError):
+        pins.test_every_truncation_and_overlength_rejected()
+
+
+def test_slabs_of_unrestored_groups_read_caught(monkeypatch):
+    # wrong: a -1 table entry still counts as a slab the load reads
+    def every_slab(lay, tables, b):
+        return [(ref.slab_index(lay, l, kv, j), l, kv, j)
+                for l in range(lay.n_layers) for kv in (0, 1) for j in range(lay.pages_per_block)]
+
+    monkeypatch.setattr(ref, "read_slabs", every_slab)
+    with pytest.raises(AssertionError):
+        pins.test_multi_page_restore_is_the_permutation_copy_with_partial_groups()
+
+
+def test_save_with_one_table_for_every_group_caught(monkeypatch):
+    # wrong: every layer's pages are looked up in layer group 0's table
+    real = ref.save
+
+    def one_table(lay, ns, src_k, src_v, tables, *a, **kw):
+        t = np.asarray(tables)
+        return real(lay, ns, src_k, src_v, np.repeat(t[:1], t.shape[0], axis=0), *a, **kw)
+
+    monkeypatch.setattr(ref, "save", one_table)
+    with pytest.raises(AssertionError):
+        pins.test_multi_page_restore_is_the_permutation_copy_with_partial_groups()
+
+
+def test_minus_one_entry_taken_as_last_page_caught(monkeypatch):
+    # wrong: a -1 table entry used as a Python index writes the pool's last page
+    def last_page(lay, ns, records, keys, block_index, tokens, tables, dst_k, dst_v, n_pages=None, misaligned=(),
+                  n_tokens=None):
+        vs = _real_restore(lay, ns, records, keys, block_index, tokens, tables, dst_k, dst_v, n_pages, misaligned,
+                           n_tokens)
+        t = np.asarray(tables)
+        S, po = lay.slab_bytes, lay.payload_offset
+        for b, v in enumerate(vs):
+            for l in range(lay.n_layers):
+                for j in range(lay.pages_per_block):
+                    if ref.table_entry(lay, t, l, b, j) != -1 or v != ref.ACCEPT:
+                        continue
+                    for kv, dst in ((0, dst_k), (1, dst_v)):
+                        s = ref.slab_index(lay, l, kv, j)
+                        dst[l][-1, :S] = np.frombuffer(records[b][po + s * S:po + (s + 1) * S], np.uint8)
+        return vs
+
+    monkeypatch.setattr(ref, "restore", last_page)
+    with pytest.raises(AssertionError):
+        pins.test_multi_page_restore_is_the_permutation_copy_with_partial_groups()
+
+
+def test_namespace_without_geometry_caught(monkeypatch):
+    # wrong: the namespace names tenant and model but not the record geometry
+    real = ref.namespace_digest
+    fixed = ref.Layout(1, 1, 32, 1, 16)
+    monkeypatch.setattr(ref, "namespace_digest", lambda tenant, model_fp, lay: real(tenant, model_fp, fixed))
+    with pytest.raises(AssertionError):
+        pins.test_namespace_separates_tenant_model_and_geometry()
+    with pytest.raises(AssertionError):
+        pins.test_multi_page_block_geometry_and_keys()
