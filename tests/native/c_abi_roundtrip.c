@@ -3,8 +3,9 @@
  * paged cache, one payload byte of record 5 flipped in device memory, and
  * the records restored into a second cache through other page tables. Every
  * verdict must be ACCEPT except block 5 (SEGMENT), every restored page must
- * equal its source page, and block 5's pages must be zero. Prints one line
- * and returns 0 on success. With a file name as its argument it also writes
+ * equal its source page, and block 5's pages must be zero; then the same
+ * restore again through tl_load_static, which allocates nothing. Prints one
+ * line and returns 0 on success. With a file name as its argument it also writes
  * its inputs and outputs there, back to back, for a check against the
  * oracle: the token ids, keys and both page tables, the source pages (per
  * layer, K then V), the records as saved, the verdicts, then the destination
@@ -54,6 +55,47 @@ static int dump_dev(FILE* f, const void* d, size_t n) {
   }
   free(h);
   return 0;
+}
+
+/* Every verdict ACCEPT except block 5's (SEGMENT); every restored page equal
+ * to its source page; block 5's pages zero. */
+static int check_restore(const uint8_t* verd, int nb, int n_layers, size_t slab, const uint64_t* src_k,
+                         const uint64_t* src_v, const uint64_t* dst_k, const uint64_t* dst_v,
+                         const int32_t* t_src, const int32_t* t_dst, const char* what) {
+  for (int b = 0; b < nb; ++b) {
+    const int want = b == 5 ? TL_SEGMENT : TL_ACCEPT;
+    if (verd[b] != want) {
+      fprintf(stderr, "%s: verdict of block %d: %s\n", what, b, tl_verdict_string(verd[b]));
+      return 1;
+    }
+  }
+  uint8_t* a = (uint8_t*)malloc(slab);
+  uint8_t* b2 = (uint8_t*)malloc(slab);
+  int bad = !a || !b2;
+  for (int l = 0; l < n_layers && !bad; ++l)
+    for (int kv = 0; kv < 2 && !bad; ++kv)
+      for (int b = 0; b < nb && !bad; ++b) {
+        const uint64_t sbase = (kv ? src_v : src_k)[l], dbase = (kv ? dst_v : dst_k)[l];
+        if (hipMemcpy(b2, (void*)(uintptr_t)(dbase + (uint64_t)t_dst[b] * slab), slab, hipMemcpyDeviceToHost) !=
+            hipSuccess) {
+          bad = 2;
+          break;
+        }
+        if (b == 5) {
+          memset(a, 0, slab);
+        } else if (hipMemcpy(a, (void*)(uintptr_t)(sbase + (uint64_t)t_src[b] * slab), slab,
+                             hipMemcpyDeviceToHost) != hipSuccess) {
+          bad = 2;
+          break;
+        }
+        if (memcmp(a, b2, slab)) {
+          fprintf(stderr, "%s: page of block %d, layer %d, %s differs\n", what, b, l, kv ? "V" : "K");
+          bad = 1;
+        }
+      }
+  free(a);
+  free(b2);
+  return bad;
 }
 
 int main(int argc, char** argv) {
@@ -190,31 +232,25 @@ int main(int argc, char** argv) {
       return 1;
     }
   }
-  for (int b = 0; b < NB; ++b) {
-    const int want = b == 5 ? TL_SEGMENT : TL_ACCEPT;
-    if (verd[b] != want) {
-      fprintf(stderr, "verdict of block %d: %s\n", b, tl_verdict_string(verd[b]));
-      return 1;
-    }
+  int r = check_restore(verd, NB, L, slab, src_k, src_v, dst_k, dst_v, t_src, t_dst, "tl_load");
+  if (r) return r;
+
+  /* the same restore through the entry point that allocates nothing (its
+   * status words live in the library), into a refilled destination cache */
+  for (int l = 0; l < L; ++l) {
+    CHECK_HIP(hipMemset((void*)(uintptr_t)dst_k[l], 0x77, PAGES * slab));
+    CHECK_HIP(hipMemset((void*)(uintptr_t)dst_v[l], 0x77, PAGES * slab));
   }
-  /* restored pages equal their source pages; block 5's pages are zero */
-  uint8_t* a = (uint8_t*)malloc(slab);
-  uint8_t* b2 = (uint8_t*)malloc(slab);
-  for (int l = 0; l < L; ++l)
-    for (int kv = 0; kv < 2; ++kv)
-      for (int b = 0; b < NB; ++b) {
-        const uint64_t sbase = (kv ? src_v : src_k)[l], dbase = (kv ? dst_v : dst_k)[l];
-        CHECK_HIP(hipMemcpy(b2, (void*)(uintptr_t)(dbase + (uint64_t)t_dst[b] * slab), slab, hipMemcpyDeviceToHost));
-        if (b == 5) {
-          memset(a, 0, slab);
-        } else {
-          CHECK_HIP(hipMemcpy(a, (void*)(uintptr_t)(sbase + (uint64_t)t_src[b] * slab), slab, hipMemcpyDeviceToHost));
-        }
-        if (memcmp(a, b2, slab)) {
-          fprintf(stderr, "page of block %d, layer %d, %s differs\n", b, l, kv ? "V" : "K");
-          return 1;
-        }
-      }
+  CHECK_HIP(hipMemset(d_verd, 0, NB));
+  st = tl_load_static(ctx, NULL, NB, d_ptrs, d_lens, &load_blk, &dst, d_verd);
+  if (st != TL_OK) {
+    fprintf(stderr, "tl_load_static: %s\n", tl_status_string(st));
+    return 1;
+  }
+  CHECK_HIP(hipDeviceSynchronize());
+  CHECK_HIP(hipMemcpy(verd, d_verd, NB, hipMemcpyDeviceToHost));
+  r = check_restore(verd, NB, L, slab, src_k, src_v, dst_k, dst_v, t_src, t_dst, "tl_load_static");
+  if (r) return r;
   tl_ctx_destroy(ctx);
   printf("c-abi round trip ok: %d blocks, record %zu bytes\n", NB, rb);
   return 0;
