@@ -57,8 +57,10 @@ class MultiRun:
         self.st = pipeline.Store(self.ctx, self.n_stored, DEV)
         self.store = self.st.records
         st = torch.zeros(self.n_stored, dtype=torch.uint8, device=DEV)
+        # every layer group reads the same source pages
+        self.src_tables = np.tile(self.src_table, (g.n_groups, 1))
         self._save_in = (torch.from_numpy(self.keys).to(DEV), i64(self.bidx),
-                         i32(self.tokens.view(np.int32)), i32(self.src_table[None, :]))
+                         i32(self.tokens.view(np.int32)), i32(self.src_tables))
         T.tl_save(self.ctx, torch.cuda.current_stream(), self.n_stored, self.src.tl(),
                   T.make_blocks(*self._save_in), self.store.ptrs, st)
         torch.cuda.synchronize()
@@ -68,7 +70,7 @@ class MultiRun:
             dmg = {rid: Damage(bits=[wl.scale_bit(frac, self.rb)]) for rid, frac in w.corrupt_flip}
             for rid, frac in w.corrupt_trunc:
                 dmg.setdefault(rid, Damage()).length = wl.scale_len(frac, self.rb)
-            tab = self.src_table[None, :]
+            tab = self.src_tables
             eq, self.want = checker.check(lay_args(self.lay), self.ns, self.src.k, self.src.v, tab, self.store.buf,
                                           [k.tobytes() for k in self.keys], self.bidx, self.tokens, tab,
                                           damage=dmg, log=log)

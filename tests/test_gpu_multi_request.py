@@ -18,14 +18,17 @@ from tests.multi_request import MultiRun
 pytestmark = pytest.mark.gpu
 
 
-# (pages per block, requests, base tokens, median prompt, longest prompt)
-REDUCED = {"one_page_blocks": (1, 16, 512, 200, 512), "three_page_blocks": (3, 16, 1536, 600, 1536)}
+# (geometry, requests, base tokens, median prompt, longest prompt)
+REDUCED = {"one_page_blocks": (wl.Geometry(2, 2, 64, 16), 16, 512, 200, 512),
+           "three_page_blocks": (wl.Geometry(2, 2, 64, 16, pages_per_block=3), 16, 1536, 600, 1536),
+           "two_layer_groups": (wl.Geometry(4, 2, 64, 16, layer_window=(0, 32, 0, 32), layer_group=(0, 1, 0, 1)),
+                                16, 512, 200, 512)}
 
 
 @pytest.mark.parametrize("case", list(REDUCED))
 def test_multi_request_reduced_full_oracle(case):
-    ppb, n_req, base_tokens, median, hi = REDUCED[case]
-    geom = wl.Geometry(2, 2, 64, 16, pages_per_block=ppb)
+    geom, n_req, base_tokens, median, hi = REDUCED[case]
+    ppb, G = geom.pages_per_block, geom.n_groups
     w = wl.multi_request(n_requests=n_req, n_base=3, base_tokens=base_tokens, median=median, lo=40, hi=hi,
                          corrupt_frac=0.10, geom=geom, seed=21)
     run = MultiRun(w, pool_pages=128, seed=21)
@@ -50,7 +53,7 @@ def test_multi_request_reduced_full_oracle(case):
         # one of them is written (accepted: the record's slabs, rejected:
         # zeros), so the prior contents do not matter
         m = n * ppb
-        vo = ref.restore(lay, run.ns, recs, keys, bidx, toks, np.arange(m)[None, :], hk, hv)
+        vo = ref.restore(lay, run.ns, recs, keys, bidx, toks, np.tile(np.arange(m), (G, 1)), hk, hv)
         assert [int(x) for x in b.verdicts] == vo
         for l in range(geom.n_layers):
             assert np.array_equal(run.dst.k[l][:m].cpu().numpy()[:, :slab], hk[l][:m, :slab])
@@ -137,8 +140,8 @@ def device_batches(run, pipe, check):
 
 @pytest.mark.parametrize("case", list(REDUCED))
 def test_device_pipeline_reduced_full_oracle(case):
-    ppb, n_req, base_tokens, median, hi = REDUCED[case]
-    geom = wl.Geometry(2, 2, 64, 16, pages_per_block=ppb)
+    geom, n_req, base_tokens, median, hi = REDUCED[case]
+    ppb, G = geom.pages_per_block, geom.n_groups
     w = wl.multi_request(n_requests=n_req, n_base=3, base_tokens=base_tokens, median=median, lo=40, hi=hi,
                          corrupt_frac=0.10, geom=geom, seed=21)
     run = MultiRun(w, pool_pages=96, seed=21)
@@ -158,7 +161,7 @@ def test_device_pipeline_reduced_full_oracle(case):
             bidx.append(i)
             toks.append(q.tokens[i * B:(i + 1) * B])
             pages.extend(range(page, page + ppb))
-        vo = ref.restore(run.lay, run.ns, recs, keys, bidx, toks, np.array(pages)[None, :], hk, hv)
+        vo = ref.restore(run.lay, run.ns, recs, keys, bidx, toks, np.tile(np.array(pages), (G, 1)), hk, hv)
         assert [int(x) for x in b.verdicts] == vo
         for l in range(geom.n_layers):
             assert np.array_equal(run.dst.k[l].cpu().numpy(), hk[l])
