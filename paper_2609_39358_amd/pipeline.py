@@ -68,10 +68,14 @@ class RestorePipeline:
     arrays into one of two pinned host sets, uploads them on a copy stream
     and enqueues tl_load on `stream` behind the upload. Nothing waits for the
     GPU except the reuse of a set two calls later, so the host work of a batch
-    overlaps the previous batch's restore when calls follow each other."""
+    overlaps the previous batch's restore when calls follow each other.
 
-    def __init__(self, store: Store, pool: PagedCache, stream=None, threads: int = 0):
-        self.store, self.pool, self.threads = store, pool, threads
+    tail: a request's partial last block is keyed (TL_KEYS_TAIL) and, when
+    its key is stored and every block before it is reused, restored with its
+    token count; the pages it holds no tokens on stay untouched (-1)."""
+
+    def __init__(self, store: Store, pool: PagedCache, stream=None, threads: int = 0, tail: bool = False):
+        self.store, self.pool, self.threads, self.tail = store, pool, threads, tail
         self.ctx = store.ctx
         self.stream = stream or torch.cuda.current_stream()
         dev = pool.k[0].device
@@ -85,7 +89,7 @@ class RestorePipeline:
         P, G = self.ctx.block_bytes // 4, self.ctx.n_groups
         shapes = {"ptrs": ((cap,), torch.int64), "lens": ((cap,), torch.int64), "keys": ((cap, 32), torch.uint8),
                   "pos": ((cap,), torch.int64), "tok": ((cap, P), torch.int32),
-                  "tab": ((G * cap * self.ppb,), torch.int32)}
+                  "tab": ((G * cap * self.ppb,), torch.int32), "ntok": ((cap,), torch.int32)}
         self._sets = []
         for _ in range(2):
             h = {k: torch.empty(sh, dtype=dt, pin_memory=True) for k, (sh, dt) in shapes.items()}
@@ -99,7 +103,7 @@ class RestorePipeline:
         ctx = self.ctx
         P, G = ctx.block_bytes // 4, ctx.n_groups
         t0 = time.perf_counter()
-        keys, koff, nk = T.tl_block_keys_batch(ctx, tokens, n_threads=self.threads, flat=True)  # a1
+        keys, koff, nk = T.tl_block_keys_batch(ctx, tokens, n_threads=self.threads, flat=True, tail=self.tail)  # a1
         hits, handles = self.store.index.lookup_prefix(keys, koff, nk)  # a2: each request's leading stored run
         t1 = time.perf_counter()
         # marshalling: the hit blocks of every request, in request order
@@ -126,23 +130,35 @@ class RestorePipeline:
             h["lens"].numpy()[:n] = self.store.lens[rid].view(np.int64)
             h["keys"].numpy()[:n] = keys[sel]
             h["pos"].numpy()[:n] = res.positions.view(np.int64)
-            tok = h["tok"].numpy()
+            tok, ntok = h["tok"].numpy(), h["ntok"].numpy()
+            m = n * self.ppb  # table entries per group
+            tab = h["tab"].numpy()[:G * m].reshape(G, m)
+            tab[:] = np.arange(m, dtype=np.int32)
             row = 0
             for t, k in zip(tokens, hits):
                 k = int(k)
-                if k:
-                    tok[row:row + k] = np.asarray(t[:k * P], dtype="<u4").view(np.int32).reshape(k, P)
-                    row += k
-            m = n * self.ppb  # table entries per group
-            h["tab"].numpy()[:G * m] = np.tile(np.arange(m, dtype=np.int32), G)
+                if not k:
+                    continue
+                t = np.asarray(t, dtype="<u4")
+                have = min(t.size, k * P)  # token ids of the k restored blocks
+                blk = tok[row:row + k].reshape(-1)
+                blk[:have] = t[:have].view(np.int32)
+                blk[have:] = 0
+                ntok[row:row + k] = P
+                if have < k * P:  # the last restored block is a partial one
+                    ntok[row + k - 1] = have - (k - 1) * P
+                    used = -(-(have - (k - 1) * P) // (P // self.ppb))  # pages holding its tokens
+                    tab[:, (row + k - 1) * self.ppb + used:(row + k) * self.ppb] = -1
+                row += k
             self.copy_stream.wait_event(loaded)  # the load that last read this device set is done
             with torch.cuda.stream(self.copy_stream):
-                for k in ("ptrs", "lens", "keys", "pos", "tok"):
+                for k in ("ptrs", "lens", "keys", "pos", "tok", "ntok"):
                     d[k][:n].copy_(h[k][:n], non_blocking=True)
                 d["tab"][:G * m].copy_(h["tab"][:G * m], non_blocking=True)
             copied.record(self.copy_stream)
             self.stream.wait_event(copied)
-            blk = T.make_blocks(d["keys"][:n], d["pos"][:n], d["tok"][:n], d["tab"][:G * m])
+            blk = T.make_blocks(d["keys"][:n], d["pos"][:n], d["tok"][:n], d["tab"][:G * m],
+                                d["ntok"][:n] if self.tail else None)
             T.tl_load(ctx, self.stream, n, d["ptrs"][:n], d["lens"][:n], blk, self.pool.tl(), verd, self.ws,
                       self.ws_bytes)
             loaded.record(self.stream)

@@ -10,7 +10,7 @@ import workloads as wl
 from oracle import taliesin_ref as ref
 from paper_2609_39358_amd import taliesin as T
 from paper_2609_39358_amd.device import PagedCache, RecordStore
-from tests.gpu_case import DEV, Case, host_layers, i32, i64, log, random_fill
+from tests.gpu_case import DEV, FP as FP_, TEN as TEN_, Case, host_layers, i32, i64, log, random_fill
 
 pytestmark = pytest.mark.gpu
 
@@ -199,3 +199,95 @@ def test_random_layouts_with_tails(seed):
     got_k, got_v = host_layers(dst)
     for l in range(geom.n_layers):
         assert np.array_equal(got_k[l], hk0[l]) and np.array_equal(got_v[l], hv0[l])
+
+
+@pytest.mark.parametrize("name", ["one_page", "three_pages", "groups"])
+def test_host_pipeline_restores_partial_last_blocks(name):
+    """The host restore pipeline with tail=True. Three documents of four
+    blocks and a partial fifth are saved whole (the partial blocks with their
+    token counts) and indexed; the third document's partial block is damaged.
+    Requests: a whole document (five blocks reused, its partial one
+    included), a prefix ending inside its third block (its own partial key is
+    stored nowhere: two blocks), the document with the damaged partial block
+    (five, the last rejected), unknown tokens (none) and an exact three-block
+    prefix (three). Keys, hits, verdicts and every pool page equal the
+    oracle's restore of the same blocks into host copies of the pool."""
+    from paper_2609_39358_amd import pipeline
+    from tests.gpu_case import ctx_of, fill_cache, layout_of
+
+    geom = geom_of(name)
+    lay, ctx = layout_of(geom), ctx_of(geom)
+    ns = ref.namespace_digest(TEN_, FP_, lay)
+    B, P, ppb, G = lay.block_tokens, geom.page_tokens, geom.pages_per_block, geom.n_groups
+    docs = [wl.tokens(4 * B + r, 50, d) for d, r in enumerate((max(B // 2, 1), 1, B - 1))]
+    # save: block 5d + i is block i of document d
+    keys, bidx, toks, ntok = [], [], [], []
+    for d in docs:
+        k = ref.block_keys(ns, d.tobytes(), lay.block_bytes, tail=True)
+        assert len(k) == 5
+        assert [x.tobytes() for x in T.tl_block_keys(ctx, d, tail=True)] == k
+        for i in range(5):
+            row = np.zeros(B, np.uint32)
+            part = d[i * B:(i + 1) * B]
+            row[:part.size] = part
+            keys.append(k[i]), bidx.append(i), toks.append(row), ntok.append(part.size)
+    n = len(keys)
+    ntok = np.array(ntok, np.uint32)
+    src_pages = n * ppb + 3
+    src = fill_cache(PagedCache(geom.n_layers, src_pages, lay.slab_bytes, DEV), geom, seed=51)
+    t_src = np.tile(wl.page_table(n * ppb, src_pages, 52), (G, 1))
+    for b in range(n):  # pages a partial block holds no tokens on are left out
+        t_src[:, b * ppb + -(-int(ntok[b]) // P):(b + 1) * ppb] = -1
+    store = pipeline.Store(ctx, n, DEV)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    d_keys = torch.from_numpy(np.frombuffer(b"".join(keys), np.uint8).reshape(n, 32).copy()).to(DEV)
+    T.tl_save(ctx, torch.cuda.current_stream(), n, src.tl(),
+              T.make_blocks(d_keys, i64(bidx), i32(np.stack(toks).view(np.int32)), i32(t_src),
+                            i32(ntok.view(np.int32))), store.records.ptrs, st)
+    torch.cuda.synchronize()
+    hk, hv = host_layers(src)
+    recs, st_o = ref.save(lay, ns, hk, hv, t_src, keys, bidx, np.stack(toks), n_pages=src_pages, n_tokens=ntok)
+    assert [int(x) for x in st.cpu()] == st_o == [ref.ACCEPT] * n
+    for b in range(n):
+        assert store.records.buf[b].cpu().numpy().tobytes() == recs[b], b
+    # damage document 2's partial block in a byte of its first page's payload
+    bad = 14
+    off = lay.payload_offset + 37
+    store.records.buf[bad, off] ^= 0x01
+    recs[bad] = recs[bad][:off] + bytes([recs[bad][off] ^ 0x01]) + recs[bad][off + 1:]
+    store.add(np.frombuffer(b"".join(keys), np.uint8).reshape(n, 32), range(n))
+    # requests and the blocks each must reuse
+    reqs = [docs[0], docs[1][:2 * B + 3], docs[2], wl.tokens(3 * B, 53), docs[0][:3 * B]]
+    want_hits = [5, 2, 5, 0, 3]
+    cap = sum(want_hits) + 2
+    pool = random_fill(PagedCache(geom.n_layers, cap * ppb, lay.slab_bytes, DEV), 54)
+    pk, pv = host_layers(pool)
+    res = pipeline.RestorePipeline(store, pool, tail=True).restore(reqs, list(range(len(reqs))))
+    torch.cuda.synchronize()
+    assert res.hits == want_hits
+    for q, k in zip(reqs, res.keys):
+        assert [x.tobytes() for x in k] == ref.block_keys(ns, q.tobytes(), lay.block_bytes, tail=True)
+    # the oracle restores the same blocks: block j of the batch onto pool
+    # pages j*ppb.., the pages a partial block holds no tokens on left alone
+    o_recs, o_keys, o_bidx, o_toks, o_ntok = [], [], [], [], []
+    for r, (q, h) in enumerate(zip(reqs, want_hits)):
+        for i in range(h):
+            slot = [b for b in range(n) if keys[b] == ref.block_keys(ns, q.tobytes(), lay.block_bytes,
+                                                                    tail=True)[i]]
+            assert len(slot) == 1
+            o_recs.append(recs[slot[0]]), o_keys.append(keys[slot[0]]), o_bidx.append(i)
+            part = q[i * B:(i + 1) * B]
+            row = np.zeros(B, np.uint32)
+            row[:part.size] = part
+            o_toks.append(row), o_ntok.append(part.size)
+    m = len(o_recs)
+    assert list(res.record_ids) == [keys.index(k) for k in o_keys]
+    t_dst = np.tile(np.arange(m * ppb, dtype=np.int32), (G, 1))
+    for j in range(m):
+        t_dst[:, j * ppb + -(-o_ntok[j] // P):(j + 1) * ppb] = -1
+    vo = ref.restore(lay, ns, o_recs, o_keys, o_bidx, np.stack(o_toks), t_dst, pk, pv, n_tokens=o_ntok)
+    assert [int(x) for x in res.verdicts.cpu()] == vo
+    assert vo.count(ref.ACCEPT) == m - 1 and vo[11] != ref.ACCEPT  # the damaged partial block (request 2's fifth)
+    gk, gv = host_layers(pool)
+    for l in range(geom.n_layers):
+        assert np.array_equal(gk[l], pk[l]) and np.array_equal(gv[l], pv[l]), l
