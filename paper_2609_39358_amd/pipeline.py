@@ -322,10 +322,11 @@ class FileRestore:
         self.ws = [torch.empty(max(self.ws_bytes, 4), dtype=torch.uint8, device=dev) for _ in range(2)]
         self.dev = dev
 
-    def restore(self, record_ids, d_keys, d_positions, d_tokens, d_tables) -> torch.Tensor:
+    def restore(self, record_ids, d_keys, d_positions, d_tokens, d_tables, d_n_tokens=None) -> torch.Tensor:
         """Record record_ids[b] restores block b (keys [n][32], positions [n],
-        tokens [n][block tokens] or None, tables [n_groups][n * ppb]; device).
-        Returns the device verdicts [n] (valid after the stream syncs)."""
+        tokens [n][block tokens] or None, tables [n_groups][n * ppb], token
+        counts [n] (u32; partial last blocks) or None; device). Returns the
+        device verdicts [n] (valid after the stream syncs)."""
         ids = np.asarray(record_ids, dtype=np.uint64)
         n, B, ppb = ids.size, self.batch, self.ctx.pages_per_block
         with _on(self.stream):
@@ -338,7 +339,7 @@ class FileRestore:
                 k = i & 1
                 tabs = d_tables[:, lo * ppb:hi * ppb].contiguous()
                 blk = T.make_blocks(d_keys[lo:hi], d_positions[lo:hi], None if d_tokens is None else d_tokens[lo:hi],
-                                    tabs)
+                                    tabs, None if d_n_tokens is None else d_n_tokens[lo:hi])
                 keep.append((tabs, blk))
                 T.tl_load(self.ctx, self.stream, hi - lo, self.ptrs[k], self.lens, blk, self.pool.tl(), verd[lo:hi],
                           self.ws[k], self.ws_bytes)

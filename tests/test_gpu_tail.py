@@ -291,3 +291,60 @@ def test_host_pipeline_restores_partial_last_blocks(name):
     gk, gv = host_layers(pool)
     for l in range(geom.n_layers):
         assert np.array_equal(gk[l], pk[l]) and np.array_equal(gv[l], pv[l]), l
+
+
+def test_file_restore_of_partial_blocks(tmp_path):
+    """Records with partial blocks written to a record file in reverse order
+    and restored through FileRestore in batches of 6 with their token counts
+    (one partial block damaged on disk); then the same file restored with
+    every block taken as full, which refuses each partial one as HEADER.
+    Verdicts and every destination page equal the oracle's restore."""
+    from paper_2609_39358_amd import pipeline
+    geom = geom_of("three_pages")
+    n = 20
+    c = Case(geom, n, 64, 64, seed=60)
+    c.make_src()
+    bt = c.lay.block_tokens
+    n_tok = counts(bt, n, 61)
+    d_ntok = i32(n_tok.view(np.int32))
+    t_src = tail_tables(c, c.t_src, n_tok)
+    t_dst = tail_tables(c, c.t_dst, n_tok)
+    store = RecordStore(n, c.lay.record_bytes, DEV)
+    st = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    T.tl_save(c.ctx, torch.cuda.current_stream(), n, c.src.tl(),
+              T.make_blocks(c.d_keys, c.d_bidx, c.d_tokens, i32(t_src), d_ntok), store.ptrs, st)
+    torch.cuda.synchronize()
+    hk, hv = host_layers(c.src)
+    recs, st_o = ref.save(c.lay, c.ns, hk, hv, t_src, [k.tobytes() for k in c.keys], c.bidx, c.tokens,
+                          n_pages=64, n_tokens=n_tok)
+    assert [int(x) for x in st.cpu()] == st_o == [ref.ACCEPT] * n
+    rb = c.lay.record_bytes
+    f = T.RecordFile(str(tmp_path / "tails.bin"), rb, create=True, n_threads=4)
+    f.write(np.arange(n)[::-1], store.buf.cpu().numpy())  # block b is record n-1-b of the file
+    tb = int(np.nonzero(n_tok < bt)[0][0])
+    one = np.zeros((1, rb), np.uint8)
+    f.read([n - 1 - tb], one)
+    one[0, c.lay.payload_offset + 3] ^= 0x08
+    f.write([n - 1 - tb], one)
+    recs = [bytearray(r) for r in recs]
+    recs[tb][c.lay.payload_offset + 3] ^= 0x08
+    recs = [bytes(r) for r in recs]
+    f.drop_cache()
+    keys = [k.tobytes() for k in c.keys]
+    for label, counts_in in (("with counts", n_tok), ("as full blocks", None)):
+        dst = random_fill(PagedCache(geom.n_layers, 64, c.stride, DEV), 62)
+        hk0, hv0 = host_layers(dst)
+        fr = pipeline.FileRestore(c.ctx, f, dst, batch=6)  # 20 blocks: three full batches and a ragged one
+        v = fr.restore(np.arange(n)[::-1], c.d_keys, c.d_bidx, c.d_tokens, i32(t_dst),
+                       None if counts_in is None else d_ntok).cpu().numpy()
+        vo = ref.restore(c.lay, c.ns, recs, keys, c.bidx, c.tokens, t_dst, hk0, hv0, n_pages=64,
+                         n_tokens=counts_in)
+        assert [int(x) for x in v] == vo, label
+        if counts_in is None:
+            assert all(vo[b] == ref.HEADER for b in range(n) if n_tok[b] < bt)
+        else:
+            assert vo[tb] == ref.SEGMENT and vo.count(ref.ACCEPT) == n - 1
+        gk, gv = host_layers(dst)
+        for l in range(geom.n_layers):
+            assert np.array_equal(gk[l], hk0[l]) and np.array_equal(gv[l], hv0[l]), (label, l)
+    f.close()
