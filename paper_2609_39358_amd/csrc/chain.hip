@@ -29,6 +29,8 @@
 // publish (the winner writes the handle and clears the writer word).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "internal.h"
 
 namespace {
@@ -748,8 +750,10 @@ __device__ __forceinline__ bool stage_hit(const StageArgs& a, uint64_t slot, uin
   return *h < a.n_handles;
 }
 
-// One workgroup of kStageThreads per chain; its threads stride over the
-// chain's slots, token ids and table entries.
+// Workgroups of kStageThreads: blockIdx.x strides over chains, and the
+// gridDim.y workgroups of a chain take equal contiguous parts of its slots
+// (with their token ids and table entries), so that a few long chains still
+// spread over many compute units.
 constexpr uint32_t kStageThreads = 256;
 
 __global__ __launch_bounds__(kStageThreads) void k_chain_stage(StageArgs a) {
@@ -759,7 +763,9 @@ __global__ __launch_bounds__(kStageThreads) void k_chain_stage(StageArgs a) {
     const uint64_t hits_raw = a.hits[c];
     const uint64_t hits = hits_raw < r.n ? hits_raw : r.n;
     const uint64_t first = a.first_block ? a.first_block[c] : 0;
-    for (uint64_t k = tid; k < r.slots; k += kStageThreads) {
+    // this workgroup's slots [k0, k1) of the chain's r.slots
+    const uint64_t k0 = r.slots * blockIdx.y / gridDim.y, k1 = r.slots * (blockIdx.y + 1) / gridDim.y;
+    for (uint64_t k = k0 + tid; k < k1; k += kStageThreads) {
       const uint64_t q = r.s0 + k;
       uint64_t h = 0;
       const bool hit = stage_hit(a, q, k, hits, &h);
@@ -769,16 +775,16 @@ __global__ __launch_bounds__(kStageThreads) void k_chain_stage(StageArgs a) {
       if (a.n_tokens_out) a.n_tokens_out[q] = k == r.full && r.tail_tok ? r.tail_tok : a.bt;
     }
     if (a.tokens_out) {
-      const uint64_t n_tok = r.slots * a.bt, have = r.full * a.bt + r.tail_tok;
+      const uint64_t have = r.full * a.bt + r.tail_tok;
       uint32_t* dst = a.tokens_out + r.s0 * a.bt;
       const uint32_t* src = a.tokens + r.t0;
-      for (uint64_t e = tid; e < n_tok; e += kStageThreads) dst[e] = e < have ? src[e] : 0;
+      for (uint64_t e = k0 * a.bt + tid; e < k1 * a.bt; e += kStageThreads) dst[e] = e < have ? src[e] : 0;
     }
     if (a.tables_out) {
-      const uint64_t per = r.slots * a.ppb, row = a.n_slots * a.ppb;
+      const uint64_t row = a.n_slots * a.ppb;
       // a restored partial block restores only the pages holding its tokens
       const uint64_t tail_pages = (r.tail_tok + a.page_tokens - 1) / a.page_tokens;
-      for (uint64_t e = tid; e < per; e += kStageThreads) {
+      for (uint64_t e = k0 * a.ppb + tid; e < k1 * a.ppb; e += kStageThreads) {
         const uint64_t k = e / a.ppb, j = e - k * a.ppb, at = r.s0 * a.ppb + e;
         uint64_t h = 0;
         const bool hit = stage_hit(a, r.s0 + k, k, hits, &h) && !(r.tail_tok && k == r.full && j >= tail_pages);
@@ -1015,9 +1021,16 @@ int launch_stage(const tl_ctx* ctx, void* stream, size_t n_chains, const tl_chai
   a.tables_in = d_tables_in;
   a.tables_out = d_tables_out;
   (void)hipGetLastError();
+  // Few chains for the device: split each chain's slots over up to 64
+  // workgroups of about 512 slots (one chain of 6,062 slots: 11 workgroups).
+  uint32_t parts = 1;
+  if (n_chains && n_chains < 256) {
+    const uint64_t per_chain = (ch->n_slots + n_chains - 1) / n_chains;
+    parts = (uint32_t)std::min<uint64_t>(std::max<uint64_t>(per_chain / 512, 1), 64);
+  }
   {
     TimedLaunch t(TL_KERNEL_STAGE, stream);
-    hipLaunchKernelGGL(k_chain_stage, dim3(grid_for(n_chains, 1, 1u << 16)), dim3(kStageThreads), 0, s, a);
+    hipLaunchKernelGGL(k_chain_stage, dim3(grid_for(n_chains, 1, 1u << 16), parts), dim3(kStageThreads), 0, s, a);
   }
   return launched();
 }
